@@ -1,0 +1,413 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix (no GPU).
+
+Each test names the passage or property it checks.  None of the expected values comes from the HIP
+library; worked values live under tests/golden/ with their citations.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy.special import erf
+
+from oracle import dispatch as od
+from oracle import dit as od_dit
+from paper_2607_04461_amd import synth
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------- activation proxy (Eq. 3-5)
+
+@pytest.mark.parametrize("case", _gold("taylor_worked.json")["cases"], ids=lambda c: c["note"][:30])
+def test_taylor_worked_examples(case):
+    entries = [(np.array([h]), tau) for h, tau in zip(case["h"], case["tau"])]
+    got = od_dit.taylor_proxy(entries, case["t_cur"], case["order"])[0]
+    assert got == pytest.approx(case["expect"], abs=1e-12)
+
+
+def test_taylor_constant_is_exact():
+    rng = np.random.default_rng(0)
+    c = rng.standard_normal((5, 7))
+    for order in (0, 1, 2):
+        entries = [(c, 0.4), (c, 0.55), (c, 0.9)]
+        assert np.array_equal(od_dit.taylor_proxy(entries, 0.3, order), c)
+
+
+def test_taylor_linear_equal_spacing_exact():
+    # h(tau) = a + b tau is reproduced exactly by orders 1 and 2 when the cached steps are equally spaced
+    rng = np.random.default_rng(1)
+    a, b = rng.standard_normal(11), rng.standard_normal(11)
+    taus = [0.5, 0.625, 0.75]
+    entries = [(a + b * t, t) for t in taus]
+    for order in (1, 2):
+        np.testing.assert_allclose(od_dit.taylor_proxy(entries, 0.375, order), a + b * 0.375,
+                                   rtol=0, atol=1e-13)
+
+
+def test_taylor_linear_any_spacing_order1_exact():
+    rng = np.random.default_rng(2)
+    a, b = rng.standard_normal(4), rng.standard_normal(4)
+    entries = [(a + b * 0.41, 0.41), (a + b * 0.7, 0.7)]
+    np.testing.assert_allclose(od_dit.taylor_proxy(entries, 0.2, 1), a + b * 0.2, atol=1e-13)
+
+
+def test_taylor_equal_spacing_coefficients():
+    # with Delta = tau_1 - tau_2 the printed expansion collapses to 2.5 h1 - 2 h2 + 0.5 h3
+    rng = np.random.default_rng(3)
+    h1, h2, h3 = rng.standard_normal((3, 9))
+    entries = [(h1, 0.25), (h2, 0.5), (h3, 0.75)]
+    np.testing.assert_allclose(od_dit.taylor_proxy(entries, 0.0, 2), 2.5 * h1 - 2 * h2 + 0.5 * h3,
+                               atol=1e-13)
+
+
+def test_taylor_quadratic_is_not_newton():
+    # Eq. 4 scales the second difference by (tau_1 - tau_2)^2 and Eq. 5 uses Delta^2/2, which is not
+    # exact for a quadratic (Newton extrapolation would give 3 h1 - 3 h2 + h3): pins "as printed".
+    taus = [0.5, 0.6, 0.7]
+    h = [t * t for t in taus]
+    entries = [(np.array([hv]), t) for hv, t in zip(h, taus)]
+    got = od_dit.taylor_proxy(entries, 0.4, 2)[0]
+    assert got == pytest.approx(2.5 * h[0] - 2 * h[1] + 0.5 * h[2], abs=1e-14)
+    assert abs(got - 0.4 ** 2) > 1e-4
+
+
+def test_taylor_affine_time_invariance():
+    rng = np.random.default_rng(4)
+    hs = rng.standard_normal((3, 6))
+    taus, t = [0.31, 0.52, 0.88], 0.12
+    base = od_dit.taylor_proxy(list(zip(hs, taus)), t, 2)
+    for alpha, beta in [(1000.0, 0.0), (2.5, -3.0), (0.01, 7.0)]:
+        scaled = od_dit.taylor_proxy(list(zip(hs, [alpha * x + beta for x in taus])), alpha * t + beta, 2)
+        np.testing.assert_allclose(scaled, base, rtol=1e-9, atol=1e-9)
+
+
+# ---------------------------------------------------------------- attention
+
+def _brute_attention(q, k, v):
+    Tq, d = q.shape
+    out = np.zeros((Tq, v.shape[1]))
+    for i in range(Tq):
+        w = [math.exp(sum(q[i, c] * k[j, c] for c in range(d)) / math.sqrt(d)) for j in range(k.shape[0])]
+        z = sum(w)
+        for j in range(k.shape[0]):
+            out[i] += (w[j] / z) * v[j]
+    return out
+
+
+@pytest.mark.parametrize("tq,tk,d", [(1, 1, 4), (5, 7, 8), (16, 3, 16), (9, 16, 2)])
+def test_attention_brute_force(tq, tk, d):
+    rng = np.random.default_rng(tq * 100 + tk)
+    q, k, v = rng.standard_normal((tq, d)), rng.standard_normal((tk, d)), rng.standard_normal((tk, d + 1))
+    np.testing.assert_allclose(od_dit.attention(q, k, v), _brute_attention(q, k, v), rtol=1e-12, atol=1e-12)
+
+
+def test_attention_identical_keys_average_values():
+    rng = np.random.default_rng(5)
+    q = rng.standard_normal((4, 8))
+    k = np.tile(rng.standard_normal((1, 8)), (6, 1))
+    v = rng.standard_normal((6, 8))
+    np.testing.assert_allclose(od_dit.attention(q, k, v), np.tile(v.mean(0), (4, 1)), atol=1e-14)
+
+
+def test_attention_is_not_transposed():
+    # keys with a dominant match route each query to exactly one value row
+    d = 4
+    k = 60.0 * np.eye(d)
+    v = np.arange(d * 3, dtype=float).reshape(d, 3)
+    q = np.eye(d)[[2, 0, 3]]
+    np.testing.assert_allclose(od_dit.attention(q, k, v), v[[2, 0, 3]], atol=1e-10)
+
+
+def test_multi_head_split_columns():
+    rng = np.random.default_rng(6)
+    q, k, v = rng.standard_normal((5, 12)), rng.standard_normal((7, 12)), rng.standard_normal((7, 12))
+    out = od_dit.multi_head_attention(q, k, v, 3)
+    for h in range(3):
+        sl = slice(4 * h, 4 * h + 4)
+        np.testing.assert_allclose(out[:, sl], _brute_attention(q[:, sl], k[:, sl], v[:, sl]), atol=1e-12)
+
+
+# ---------------------------------------------------------------- elementary ops (textbook)
+
+def test_gelu_tanh_close_to_erf_gelu():
+    x = np.linspace(-8, 8, 4001)
+    exact = 0.5 * x * (1 + erf(x / math.sqrt(2)))
+    dev = np.abs(od_dit.gelu_tanh(x) - exact)
+    assert dev.max() < 5e-4            # the tanh approximation's known small deviation
+    assert dev.max() > 1e-6            # ... and it is the tanh form, not erf itself
+    assert od_dit.gelu_tanh(np.array([0.0]))[0] == 0.0
+
+
+def test_silu_textbook():
+    x = np.array([-3.0, 0.0, 0.5, 4.0])
+    np.testing.assert_allclose(od_dit.silu(x), x * (0.5 + 0.5 * np.tanh(x / 2)), atol=1e-15)
+
+
+def test_layer_norm_hand_example():
+    x = np.array([[1.0, 2.0, 3.0, 4.0]])
+    # mean 2.5, biased variance 1.25
+    expect = np.array([-1.5, -0.5, 0.5, 1.5]) / math.sqrt(1.25 + 1e-6)
+    np.testing.assert_allclose(od_dit.layer_norm(x, 1e-6), expect[None], atol=1e-14)
+
+
+def test_layer_norm_invariants():
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((6, 33)) * 5 + 3
+    y = od_dit.layer_norm(x, 0.0)
+    np.testing.assert_allclose(y.mean(-1), 0, atol=1e-13)
+    np.testing.assert_allclose(y.var(-1), 1, atol=1e-12)
+    np.testing.assert_allclose(od_dit.layer_norm(7 * x - 2, 0.0), y, atol=1e-12)
+
+
+def test_timestep_features():
+    half = 32
+    f0 = od_dit.timestep_features(0.0, 2 * half)
+    assert np.array_equal(f0, np.concatenate([np.ones(half), np.zeros(half)]))
+    f = od_dit.timestep_features(0.37, 2 * half)
+    np.testing.assert_allclose(f[:half] ** 2 + f[half:] ** 2, 1.0, atol=1e-14)
+    assert f[0] == pytest.approx(math.cos(370.0), abs=1e-12)       # first frequency is 1
+    assert f[half] == pytest.approx(math.sin(370.0), abs=1e-12)
+    # geometric frequencies 10000^(-j/half): at tiny t, sin(x) ~ x gives the ratio of neighbours
+    g = od_dit.timestep_features(1e-9, 2 * half)
+    ratios = g[half + 1:] / g[half:-1]
+    np.testing.assert_allclose(ratios, 10000.0 ** (-1.0 / half), rtol=1e-9)
+    assert g[2 * half - 1] / g[half] == pytest.approx(1e-4 ** ((half - 1) / half), rel=1e-9)
+
+
+def test_linear_orientation():
+    x = np.array([[1.0, 2.0, 3.0]])
+    w = np.array([[1.0, 0.0, 0.0], [0.0, 0.0, 2.0]])        # [out=2, in=3]
+    np.testing.assert_allclose(od_dit.linear(x, w, np.array([10.0, 20.0])), [[11.0, 26.0]])
+
+
+# ---------------------------------------------------------------- patchify / Euler
+
+def test_patchify_golden():
+    g = _gold("patchify_4x4.json")
+    z = (4 * np.arange(4)[:, None] + np.arange(4)[None, :]).astype(float)[None]
+    assert np.array_equal(od_dit.patchify(z, 2), np.array(g["latent_1x4x4"]["tokens"], float))
+    c, y, x = np.meshgrid(np.arange(2), np.arange(2), np.arange(2), indexing="ij")
+    z2 = (100 * c + 10 * y + x).astype(float)
+    assert np.array_equal(od_dit.patchify(z2, 2), np.array(g["latent_2x2x2"]["tokens"], float))
+
+
+def test_unpatchify_inverts_patchify():
+    z = np.random.default_rng(8).standard_normal((16, 6, 10))
+    assert np.array_equal(od_dit.unpatchify(od_dit.patchify(z, 2), 16, 6, 10, 2), z)
+
+
+def _tiny_weights(seed=1234, shape=synth.TINY):
+    _, W = synth.make_weights(shape, seed)
+    return {k: v.copy() for k, v in W.items()}
+
+
+def test_euler_closed_form():
+    # App. A.1 Eq. 20 with a = 0 is z + v dt.  A head with W_h = 0 makes v = unpatchify(b_h).
+    s = synth.TINY
+    W = _tiny_weights()
+    W["head_w"][:] = 0.0
+    W["head_b"][:] = np.arange(s.patch_dim, dtype=np.float32) * 0.25 - 3.0
+    z = synth.make_latents(2, 16, 8, 8)
+    text = synth.make_text(1, 8, 32)
+    kv = od_dit.prepare_text(W, s, text)
+    out = od_dit.refine_step(W, s, z, 0.75, 0.5, kv, np.zeros(2, np.int32))
+    expect = np.empty_like(out)
+    for n in range(2):
+        for c in range(16):
+            for y in range(8):
+                for x in range(8):
+                    b = W["head_b"][c * 4 + 2 * (y % 2) + (x % 2)]
+                    expect[n, c, y, x] = float(z[n, c, y, x]) + (0.5 - 0.75) * float(b)
+    np.testing.assert_allclose(out, expect, rtol=0, atol=1e-15)
+
+
+# ---------------------------------------------------------------- step-level invariants
+
+def _tiny_setup():
+    wl = synth.WORKLOADS["tiny"]
+    W = _tiny_weights(wl.seed_w)
+    z = synth.make_latents(wl.n, 16, wl.latent_h, wl.latent_w)
+    text = synth.make_text(wl.n_cond, wl.text_len, wl.shape.text_dim)
+    return wl, W, z, text
+
+
+def test_skip_is_identity_on_residual_stream():
+    wl, W, z, text = _tiny_setup()
+    kv = od_dit.prepare_text(W, wl.shape, text)
+    cache = od_dit.PoolCache(2)
+    hidden = {}
+    skip = np.array([0, 1], np.uint8)
+    od_dit.draft_step(W, wl.shape, z, 1.0, 0.75, kv, wl.cond_index(), skip, np.zeros(2, np.uint8),
+                      cache, hidden=hidden)
+    for n in range(wl.n):
+        h = hidden[n]               # after embed, after block 0, after block 1
+        assert np.array_equal(h[2], h[1])
+        assert not np.array_equal(h[1], h[0])
+
+
+def test_zero_branch_model_any_skip_mask_bit_identical():
+    wl, W, z, text = _tiny_setup()
+    for l in range(2):
+        for nm in ("wo", "bo", "woc", "boc", "w2", "b2"):
+            W[f"blk{l}.{nm}"][:] = 0.0
+    kv = od_dit.prepare_text(W, wl.shape, text)
+    outs = []
+    for skip in ([0, 0], [1, 0], [0, 1], [1, 1]):
+        o, _ = od_dit.draft_step(W, wl.shape, z, 1.0, 0.75, kv, wl.cond_index(), np.array(skip, np.uint8),
+                                 np.zeros(2, np.uint8), od_dit.PoolCache(2))
+        outs.append(o)
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+def test_empty_masks_equal_full_step():
+    wl, W, z, text = _tiny_setup()
+    kv = od_dit.prepare_text(W, wl.shape, text)
+    zeros = np.zeros(2, np.uint8)
+    a, tr = od_dit.draft_step(W, wl.shape, z, 0.75, 0.5, kv, wl.cond_index(), zeros, zeros, od_dit.PoolCache(2))
+    b = od_dit.refine_step(W, wl.shape, z, 0.75, 0.5, kv, wl.cond_index())
+    assert np.array_equal(a, b)
+    assert all(e[0] == od.COMPUTE for e in tr)
+
+
+def test_candidate_permutation_invariance():
+    wl, W, z, text = _tiny_setup()
+    text2 = synth.make_text(2, wl.text_len, wl.shape.text_dim)
+    z4 = np.concatenate([z, synth.make_latents(2, 16, 8, 8, first_seed=500)])
+    cond = np.array([0, 1, 1, 0], np.int32)
+    perm = np.array([2, 0, 3, 1])
+    sched = wl.schedule()
+
+    def run(zz, cc):
+        out, _, traces = od_dit.run_draft(W, wl.shape, zz, sched, 4, wl.masks, text2, cc)
+        return out, traces
+
+    a, ta = run(z4, cond)
+    b, tb = run(z4[perm], cond[perm])
+    assert np.array_equal(b, a[perm])
+    assert ta == tb
+
+
+def test_truncation_is_prefix_and_resume_is_markov():
+    wl, W, z, text = _tiny_setup()
+    sched = wl.schedule()
+    cond = wl.cond_index()
+    seen = {}
+    full, _, _ = od_dit.run_draft(W, wl.shape, z, sched, 4, wl.masks, text, cond,
+                                  on_step=lambda k, zz: seen.__setitem__(k, zz.copy()))
+    short, _, _ = od_dit.run_draft(W, wl.shape, z, sched, 2, wl.masks, text, cond)
+    assert np.array_equal(short, seen[1])
+    # resume: knobs-off trajectory split at step 2 equals the uninterrupted one (Sec. 4.2 Stage 3)
+    whole = od_dit.run_refine(W, wl.shape, z, sched, 0, text, cond)
+    zero = lambda k: (np.zeros(2, np.uint8), np.zeros(2, np.uint8))
+    head, _, _ = od_dit.run_draft(W, wl.shape, z, sched, 2, zero, text, cond)
+    tail = od_dit.run_refine(W, wl.shape, head, sched, 2, text, cond)
+    assert np.array_equal(tail, whole)
+
+
+def test_proxy_step_uses_cached_outputs():
+    # at the tiny workload's step 3, block 0 is an order-2 proxy over steps 0,1,2 and block 1 is
+    # skipped: the residual stream entering the head must be 2.5 h(t2) - 2 h(t1) + 0.5 h(t0)
+    wl, W, z, text = _tiny_setup()
+    kv = od_dit.prepare_text(W, wl.shape, text)
+    cache = od_dit.PoolCache(2)
+    sched = wl.schedule()
+    hist = []
+    zz = z
+    for k in range(4):
+        hidden = {}
+        skip, proxy = wl.masks(k)
+        zz, _ = od_dit.draft_step(W, wl.shape, zz, sched[k], sched[k + 1], kv, wl.cond_index(), skip,
+                                  proxy, cache, hidden=hidden)
+        hist.append(hidden)
+    for n in range(wl.n):
+        h0, h1, h2 = (hist[k][n][1] for k in (0, 1, 2))
+        np.testing.assert_allclose(hist[3][n][1], 2.5 * h2 - 2 * h1 + 0.5 * h0, rtol=1e-12, atol=1e-12)
+        assert np.array_equal(hist[3][n][2], hist[3][n][1])
+
+
+def test_modulation_slot_order():
+    # with the shared modulation zeroed, block l's six vectors are its table rows: shift1, scale1,
+    # gate1, shift2, scale2, gate2.  Zero the attention branches and set scale2 = -1 so the MLP sees
+    # only shift2; the block must then add gate2 * (gelu(W1 shift2 + b1) W2^T + b2) to every token.
+    wl, W, z, text = _tiny_setup()
+    s = wl.shape
+    W["mod_w"][:] = 0.0
+    W["mod_b"][:] = 0.0
+    rng = np.random.default_rng(9)
+    tab = rng.standard_normal((6, s.hidden)).astype(np.float32)
+    tab[4] = -1.0
+    tab[2] = 0.0
+    W["blk0.mod"][:] = tab
+    for nm in ("woc", "boc"):
+        W[f"blk0.{nm}"][:] = 0.0
+    bm, _ = od_dit.modulations(W, 2, s.freq_dim, 0.6)
+    np.testing.assert_array_equal(bm[0], tab.astype(np.float64))
+    h = rng.standard_normal((16, s.hidden))
+    kv = od_dit.prepare_text(W, s, text)[0]
+    out = od_dit.block_forward(W, 0, h, bm[0], kv[0], s.heads, s.ln_eps)
+    mlp = od_dit.gelu_tanh(tab[3].astype(float) @ W["blk0.w1"].T.astype(float) + W["blk0.b1"]) \
+        @ W["blk0.w2"].T.astype(float) + W["blk0.b2"]
+    np.testing.assert_allclose(out - h, np.tile(tab[5] * mlp, (16, 1)), rtol=1e-10, atol=1e-12)
+
+
+# ---------------------------------------------------------------- dispatch
+
+@pytest.mark.parametrize("name", ["tiny", "mid"])
+def test_dispatch_golden_traces(name):
+    g = _gold("dispatch_traces.json")
+    wl = synth.WORKLOADS[name]
+    L = wl.shape.num_blocks
+    meta = od.empty_meta(L)
+    sched = wl.schedule()
+    for k, expect in enumerate(g[name]):
+        skip, proxy = wl.masks(k)
+        trace, meta = od.plan_step(skip, proxy, meta, sched[k])
+        assert [list(e) for e in trace] == expect, f"step {k}"
+        if name == "mid" and k + 1 in (5, 7):
+            # cached timesteps of block 2 seen by the next step's proxy, most recent first
+            want = g[f"mid_block2_cached_steps_at_step{k + 1}"]
+            got = [meta[2]["t"][s] for s in od.recent_slots(meta[2])]
+            assert got == [float(sched[j]) for j in want]
+
+
+@pytest.mark.parametrize("case", _gold("phi_star.json")["cases"], ids=lambda c: c["model"][:24])
+def test_phi_star_block_evaluations(case):
+    L = case["L"]
+    phi = tuple(case["phi"])
+    meta = od.empty_meta(L)
+    evals = 0
+    compute_steps = 0
+    for k in range(phi[0]):
+        skip, proxy = od.masks_from_phi(phi, L, k)
+        if k >= phi[1]:
+            assert list(np.nonzero(skip)[0]) == case["skip_blocks_0based"]
+        trace, meta = od.plan_step(skip, proxy, meta, 1.0 - k / 50)
+        n = sum(1 for e in trace if e[0] == od.COMPUTE)
+        evals += n
+        compute_steps += int(n > 0)
+    assert evals == case["compute_block_evals"]
+    assert compute_steps == case["compute_steps"]
+
+
+def test_dispatch_fallback_and_liveness():
+    meta = od.empty_meta(4)
+    ones = np.ones(4, np.uint8)
+    zeros = np.zeros(4, np.uint8)
+    tr, meta = od.plan_step(zeros, ones, meta, 1.0)          # empty cache: every proxy computes
+    assert [e[0] for e in tr] == [od.COMPUTE] * 4
+    # block 0's proxy is followed (after a skip) by a computed block: live; the last proxy is live
+    tr, meta2 = od.plan_step(np.array([0, 1, 0, 0], np.uint8), np.array([1, 1, 0, 1], np.uint8), meta, 0.9)
+    assert tr == [(od.PROXY, 0, 0, 1), (od.SKIP, -1, -1, 0), (od.COMPUTE, -1, 1, 1), (od.PROXY, 0, 0, 1)]
+    assert meta2[3] == meta[3] and meta2[2]["count"] == 2 and meta2[1] == meta[1]
+    # a proxy whose output is overwritten by the next proxy before anything reads it is dead
+    tr, _ = od.plan_step(zeros, np.array([1, 0, 1, 1], np.uint8), meta2, 0.8)
+    assert [e[3] for e in tr] == [1, 1, 0, 1]
+    assert tr[2] == (od.PROXY, 1, 1, 0)          # block 2 was computed at 1.0 and 0.9
