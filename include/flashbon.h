@@ -1,0 +1,187 @@
+/*
+ * flashbon.h -- C ABI of the MI355X (gfx950) batched draft-generation library for Flash-BoN
+ * (arXiv 2607.04461).
+ *
+ * The library runs one denoising step of a DiT over a pool of N candidates with the paper's three
+ * draft knobs (Sec. 4.1):
+ *   (1) timestep truncation   -- the caller loops over the first S' steps of the schedule (Eq. 2);
+ *   (2) activation proxies    -- a proxied block's output is the second-order Taylor forecast of
+ *                                Eq. 3-5 from that block's cached outputs;
+ *   (3) layer skipping        -- a skipped block is the identity on the residual stream (Eq. 6);
+ * a computed block is h = B_l(h, x, t) (Eq. 7).  The latent update is the flow-matching Euler step
+ * (App. A.1, Eq. 20 with a = 0): z <- z + (t_next - t_cur) v.  Refinement (Sec. 4.2 Stage 3,
+ * Eq. 13) is the same step with every knob off.
+ *
+ * Conventions shared by every call:
+ *   - Every call returns flashbon_status (0 = OK).  Validation errors return before any device
+ *     write and before any change to host-side state (meta, trace, text_kv_valid).  A HIP failure
+ *     returns FLASHBON_EHIP; the device state of the caller's buffers is then undefined and the
+ *     caller must re-zero `meta` and `text_kv_valid`.  flashbon_last_error() describes the last
+ *     failure of the calling thread.  Nothing throws or aborts across this boundary.
+ *   - "device" pointers are HIP device allocations on the current device; "host" pointers are
+ *     ordinary host memory.  The caller owns every buffer it passes; the library owns only the
+ *     model (weights + workspace).  The library keeps no pointer to caller buffers after a call
+ *     returns, except that work enqueued on `stream` keeps reading/writing them until it completes.
+ *   - Device work is enqueued on `stream` (a hipStream_t passed as void*; NULL = default stream) and
+ *     the call returns without synchronising.  Host outputs (trace, meta, text_kv_valid) are final
+ *     at return, since dispatch is decided on the host.
+ *   - Calls on one model must be serialised (the workspace is shared); overlapping calls race.
+ *   - Row-major layouts throughout; tensors are dense (no padding between rows).
+ */
+#ifndef FLASHBON_H
+#define FLASHBON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FLASHBON_OK = 0,
+  FLASHBON_EINVAL = -1, /* NULL where a pointer is required, bad enum, non-finite or unordered t */
+  FLASHBON_ESHAPE = -2, /* a size is zero/negative, inconsistent, or above the configured maxima */
+  FLASHBON_ENOMEM = -3, /* a device or pinned-host allocation failed (init only) */
+  FLASHBON_EHIP = -4,   /* a HIP runtime call or kernel launch failed */
+  FLASHBON_ESTATE = -5  /* cache metadata out of range (count > 3, head > 2, ...) */
+} flashbon_status;
+
+typedef enum {
+  FLASHBON_FP32 = 0, /* all GEMM operands, attention and activations in fp32 */
+  FLASHBON_BF16 = 1  /* bf16 GEMM/attention operands with fp32 accumulation; residual stream,
+                        cache, latents and normalisation statistics stay fp32 */
+} flashbon_dtype;
+
+/* Model shape.  The DiT block is a Wan-shaped block (the paper does not describe one):
+ *   a = LN(h)(1+scale1)+shift1; h += gate1 * SelfAttn(a)
+ *   c = LN(h);                  h += CrossAttn(c, text)
+ *   a = LN(h)(1+scale2)+shift2; h += gate2 * MLP(a), MLP = W2 GELU_tanh(W1 a + b1) + b2
+ * LN is non-affine over `hidden`; head_dim = hidden / heads. */
+typedef struct {
+  int32_t num_blocks;      /* L */
+  int32_t hidden;          /* D */
+  int32_t heads;           /* H; hidden % heads == 0, head_dim <= 128 and a multiple of 8 */
+  int32_t mlp_hidden;      /* F */
+  int32_t latent_channels; /* C */
+  int32_t patch;           /* p (2): token = p x p patch of every channel */
+  int32_t freq_dim;        /* width of the sinusoidal timestep features (even) */
+  int32_t text_dim;        /* width of the text-conditioning tokens */
+  int32_t dtype;           /* flashbon_dtype */
+  float ln_eps;            /* LayerNorm epsilon (1e-6) */
+  int32_t max_n;           /* largest pool size a step may use */
+  int32_t max_tokens;      /* largest T = (latent_h/p)(latent_w/p) */
+  int32_t max_text_len;    /* largest text_len */
+  int32_t max_cond;        /* largest n_cond */
+} flashbon_model_config;
+
+/* Per-block activation-cache metadata, host side (one per block).  The cache of a block is a ring of
+ * three slots.  A computed block writes slot `head`, stores t_cur in t[head], advances
+ * head = (head+1) % 3 and saturates count at 3.  The most recent entry is slot (head+2) % 3, then
+ * (head+1) % 3, then head.  The caller zeroes it at the start of a pool. */
+typedef struct {
+  int32_t count; /* valid entries, 0..3 */
+  int32_t head;  /* next slot to write, 0..2 */
+  float t[3];    /* timestep of the entry in each slot */
+} flashbon_cache_meta;
+
+enum { FLASHBON_COMPUTE = 0, FLASHBON_SKIP = 1, FLASHBON_PROXY = 2 };
+
+/* What one block did at one step (bit-exact, host-decided):
+ *   COMPUTE: order -1, slot = cache slot written, live 1
+ *   SKIP   : order -1, slot -1, live 0
+ *   PROXY  : order 0..2 (Taylor order = min(count,3)-1), slot = most recent entry's slot,
+ *            live = 1 iff the next non-skipped block is computed or there is none (otherwise the
+ *            proxy's output would be overwritten unread, and nothing is launched for it). */
+typedef struct {
+  int8_t action;
+  int8_t order;
+  int8_t slot;
+  int8_t live;
+} flashbon_trace_entry;
+
+typedef struct {
+  int32_t n;        /* candidates in this call, 1..max_n */
+  int32_t latent_h; /* H, multiple of patch */
+  int32_t latent_w; /* W, multiple of patch; T = (H/p)(W/p) <= max_tokens */
+
+  float *latents; /* device [n, C, H, W] fp32: z_{t_cur} in, z_{t_next} out (in place) */
+  float t_cur;    /* current timestep t_k (host scalar from the caller's schedule) */
+  float t_next;   /* next timestep t_{k+1}; the update adds (t_next - t_cur) * v */
+
+  const float *text;         /* device [n_cond, text_len, text_dim] fp32 conditioning tokens */
+  int32_t n_cond;            /* prompts in the pool, 1..max_cond */
+  int32_t text_len;          /* tokens per prompt, 1..max_text_len */
+  const int32_t *cond_index; /* host [n]: prompt of each candidate, values in [0, n_cond) */
+  void *text_kv;             /* device scratch of flashbon_text_kv_bytes() bytes, caller-owned:
+                                per-block cross-attention K/V of every prompt */
+  int32_t *text_kv_valid;    /* host flag in/out: 0 -> the call first computes text_kv from `text`
+                                and sets it to 1; 1 -> text_kv is reused as is.  The caller resets it
+                                to 0 whenever `text` changes. */
+
+  const uint8_t *skip;  /* host [num_blocks]: 1 = skip block l at this step (draft only) */
+  const uint8_t *proxy; /* host [num_blocks]: 1 = proxy block l at this step (draft only);
+                           skip wins over proxy; a proxy with an empty cache computes */
+  float *cache;         /* device fp32 [num_blocks][3][n][T][hidden] (flashbon_cache_bytes());
+                           draft only: computed block outputs, proxy inputs */
+  flashbon_cache_meta *meta;   /* host [num_blocks] in/out (draft only) */
+  flashbon_trace_entry *trace; /* host [num_blocks] out, optional (NULL = not reported) */
+
+  float *hidden_dump; /* optional debug output, device fp32 [num_blocks+1][n][T][hidden]: the residual
+                         stream after the patch embedding (index 0) and after block l (index l+1).
+                         Entries whose value is never formed (a dead proxy, or the embedding when the
+                         first non-skipped block is a proxy) are left untouched.  NULL = off. */
+  void *stream;       /* hipStream_t */
+} flashbon_step_args;
+
+/* Number of floats `host_weights` must hold for `cfg`. Returns 0 if cfg is invalid. */
+size_t flashbon_weight_count(const flashbon_model_config *cfg);
+
+/* Create a model: validates cfg, allocates device weights (fp32 for small vectors and the timestep
+ * path, plus a bf16 copy of every matrix in BF16 mode) and a workspace sized for the maxima,
+ * copies `host_weights` (fp32, `n_weights` floats, packed as below) and synchronises.
+ * Packing order, every matrix [out][in] row-major:
+ *   t_w1[D][freq] t_b1[D] t_w2[D][D] t_b2[D] mod_w[6D][D] mod_b[6D] head_mod_w[2D][D] head_mod_b[2D]
+ *   pe_w[D][C p p] pe_b[D] txt_w[D][text_dim] txt_b[D]
+ *   per block l: mod[6][D] wq wk wv[D][D each] bq bk bv[D each] wo[D][D] bo[D] wqc[D][D] bqc[D]
+ *                wkc wvc[D][D each] bkc bvc[D each] woc[D][D] boc[D] w1[F][D] b1[F] w2[D][F] b2[D]
+ *   head_w[C p p][D] head_b[C p p]
+ * Timestep conditioning: f = [cos(1000 t w_j) | sin(1000 t w_j)], w_j = 10000^(-j/(freq/2));
+ * e = t_w2 SiLU(t_w1 f + t_b1) + t_b2; m = mod_w SiLU(e) + mod_b; block l uses m + mod_l split as
+ * (shift1, scale1, gate1, shift2, scale2, gate2); the head uses head_mod_w SiLU(e) + head_mod_b split
+ * as (shift, scale).  On success *out owns the model; free it with flashbon_free. */
+flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const float *host_weights,
+                                    size_t n_weights, void **out);
+
+/* Bytes of the caller-owned cross-attention K/V scratch for n_cond prompts of text_len tokens. */
+size_t flashbon_text_kv_bytes(const void *model, int32_t n_cond, int32_t text_len);
+
+/* Bytes of the caller-owned activation cache for n candidates of `tokens` tokens. */
+size_t flashbon_cache_bytes(const void *model, int32_t n, int32_t tokens);
+
+/* One draft step (Sec. 4.2 Stage 1, Eq. 8) over the pool with the step's skip/proxy masks: plans
+ * every block on the host (trace, meta), then enqueues the step.  Skipped blocks and dead proxies
+ * launch nothing. */
+flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args);
+
+/* One full-quality step (Sec. 4.2 Stage 3, Eq. 13): as flashbon_draft_step with every mask zero;
+ * skip, proxy, cache and meta are ignored (may be NULL).  trace, if given, reports all COMPUTE. */
+flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args);
+
+/* Release the model.  NULL is a no-op.  Synchronises the device before freeing. */
+void flashbon_free(void *model);
+
+/* Host-only dispatch of one step, as flashbon_draft_step performs it (Eq. 3-6 plus the cache
+ * ring): fills trace[num_blocks] and advances meta[num_blocks] in place.  No device work. */
+flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, const uint8_t *proxy,
+                                   flashbon_cache_meta *meta, float t_cur,
+                                   flashbon_trace_entry *trace);
+
+/* Description of the calling thread's last failure ("" if none).  Valid until the next call. */
+const char *flashbon_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHBON_H */

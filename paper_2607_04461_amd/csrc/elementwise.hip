@@ -1,0 +1,245 @@
+// HBM-bound kernels of the draft step: adaLN normalisation, the activation proxy (Eq. 3-5),
+// patchify, the timestep path and dtype conversion.
+#include "common.h"
+#include "kernels.h"
+
+namespace fb {
+
+// ------------------------------------------------------------------------------------------ adaLN
+// One wave per row; the row stays in registers between the two statistics passes (D <= 64*4*MAXV).
+constexpr int LN_MAXV = 24;  // float4 per lane -> D <= 6144
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_ln_mod(int M, int D, float eps, const float *__restrict__ x,
+                                                const float *__restrict__ shift,
+                                                const float *__restrict__ scale, T *__restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const float4 *xr = reinterpret_cast<const float4 *>(x + row * D);
+  const int nv = D >> 2;
+  float4 v[LN_MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i) {
+    int c = lane + i * 64;
+    if (c < nv) {
+      v[i] = xr[c];
+      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+  }
+  const float mean = wave_sum(s) / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i) {
+    int c = lane + i * 64;
+    if (c < nv) {
+      float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
+      q += (a * a + b * b) + (cc * cc + d * d);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+  T *orow = out + row * D;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; ++i) {
+    int c = lane + i * 64;
+    if (c < nv) {
+      float r[4] = {(v[i].x - mean) * rstd, (v[i].y - mean) * rstd, (v[i].z - mean) * rstd,
+                    (v[i].w - mean) * rstd};
+      if (shift) {
+        float4 sh = reinterpret_cast<const float4 *>(shift)[c];
+        float4 sc = reinterpret_cast<const float4 *>(scale)[c];
+        r[0] = r[0] * (1.0f + sc.x) + sh.x;
+        r[1] = r[1] * (1.0f + sc.y) + sh.y;
+        r[2] = r[2] * (1.0f + sc.z) + sh.z;
+        r[3] = r[3] * (1.0f + sc.w) + sh.w;
+      }
+      if constexpr (sizeof(T) == 4) {
+        reinterpret_cast<float4 *>(orow)[c] = make_float4(r[0], r[1], r[2], r[3]);
+      } else {
+        bf16x4 o4 = {(bf16)r[0], (bf16)r[1], (bf16)r[2], (bf16)r[3]};
+        reinterpret_cast<bf16x4 *>(orow)[c] = o4;
+      }
+    }
+  }
+}
+
+hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, const float *shift,
+                         const float *scale, void *out, hipStream_t s) {
+  dim3 grid((M + 3) / 4), block(256);
+  if (t == ACT_BF16)
+    hipLaunchKernelGGL(k_ln_mod<bf16>, grid, block, 0, s, M, D, eps, x, shift, scale, (bf16 *)out);
+  else
+    hipLaunchKernelGGL(k_ln_mod<float>, grid, block, 0, s, M, D, eps, x, shift, scale, (float *)out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------ activation proxy
+// Difference form h1 + ca (h1 - h2) + cb (h1 - 2 h2 + h3): a constant cache reproduces itself
+// exactly, whatever the coefficients.
+template <int ORDER>
+__global__ __launch_bounds__(256) void k_proxy(int64_t n4, const float4 *__restrict__ h1,
+                                               const float4 *__restrict__ h2,
+                                               const float4 *__restrict__ h3, float ca, float cb,
+                                               float4 *__restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float4 a = h1[i];
+    if constexpr (ORDER == 0) {
+      out[i] = a;
+    } else {
+      float4 b = h2[i];
+      float4 d1 = make_float4(a.x - b.x, a.y - b.y, a.z - b.z, a.w - b.w);
+      float4 r = make_float4(a.x + ca * d1.x, a.y + ca * d1.y, a.z + ca * d1.z, a.w + ca * d1.w);
+      if constexpr (ORDER == 2) {
+        float4 c = h3[i];
+        r.x += cb * ((a.x - b.x) - (b.x - c.x));
+        r.y += cb * ((a.y - b.y) - (b.y - c.y));
+        r.z += cb * ((a.z - b.z) - (b.z - c.z));
+        r.w += cb * ((a.w - b.w) - (b.w - c.w));
+      }
+      out[i] = r;
+    }
+  }
+}
+
+__global__ void k_proxy_tail(int64_t start, int64_t count, const float *h1, const float *h2,
+                             const float *h3, int order, float ca, float cb, float *out) {
+  int64_t i = start + threadIdx.x;
+  if (i >= count) return;
+  float a = h1[i];
+  float r = a;
+  if (order >= 1) r = a + ca * (a - h2[i]);
+  if (order >= 2) r += cb * ((a - h2[i]) - (h2[i] - h3[i]));
+  out[i] = r;
+}
+
+hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const float *h3, int order,
+                        float ca, float cb, float *out, hipStream_t s) {
+  int64_t n4 = count / 4;
+  if (n4 > 0) {
+    int64_t blocks = (n4 + 255) / 256;
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    dim3 g((unsigned)blocks), b(256);
+    auto *o = (float4 *)out;
+    auto *a = (const float4 *)h1, *bb = (const float4 *)h2, *c = (const float4 *)h3;
+    if (order == 0) hipLaunchKernelGGL(k_proxy<0>, g, b, 0, s, n4, a, bb, c, ca, cb, o);
+    else if (order == 1) hipLaunchKernelGGL(k_proxy<1>, g, b, 0, s, n4, a, bb, c, ca, cb, o);
+    else hipLaunchKernelGGL(k_proxy<2>, g, b, 0, s, n4, a, bb, c, ca, cb, o);
+  }
+  if (count % 4)
+    hipLaunchKernelGGL(k_proxy_tail, dim3(1), dim3(64), 0, s, n4 * 4, count, h1, h2, h3, order, ca,
+                       cb, out);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------------------------------------- patchify
+template <typename T>
+__global__ __launch_bounds__(256) void k_patchify(int n, int C, int H, int W, int p,
+                                                  const float *__restrict__ z, T *__restrict__ tok) {
+  const int P = C * p * p, wp = W / p, T_ = (H / p) * wp;
+  const int64_t total = (int64_t)n * T_ * P;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    int f = (int)(idx % P);
+    int64_t m = idx / P;
+    int t = (int)(m % T_), b = (int)(m / T_);
+    int i = t / wp, j = t % wp;
+    int c = f / (p * p), r = f % (p * p), di = r / p, dj = r % p;
+    tok[idx] = from_f32<T>(z[(((int64_t)b * C + c) * H + (p * i + di)) * W + (p * j + dj)]);
+  }
+}
+
+hipError_t launch_patchify(ActType t, int n, int C, int H, int W, int p, const float *z, void *tok,
+                           hipStream_t s) {
+  int64_t total = (int64_t)n * C * H * W;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (t == ACT_BF16)
+    hipLaunchKernelGGL(k_patchify<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, n, C, H, W, p, z,
+                       (bf16 *)tok);
+  else
+    hipLaunchKernelGGL(k_patchify<float>, dim3((unsigned)blocks), dim3(256), 0, s, n, C, H, W, p, z,
+                       (float *)tok);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------------------------- timestep path
+__global__ void k_time_features(double t, int half, float *f) {
+  int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= half) return;
+  double w = pow(10000.0, -(double)j / (double)half);
+  double a = 1000.0 * t * w;
+  f[j] = (float)cos(a);
+  f[half + j] = (float)sin(a);
+}
+
+hipError_t launch_time_features(double t, int freq_dim, float *f, hipStream_t s) {
+  int half = freq_dim / 2;
+  hipLaunchKernelGGL(k_time_features, dim3((half + 255) / 256), dim3(256), 0, s, t, half, f);
+  return hipGetLastError();
+}
+
+// One wave per output row; lanes stride over the row with float4 loads.
+__global__ __launch_bounds__(256) void k_gemv(int out, int in, const float *__restrict__ W,
+                                              const float *__restrict__ b,
+                                              const float *__restrict__ x, float *__restrict__ y,
+                                              int act_in, int act_out) {
+  const int lane = threadIdx.x & 63;
+  const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (o >= out) return;
+  const float *wr = W + (int64_t)o * in;
+  float acc = 0.f;
+  for (int k = lane; k < in; k += 64) {
+    float xv = x[k];
+    if (act_in == 1) xv = silu(xv);
+    acc += wr[k] * xv;
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    float r = acc + (b ? b[o] : 0.f);
+    if (act_out == 1) r = silu(r);
+    y[o] = r;
+  }
+}
+
+hipError_t launch_gemv(int out, int in, const float *W, const float *b, const float *x, float *y,
+                       int act_in, int act_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_gemv, dim3((out + 3) / 4), dim3(256), 0, s, out, in, W, b, x, y, act_in,
+                     act_out);
+  return hipGetLastError();
+}
+
+__global__ void k_block_mods(int L, int width, const float *__restrict__ m,
+                             const float *__restrict__ tables, int64_t stride,
+                             float *__restrict__ mods) {
+  int j = blockIdx.x * blockDim.x + threadIdx.x;
+  int l = blockIdx.y;
+  if (j >= width) return;
+  mods[(int64_t)l * width + j] = m[j] + tables[l * stride + j];
+}
+
+hipError_t launch_block_mods(int L, int width, const float *m, const float *tables,
+                             int64_t table_stride, float *mods, hipStream_t s) {
+  hipLaunchKernelGGL(k_block_mods, dim3((width + 255) / 256, L), dim3(256), 0, s, L, width, m,
+                     tables, table_stride, mods);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------ conversion
+__global__ __launch_bounds__(256) void k_f32_to_bf16(int64_t n, const float *__restrict__ x,
+                                                     bf16 *__restrict__ y) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    y[i] = (bf16)x[i];
+}
+
+hipError_t launch_f32_to_bf16(int64_t count, const float *x, void *y, hipStream_t s) {
+  int64_t blocks = (count + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_f32_to_bf16, dim3((unsigned)blocks), dim3(256), 0, s, count, x, (bf16 *)y);
+  return hipGetLastError();
+}
+
+}  // namespace fb

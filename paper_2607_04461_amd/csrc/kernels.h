@@ -1,0 +1,69 @@
+// Internal launcher interface between the host-side step driver and the HIP kernels.
+// Every launcher enqueues on `s` and returns hipGetLastError() of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fb {
+
+enum ActType { ACT_F32 = 0, ACT_BF16 = 1 };
+
+enum Epilogue {
+  EPI_STORE = 0,      // out act  = acc + bias
+  EPI_GELU = 1,       // out act  = gelu(acc + bias)
+  EPI_STORE_F32 = 2,  // out fp32 = acc + bias
+  EPI_RESIDUAL = 3,   // out fp32 += gate * (acc + bias); optional cache copy of the result
+  EPI_EULER = 4       // latent z[scatter(m, n)] += dt * (acc + bias)   (head + unpatchify + Euler)
+};
+
+struct EpiArgs {
+  void *out = nullptr;         // [M][ldo] (act or fp32)
+  int64_t ldo = 0;
+  const float *bias = nullptr; // [N] or null
+  const float *gate = nullptr; // [N] or null (RESIDUAL)
+  float *cache = nullptr;      // [M][ldo] fp32 or null (RESIDUAL)
+  // EULER: z [n][C][H][W] fp32, tokens per candidate T = (H/p)(W/p), N = C p p
+  float *z = nullptr;
+  float dt = 0.f;
+  int C = 0, H = 0, W = 0, p = 0, T = 0;
+};
+
+// C[m][n] = sum_k A[m][k] * Wt[n][k] (+ epilogue).  K % 8 == 0.
+hipError_t launch_linear(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt,
+                         const EpiArgs &e, hipStream_t s);
+
+struct AttnArgs {
+  int batch, heads, head_dim, tq, tk;
+  const void *q; int64_t q_bs, q_rs;
+  const void *k; const void *v; int64_t kv_bs, kv_rs;
+  const int32_t *kv_index; int n_kv;   // device, or null (kv batch = q batch)
+  void *out; int64_t o_bs, o_rs;
+};
+hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s);
+
+hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, const float *shift,
+                         const float *scale, void *out, hipStream_t s);
+
+// out = h1 + ca (h1 - h2) + cb (h1 - 2 h2 + h3)   (order 2; order 1 drops cb, order 0 copies h1)
+hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const float *h3, int order,
+                        float ca, float cb, float *out, hipStream_t s);
+
+// tokens [n*T][C p p] (act) from z [n][C][H][W] fp32
+hipError_t launch_patchify(ActType t, int n, int C, int H, int W, int p, const float *z, void *tok,
+                           hipStream_t s);
+
+// sinusoidal features of 1000 t, computed in double: f[j] = cos, f[half + j] = sin
+hipError_t launch_time_features(double t, int freq_dim, float *f, hipStream_t s);
+
+// y[o] = act_out(sum_k W[o][k] act_in(x[k]) + b[o]); act: 0 none, 1 SiLU.  fp32.
+hipError_t launch_gemv(int out, int in, const float *W, const float *b, const float *x, float *y,
+                       int act_in, int act_out, hipStream_t s);
+
+// mods[l][j] = m[j] + table_l[j], table_l = tables + l * table_stride, j < width
+hipError_t launch_block_mods(int L, int width, const float *m, const float *tables,
+                             int64_t table_stride, float *mods, hipStream_t s);
+
+hipError_t launch_f32_to_bf16(int64_t count, const float *x, void *y, hipStream_t s);
+
+}  // namespace fb

@@ -1,0 +1,412 @@
+// C ABI of the draft-step library: model creation, the draft / refine step driver, and helpers.
+// Host code only: validates, plans (dispatch.cpp), then enqueues the kernels of kernels.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/flashbon.h"
+#include "dispatch.h"
+#include "kernels.h"
+#include "model.h"
+
+namespace fb {
+
+thread_local std::string g_err;
+
+flashbon_status fail(flashbon_status st, const std::string &msg) {
+  g_err = msg;
+  return st;
+}
+
+bool config_ok(const flashbon_model_config *c, std::string *why) {
+  auto bad = [&](const char *m) { if (why) *why = m; return false; };
+  if (!c) return bad("config is NULL");
+  if (c->num_blocks < 1) return bad("num_blocks must be >= 1");
+  if (c->hidden < 8 || c->hidden % 8) return bad("hidden must be a positive multiple of 8");
+  if (c->hidden > 6144) return bad("hidden must be <= 6144");
+  if (c->heads < 1 || c->hidden % c->heads) return bad("heads must divide hidden");
+  int dh = c->hidden / c->heads;
+  if (dh != 8 && dh != 16 && dh != 32 && dh != 64 && dh != 128)
+    return bad("head_dim must be one of 8, 16, 32, 64, 128");
+  if (c->mlp_hidden < 8 || c->mlp_hidden % 8) return bad("mlp_hidden must be a positive multiple of 8");
+  if (c->latent_channels < 1 || c->patch < 1) return bad("latent_channels and patch must be >= 1");
+  if ((c->latent_channels * c->patch * c->patch) % 8) return bad("latent_channels*patch^2 must be a multiple of 8");
+  if (c->freq_dim < 2 || c->freq_dim % 8) return bad("freq_dim must be a positive multiple of 8");
+  if (c->text_dim < 8 || c->text_dim % 8) return bad("text_dim must be a positive multiple of 8");
+  if (c->dtype != FLASHBON_FP32 && c->dtype != FLASHBON_BF16) return bad("dtype must be FP32 or BF16");
+  if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return bad("ln_eps must be positive");
+  if (c->max_n < 1 || c->max_tokens < 1 || c->max_text_len < 1 || c->max_cond < 1)
+    return bad("max_n, max_tokens, max_text_len, max_cond must be >= 1");
+  if ((int64_t)c->max_n * c->max_tokens > (int64_t)1 << 30) return bad("max_n * max_tokens too large");
+  return true;
+}
+
+Layout make_layout(const flashbon_model_config &c) {
+  Layout L;
+  size_t o = 0;
+  auto take = [&](size_t n) { size_t r = o; o += n; return r; };
+  const size_t D = c.hidden, F = c.mlp_hidden, P = (size_t)c.latent_channels * c.patch * c.patch;
+  const size_t fd = c.freq_dim, Dt = c.text_dim;
+  L.t_w1 = take(D * fd); L.t_b1 = take(D); L.t_w2 = take(D * D); L.t_b2 = take(D);
+  L.mod_w = take(6 * D * D); L.mod_b = take(6 * D);
+  L.hmod_w = take(2 * D * D); L.hmod_b = take(2 * D);
+  L.pe_w = take(D * P); L.pe_b = take(D);
+  L.txt_w = take(D * Dt); L.txt_b = take(D);
+  L.blk.resize(c.num_blocks);
+  for (int l = 0; l < c.num_blocks; ++l) {
+    BlockOff &b = L.blk[l];
+    b.mod = take(6 * D);
+    b.wqkv = take(3 * D * D); b.bqkv = take(3 * D);
+    b.wo = take(D * D); b.bo = take(D);
+    b.wqc = take(D * D); b.bqc = take(D);
+    b.wkvc = take(2 * D * D); b.bkvc = take(2 * D);
+    b.woc = take(D * D); b.boc = take(D);
+    b.w1 = take(F * D); b.b1 = take(F);
+    b.w2 = take(D * F); b.b2 = take(D);
+  }
+  L.block_stride = c.num_blocks > 1 ? L.blk[1].mod - L.blk[0].mod : 0;
+  L.head_w = take(P * D); L.head_b = take(P);
+  L.total = o;
+  return L;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace fb
+
+using namespace fb;
+
+#define HIPCHK(expr, what)                                                                       \
+  do {                                                                                           \
+    hipError_t _e = (expr);                                                                      \
+    if (_e != hipSuccess) return fail(FLASHBON_EHIP, std::string(what) + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
+extern "C" {
+
+const char *flashbon_last_error(void) { return g_err.c_str(); }
+
+size_t flashbon_weight_count(const flashbon_model_config *cfg) {
+  if (!config_ok(cfg, nullptr)) return 0;
+  return make_layout(*cfg).total;
+}
+
+flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, const uint8_t *proxy,
+                                   flashbon_cache_meta *meta, float t_cur,
+                                   flashbon_trace_entry *trace) {
+  if (num_blocks < 1) return fail(FLASHBON_ESHAPE, "num_blocks must be >= 1");
+  if (!meta || !trace) return fail(FLASHBON_EINVAL, "meta and trace are required");
+  if (!std::isfinite(t_cur)) return fail(FLASHBON_EINVAL, "t_cur must be finite");
+  for (int l = 0; l < num_blocks; ++l)
+    if (!meta_valid(meta[l])) return fail(FLASHBON_ESTATE, "cache meta out of range at block " + std::to_string(l));
+  plan_step(num_blocks, skip, proxy, meta, t_cur, trace);
+  g_err.clear();
+  return FLASHBON_OK;
+}
+
+flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const float *host_weights,
+                                    size_t n_weights, void **out) {
+  std::string why;
+  if (!out) return fail(FLASHBON_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!config_ok(cfg, &why)) return fail(cfg ? FLASHBON_ESHAPE : FLASHBON_EINVAL, why);
+  if (!host_weights) return fail(FLASHBON_EINVAL, "host_weights is NULL");
+  Model *m = new Model();
+  m->c = *cfg;
+  m->lay = make_layout(*cfg);
+  if (n_weights != m->lay.total) {
+    size_t want = m->lay.total;
+    delete m;
+    return fail(FLASHBON_ESHAPE, "n_weights " + std::to_string(n_weights) + " != expected " + std::to_string(want));
+  }
+  m->act = cfg->dtype == FLASHBON_BF16 ? ACT_BF16 : ACT_F32;
+  m->asz = m->act == ACT_BF16 ? 2 : 4;
+  m->D = cfg->hidden; m->H = cfg->heads; m->dh = cfg->hidden / cfg->heads; m->F = cfg->mlp_hidden;
+  m->C = cfg->latent_channels; m->p = cfg->patch; m->P = m->C * m->p * m->p;
+  m->fd = cfg->freq_dim; m->Dt = cfg->text_dim; m->L = cfg->num_blocks;
+  m->maxM = (int64_t)cfg->max_n * cfg->max_tokens;
+  if (hipGetDevice(&m->device) != hipSuccess) { delete m; return fail(FLASHBON_EHIP, "hipGetDevice"); }
+
+  auto cleanup = [&](flashbon_status st, const std::string &msg) {
+    flashbon_free(m);
+    return fail(st, msg);
+  };
+  const size_t total = m->lay.total;
+  if (hipMalloc(&m->w32, total * 4) != hipSuccess) return cleanup(FLASHBON_ENOMEM, "weights (fp32)");
+  if (m->act == ACT_BF16 && hipMalloc(&m->w16, total * 2) != hipSuccess)
+    return cleanup(FLASHBON_ENOMEM, "weights (bf16)");
+
+  // workspace carve-out
+  const size_t D = m->D, F = m->F, P = m->P, M = m->maxM, a = m->asz;
+  const size_t txt_rows = (size_t)cfg->max_cond * cfg->max_text_len;
+  size_t off = 0;
+  auto carve = [&](size_t bytes) { size_t r = off; off += align256(bytes); return r; };
+  size_t o_h = carve(M * D * 4), o_a = carve(M * D * a), o_qkv = carve(M * 3 * D * a),
+         o_o = carve(M * D * a), o_u = carve(M * F * a), o_tok = carve(M * P * a),
+         o_txt = carve(m->act == ACT_BF16 ? txt_rows * m->Dt * a : 0), o_ctx = carve(txt_rows * D * a),
+         o_tf = carve(m->fd * 4), o_e1 = carve(D * 4), o_e = carve(D * 4), o_m6 = carve(6 * D * 4),
+         o_bm = carve((size_t)m->L * 6 * D * 4), o_hm = carve(2 * D * 4), o_cond = carve(cfg->max_n * 4);
+  if (hipMalloc(&m->ws, off) != hipSuccess) return cleanup(FLASHBON_ENOMEM, "workspace of " + std::to_string(off) + " bytes");
+  m->ws_bytes = off;
+  char *w = (char *)m->ws;
+  m->h = (float *)(w + o_h); m->a = w + o_a; m->qkv = w + o_qkv; m->o = w + o_o; m->u = w + o_u;
+  m->tok = w + o_tok; m->txt = w + o_txt; m->ctx = w + o_ctx;
+  m->tf = (float *)(w + o_tf); m->e1 = (float *)(w + o_e1); m->e = (float *)(w + o_e);
+  m->m6 = (float *)(w + o_m6); m->bmods = (float *)(w + o_bm); m->hmod = (float *)(w + o_hm);
+  m->d_cond = (int32_t *)(w + o_cond);
+
+  if (hipMemcpy(m->w32, host_weights, total * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return cleanup(FLASHBON_EHIP, "weight upload");
+  if (m->act == ACT_BF16) {
+    if (launch_f32_to_bf16((int64_t)total, m->w32, m->w16, 0) != hipSuccess)
+      return cleanup(FLASHBON_EHIP, "weight conversion");
+  }
+  if (hipDeviceSynchronize() != hipSuccess) return cleanup(FLASHBON_EHIP, "init synchronise");
+  *out = m;
+  g_err.clear();
+  return FLASHBON_OK;
+}
+
+void flashbon_free(void *model) {
+  if (!model) return;
+  Model *m = (Model *)model;
+  (void)hipDeviceSynchronize();
+  if (m->w32) (void)hipFree(m->w32);
+  if (m->w16) (void)hipFree(m->w16);
+  if (m->ws) (void)hipFree(m->ws);
+  delete m;
+}
+
+size_t flashbon_text_kv_bytes(const void *model, int32_t n_cond, int32_t text_len) {
+  if (!model || n_cond < 1 || text_len < 1) return 0;
+  const Model *m = (const Model *)model;
+  return (size_t)m->L * n_cond * text_len * 2 * m->D * m->asz;
+}
+
+size_t flashbon_cache_bytes(const void *model, int32_t n, int32_t tokens) {
+  if (!model || n < 1 || tokens < 1) return 0;
+  const Model *m = (const Model *)model;
+  return (size_t)m->L * 3 * n * tokens * m->D * 4;
+}
+
+}  // extern "C"
+
+namespace fb {
+
+static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draft) {
+  if (!m) return fail(FLASHBON_EINVAL, "model is NULL");
+  if (!a) return fail(FLASHBON_EINVAL, "args is NULL");
+  const flashbon_model_config &c = m->c;
+  const int L = m->L, D = m->D, F = m->F, P = m->P, p = m->p;
+  // ---------------------------------------------------------------- validation (no side effects)
+  if (a->n < 1 || a->n > c.max_n) return fail(FLASHBON_ESHAPE, "n outside [1, max_n]");
+  if (a->latent_h < p || a->latent_w < p || a->latent_h % p || a->latent_w % p)
+    return fail(FLASHBON_ESHAPE, "latent_h/latent_w must be positive multiples of patch");
+  const int64_t T64 = (int64_t)(a->latent_h / p) * (a->latent_w / p);
+  if (T64 > c.max_tokens) return fail(FLASHBON_ESHAPE, "tokens exceed max_tokens");
+  const int T = (int)T64;
+  const int64_t M = (int64_t)a->n * T;
+  if (!a->latents) return fail(FLASHBON_EINVAL, "latents is NULL");
+  if (!std::isfinite(a->t_cur) || !std::isfinite(a->t_next)) return fail(FLASHBON_EINVAL, "t_cur/t_next must be finite");
+  if (!a->text || !a->cond_index || !a->text_kv || !a->text_kv_valid)
+    return fail(FLASHBON_EINVAL, "text, cond_index, text_kv and text_kv_valid are required");
+  if (a->n_cond < 1 || a->n_cond > c.max_cond) return fail(FLASHBON_ESHAPE, "n_cond outside [1, max_cond]");
+  if (a->text_len < 1 || a->text_len > c.max_text_len) return fail(FLASHBON_ESHAPE, "text_len outside [1, max_text_len]");
+  for (int i = 0; i < a->n; ++i)
+    if (a->cond_index[i] < 0 || a->cond_index[i] >= a->n_cond)
+      return fail(FLASHBON_EINVAL, "cond_index[" + std::to_string(i) + "] outside [0, n_cond)");
+  if (draft) {
+    if (!a->meta) return fail(FLASHBON_EINVAL, "draft step needs meta");
+    if (!a->cache) return fail(FLASHBON_EINVAL, "draft step needs cache");
+    for (int l = 0; l < L; ++l)
+      if (!meta_valid(a->meta[l])) return fail(FLASHBON_ESTATE, "cache meta out of range at block " + std::to_string(l));
+  }
+  std::vector<flashbon_cache_meta> meta_new(L);
+  std::vector<flashbon_trace_entry> trace(L);
+  if (draft) {
+    std::memcpy(meta_new.data(), a->meta, sizeof(flashbon_cache_meta) * L);
+    plan_step(L, a->skip, a->proxy, meta_new.data(), a->t_cur, trace.data());
+  } else {
+    std::vector<flashbon_cache_meta> z(L);
+    std::memset(z.data(), 0, sizeof(flashbon_cache_meta) * L);
+    plan_step(L, nullptr, nullptr, z.data(), a->t_cur, trace.data());
+  }
+  std::vector<float> ca(L, 0.f), cb(L, 0.f);
+  for (int l = 0; l < L; ++l) {
+    if (trace[l].action != FLASHBON_PROXY || !trace[l].live) continue;
+    const flashbon_cache_meta &mb = a->meta[l];
+    if (trace[l].order >= 1) {
+      float t1 = mb.t[(mb.head + 2) % 3], t2 = mb.t[(mb.head + 1) % 3];
+      if (!(t1 != t2) || !std::isfinite(t1) || !std::isfinite(t2))
+        return fail(FLASHBON_ESTATE, "cached timesteps of block " + std::to_string(l) + " coincide or are not finite");
+    }
+    taylor_coefficients(mb, a->t_cur, trace[l].order, &ca[l], &cb[l]);
+  }
+
+  // ---------------------------------------------------------------- enqueue
+  hipStream_t s = (hipStream_t)a->stream;
+  const ActType act = m->act;
+  const size_t asz = m->asz;
+  auto Wp = [&](size_t off) -> const void * {
+    return act == ACT_BF16 ? (const void *)((const char *)m->w16 + off * 2) : (const void *)(m->w32 + off);
+  };
+  auto Bp = [&](size_t off) -> const float * { return m->w32 + off; };
+
+  // cond_index -> device, only when it changed (the previous step may still read the old copy)
+  std::vector<int32_t> cond(a->cond_index, a->cond_index + a->n);
+  if (cond != m->last_cond) {
+    HIPCHK(hipStreamSynchronize(s), "synchronise before cond_index upload");
+    HIPCHK(hipMemcpy(m->d_cond, cond.data(), sizeof(int32_t) * a->n, hipMemcpyHostToDevice), "cond_index upload");
+    m->last_cond = cond;
+  }
+
+  const int Lt = a->text_len, NC = a->n_cond;
+  const int64_t kv_block = (int64_t)NC * Lt * 2 * D;  // elements per block in text_kv
+  if (*a->text_kv_valid == 0) {
+    const void *txt = a->text;
+    if (act == ACT_BF16) {
+      HIPCHK(launch_f32_to_bf16((int64_t)NC * Lt * m->Dt, a->text, m->txt, s), "text convert");
+      txt = m->txt;
+    }
+    EpiArgs e;
+    e.out = m->ctx; e.ldo = D; e.bias = Bp(m->lay.txt_b);
+    HIPCHK(launch_linear(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s), "text projection");
+    for (int l = 0; l < L; ++l) {
+      EpiArgs k;
+      k.out = (char *)a->text_kv + (size_t)l * kv_block * asz; k.ldo = 2 * D; k.bias = Bp(m->lay.blk[l].bkvc);
+      HIPCHK(launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, m->ctx, Wp(m->lay.blk[l].wkvc), k, s), "text K/V");
+    }
+  }
+
+  // timestep conditioning, shared by all candidates
+  HIPCHK(launch_time_features((double)a->t_cur, m->fd, m->tf, s), "time features");
+  HIPCHK(launch_gemv(D, m->fd, m->w32 + m->lay.t_w1, Bp(m->lay.t_b1), m->tf, m->e1, 0, 1, s), "time mlp 1");
+  HIPCHK(launch_gemv(D, D, m->w32 + m->lay.t_w2, Bp(m->lay.t_b2), m->e1, m->e, 0, 0, s), "time mlp 2");
+  HIPCHK(launch_gemv(6 * D, D, m->w32 + m->lay.mod_w, Bp(m->lay.mod_b), m->e, m->m6, 1, 0, s), "modulation");
+  HIPCHK(launch_gemv(2 * D, D, m->w32 + m->lay.hmod_w, Bp(m->lay.hmod_b), m->e, m->hmod, 1, 0, s), "head modulation");
+  HIPCHK(launch_block_mods(L, 6 * D, m->m6, m->w32 + m->lay.blk[0].mod, (int64_t)m->lay.block_stride, m->bmods, s),
+         "block modulation");
+
+  const int64_t MD = M * D;
+  auto dump = [&](int idx) -> flashbon_status {
+    if (!a->hidden_dump) return FLASHBON_OK;
+    HIPCHK(hipMemcpyAsync(a->hidden_dump + (int64_t)idx * MD, m->h, MD * 4, hipMemcpyDeviceToDevice, s), "hidden dump");
+    return FLASHBON_OK;
+  };
+  flashbon_status st;
+
+  // patch embedding, unless the first non-skipped block is a proxy (its input is then never read)
+  bool embed_live = true;
+  for (int l = 0; l < L; ++l)
+    if (trace[l].action != FLASHBON_SKIP) { embed_live = trace[l].action == FLASHBON_COMPUTE; break; }
+  if (embed_live) {
+    HIPCHK(launch_patchify(act, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s), "patchify");
+    EpiArgs e;
+    e.out = m->h; e.ldo = D; e.bias = Bp(m->lay.pe_b);
+    HIPCHK(launch_linear(act, EPI_STORE_F32, (int)M, D, P, m->tok, Wp(m->lay.pe_w), e, s), "patch embed");
+    if ((st = dump(0)) != FLASHBON_OK) return st;
+  }
+
+  const int H = m->H, dh = m->dh;
+  for (int l = 0; l < L; ++l) {
+    const flashbon_trace_entry &tr = trace[l];
+    const BlockOff &b = m->lay.blk[l];
+    const float *mod = m->bmods + (int64_t)l * 6 * D;
+    if (tr.action == FLASHBON_SKIP) {
+      if ((st = dump(l + 1)) != FLASHBON_OK) return st;
+      continue;
+    }
+    if (tr.action == FLASHBON_PROXY) {
+      if (!tr.live) continue;
+      const flashbon_cache_meta &mb = a->meta[l];
+      const int s1 = (mb.head + 2) % 3, s2 = (mb.head + 1) % 3, s3 = mb.head;
+      auto slot_ptr = [&](int sl) { return a->cache + ((int64_t)l * 3 + sl) * MD; };
+      HIPCHK(launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s),
+             "activation proxy");
+      if ((st = dump(l + 1)) != FLASHBON_OK) return st;
+      continue;
+    }
+    // COMPUTE (Eq. 7)
+    HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 0 * D, mod + 1 * D, m->a, s), "adaLN 1");
+    {
+      EpiArgs e; e.out = m->qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
+      HIPCHK(launch_linear(act, EPI_STORE, (int)M, 3 * D, D, m->a, Wp(b.wqkv), e, s), "qkv projection");
+    }
+    {
+      AttnArgs at;
+      at.batch = a->n; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = T;
+      at.q = m->qkv; at.q_bs = (int64_t)T * 3 * D; at.q_rs = 3 * D;
+      at.k = (const char *)m->qkv + (size_t)D * asz; at.v = (const char *)m->qkv + (size_t)2 * D * asz;
+      at.kv_bs = (int64_t)T * 3 * D; at.kv_rs = 3 * D; at.kv_index = nullptr; at.n_kv = a->n;
+      at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
+      HIPCHK(launch_attention(act, at, s), "self-attention");
+    }
+    {
+      EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.bo); e.gate = mod + 2 * D;
+      HIPCHK(launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.wo), e, s), "self-attn out projection");
+    }
+    HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, nullptr, nullptr, m->a, s), "cross LN");
+    {
+      EpiArgs e; e.out = m->qkv; e.ldo = D; e.bias = Bp(b.bqc);
+      HIPCHK(launch_linear(act, EPI_STORE, (int)M, D, D, m->a, Wp(b.wqc), e, s), "cross q projection");
+    }
+    {
+      const char *kv = (const char *)a->text_kv + (size_t)l * kv_block * asz;
+      AttnArgs at;
+      at.batch = a->n; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = Lt;
+      at.q = m->qkv; at.q_bs = (int64_t)T * D; at.q_rs = D;
+      at.k = kv; at.v = kv + (size_t)D * asz; at.kv_bs = (int64_t)Lt * 2 * D; at.kv_rs = 2 * D;
+      at.kv_index = m->d_cond; at.n_kv = NC;
+      at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
+      HIPCHK(launch_attention(act, at, s), "cross-attention");
+    }
+    {
+      EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.boc);
+      HIPCHK(launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.woc), e, s), "cross out projection");
+    }
+    HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 3 * D, mod + 4 * D, m->a, s), "adaLN 2");
+    {
+      EpiArgs e; e.out = m->u; e.ldo = F; e.bias = Bp(b.b1);
+      HIPCHK(launch_linear(act, EPI_GELU, (int)M, F, D, m->a, Wp(b.w1), e, s), "mlp up");
+    }
+    {
+      EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
+      if (draft) e.cache = a->cache + ((int64_t)l * 3 + tr.slot) * MD;
+      HIPCHK(launch_linear(act, EPI_RESIDUAL, (int)M, D, F, m->u, Wp(b.w2), e, s), "mlp down");
+    }
+    if ((st = dump(l + 1)) != FLASHBON_OK) return st;
+  }
+
+  // head + unpatchify + Euler update of the latents
+  HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, m->hmod, m->hmod + D, m->a, s), "head adaLN");
+  {
+    EpiArgs e;
+    e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;
+    e.C = m->C; e.H = a->latent_h; e.W = a->latent_w; e.p = p; e.T = T;
+    HIPCHK(launch_linear(act, EPI_EULER, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s), "head + Euler");
+  }
+
+  // ---------------------------------------------------------------- commit host state
+  if (draft) std::memcpy(a->meta, meta_new.data(), sizeof(flashbon_cache_meta) * L);
+  if (a->trace) std::memcpy(a->trace, trace.data(), sizeof(flashbon_trace_entry) * L);
+  *a->text_kv_valid = 1;
+  g_err.clear();
+  return FLASHBON_OK;
+}
+
+}  // namespace fb
+
+extern "C" {
+
+flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args) {
+  return run_step((Model *)model, args, true);
+}
+
+flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args) {
+  return run_step((Model *)model, args, false);
+}
+
+}  // extern "C"

@@ -1,0 +1,257 @@
+"""Python binding of ``libflashbon.so`` (include/flashbon.h, include/flashbon_ops.h).
+
+Argument marshalling only: every step of the draft path runs in the library's HIP kernels.  Device
+buffers are anything with ``data_ptr()`` (torch CUDA tensors); ``stream=None`` means torch's current
+stream on the current device.  The library must have been built (``__graft_entry__.build()``); a
+missing library raises, there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashbon.so")
+_lib: Optional[ctypes.CDLL] = None
+
+OK, EINVAL, ESHAPE, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
+FP32, BF16 = 0, 1
+COMPUTE, SKIP, PROXY = 0, 1, 2
+EPI_STORE, EPI_GELU, EPI_STORE_F32, EPI_RESIDUAL = 0, 1, 2, 3
+
+
+class FlashbonError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where} failed with status {status}: {msg}")
+        self.status = status
+
+
+class ModelConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("num_blocks", "hidden", "heads", "mlp_hidden",
+                                               "latent_channels", "patch", "freq_dim", "text_dim",
+                                               "dtype")] + \
+               [("ln_eps", ctypes.c_float)] + \
+               [(n, ctypes.c_int32) for n in ("max_n", "max_tokens", "max_text_len", "max_cond")]
+
+
+class CacheMeta(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int32), ("head", ctypes.c_int32), ("t", ctypes.c_float * 3)]
+
+
+class TraceEntry(ctypes.Structure):
+    _fields_ = [("action", ctypes.c_int8), ("order", ctypes.c_int8), ("slot", ctypes.c_int8),
+                ("live", ctypes.c_int8)]
+
+
+class StepArgs(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int32), ("latent_h", ctypes.c_int32), ("latent_w", ctypes.c_int32),
+        ("latents", ctypes.c_void_p), ("t_cur", ctypes.c_float), ("t_next", ctypes.c_float),
+        ("text", ctypes.c_void_p), ("n_cond", ctypes.c_int32), ("text_len", ctypes.c_int32),
+        ("cond_index", ctypes.POINTER(ctypes.c_int32)), ("text_kv", ctypes.c_void_p),
+        ("text_kv_valid", ctypes.POINTER(ctypes.c_int32)),
+        ("skip", ctypes.POINTER(ctypes.c_uint8)), ("proxy", ctypes.POINTER(ctypes.c_uint8)),
+        ("cache", ctypes.c_void_p), ("meta", ctypes.POINTER(CacheMeta)),
+        ("trace", ctypes.POINTER(TraceEntry)), ("hidden_dump", ctypes.c_void_p),
+        ("stream", ctypes.c_void_p),
+    ]
+
+
+EXPORTS = [
+    "flashbon_weight_count", "flashbon_init_model", "flashbon_text_kv_bytes", "flashbon_cache_bytes",
+    "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
+    "flashbon_last_error", "flashbon_op_linear", "flashbon_op_attention", "flashbon_op_ln_mod",
+    "flashbon_op_proxy",
+]
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load() -> ctypes.CDLL:
+    """Load the built library (raises FileNotFoundError if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise FileNotFoundError(f"{_LIB_PATH} is not built; run __graft_entry__.build()")
+    L = ctypes.CDLL(_LIB_PATH)
+    vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    L.flashbon_weight_count.argtypes = [ctypes.POINTER(ModelConfig)]
+    L.flashbon_weight_count.restype = sz
+    L.flashbon_init_model.argtypes = [ctypes.POINTER(ModelConfig), vp, sz, ctypes.POINTER(vp)]
+    L.flashbon_init_model.restype = i32
+    L.flashbon_text_kv_bytes.argtypes = [vp, i32, i32]
+    L.flashbon_text_kv_bytes.restype = sz
+    L.flashbon_cache_bytes.argtypes = [vp, i32, i32]
+    L.flashbon_cache_bytes.restype = sz
+    L.flashbon_draft_step.argtypes = [vp, ctypes.POINTER(StepArgs)]
+    L.flashbon_draft_step.restype = i32
+    L.flashbon_refine_step.argtypes = [vp, ctypes.POINTER(StepArgs)]
+    L.flashbon_refine_step.restype = i32
+    L.flashbon_free.argtypes = [vp]
+    L.flashbon_free.restype = None
+    L.flashbon_plan_step.argtypes = [i32, ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_uint8),
+                                     ctypes.POINTER(CacheMeta), f32, ctypes.POINTER(TraceEntry)]
+    L.flashbon_plan_step.restype = i32
+    L.flashbon_last_error.argtypes = []
+    L.flashbon_last_error.restype = ctypes.c_char_p
+    L.flashbon_op_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
+    L.flashbon_op_linear.restype = i32
+    L.flashbon_op_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, i64, i64, vp, vp, i64, i64,
+                                        vp, i32, vp, i64, i64, vp]
+    L.flashbon_op_attention.restype = i32
+    L.flashbon_op_ln_mod.argtypes = [i32, i32, i32, f32, vp, vp, vp, vp, vp]
+    L.flashbon_op_ln_mod.restype = i32
+    L.flashbon_op_proxy.argtypes = [i64, vp, vp, vp, i32, f32, f32, f32, vp, vp]
+    L.flashbon_op_proxy.restype = i32
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise FlashbonError(status, where, load().flashbon_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return int(stream)
+    import torch
+    return int(torch.cuda.current_stream().cuda_stream)
+
+
+def _u8(mask: Optional[Sequence[int]], n: int):
+    if mask is None:
+        return None, None
+    a = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
+    if a.shape != (n,):
+        raise ValueError(f"mask must have shape ({n},)")
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))
+
+
+def make_config(shape, dtype: int, max_n: int, max_tokens: int, max_text_len: int, max_cond: int) -> ModelConfig:
+    return ModelConfig(shape.num_blocks, shape.hidden, shape.heads, shape.mlp_hidden,
+                       shape.latent_channels, shape.patch, shape.freq_dim, shape.text_dim, dtype,
+                       shape.ln_eps, max_n, max_tokens, max_text_len, max_cond)
+
+
+def flashbon_weight_count(cfg: ModelConfig) -> int:
+    return int(load().flashbon_weight_count(ctypes.byref(cfg)))
+
+
+def flashbon_init_model(cfg: ModelConfig, host_weights: np.ndarray) -> int:
+    w = np.ascontiguousarray(host_weights, dtype=np.float32)
+    h = ctypes.c_void_p()
+    _check(load().flashbon_init_model(ctypes.byref(cfg), w.ctypes.data, w.size, ctypes.byref(h)),
+           "flashbon_init_model")
+    return int(h.value)
+
+
+def flashbon_free(model: Optional[int]) -> None:
+    if model:
+        load().flashbon_free(model)
+
+
+def flashbon_text_kv_bytes(model: int, n_cond: int, text_len: int) -> int:
+    return int(load().flashbon_text_kv_bytes(model, n_cond, text_len))
+
+
+def flashbon_cache_bytes(model: int, n: int, tokens: int) -> int:
+    return int(load().flashbon_cache_bytes(model, n, tokens))
+
+
+def new_meta(num_blocks: int):
+    return (CacheMeta * num_blocks)()
+
+
+def new_trace(num_blocks: int):
+    return (TraceEntry * num_blocks)()
+
+
+def trace_list(trace) -> list:
+    return [(e.action, e.order, e.slot, e.live) for e in trace]
+
+
+def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
+          skip=None, proxy=None, cache=None, meta=None, trace=None, hidden_dump=None, stream=None,
+          num_blocks=None):
+    n, C, H, W = (int(x) for x in latents.shape)
+    n_cond, text_len = int(text.shape[0]), int(text.shape[1])
+    cond = np.ascontiguousarray(np.asarray(cond_index, dtype=np.int32))
+    if cond.shape != (n,):
+        raise ValueError(f"cond_index must have shape ({n},)")
+    L = num_blocks if num_blocks is not None else (len(meta) if meta is not None else None)
+    sk, skp = _u8(skip, L) if skip is not None else (None, None)
+    px, pxp = _u8(proxy, L) if proxy is not None else (None, None)
+    a = StepArgs()
+    a.n, a.latent_h, a.latent_w = n, H, W
+    a.latents = _ptr(latents)
+    a.t_cur, a.t_next = float(t_cur), float(t_next)
+    a.text = _ptr(text)
+    a.n_cond, a.text_len = n_cond, text_len
+    a.cond_index = cond.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    a.text_kv = _ptr(text_kv)
+    a.text_kv_valid = ctypes.pointer(text_kv_valid)
+    a.skip, a.proxy = skp, pxp
+    a.cache = _ptr(cache)
+    a.meta = meta
+    a.trace = trace
+    a.hidden_dump = _ptr(hidden_dump)
+    a.stream = _stream(stream)
+    _check(fn(model, ctypes.byref(a)), where)
+
+
+def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
+                        skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None):
+    """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays."""
+    _step(load().flashbon_draft_step, "flashbon_draft_step", model, latents, t_cur, t_next, text,
+          cond_index, text_kv, text_kv_valid, skip, proxy, cache, meta, trace, hidden_dump, stream,
+          num_blocks=len(meta))
+
+
+def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
+                         trace=None, hidden_dump=None, stream=None):
+    _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
+          cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream)
+
+
+def flashbon_plan_step(skip, proxy, meta, t_cur: float, trace=None):
+    L = len(meta)
+    sk, skp = _u8(skip, L)
+    px, pxp = _u8(proxy, L)
+    if trace is None:
+        trace = new_trace(L)
+    _check(load().flashbon_plan_step(L, skp, pxp, meta, float(t_cur), trace), "flashbon_plan_step")
+    return trace
+
+
+# --------------------------------------------------------------------------- kernel-level entry points
+
+def flashbon_op_linear(dtype, M, N, K, A, W, bias, epilogue, out, gate=None, cache_out=None, stream=None):
+    _check(load().flashbon_op_linear(dtype, M, N, K, _ptr(A), _ptr(W), _ptr(bias), epilogue, _ptr(out),
+                                     _ptr(gate), _ptr(cache_out), _stream(stream)), "flashbon_op_linear")
+
+
+def flashbon_op_attention(dtype, batch, heads, head_dim, tq, tk, q, q_bs, q_rs, k, v, kv_bs, kv_rs,
+                          kv_index, n_kv, out, o_bs, o_rs, stream=None):
+    _check(load().flashbon_op_attention(dtype, batch, heads, head_dim, tq, tk, _ptr(q), q_bs, q_rs, _ptr(k),
+                                        _ptr(v), kv_bs, kv_rs, _ptr(kv_index), n_kv, _ptr(out), o_bs, o_rs,
+                                        _stream(stream)), "flashbon_op_attention")
+
+
+def flashbon_op_ln_mod(dtype, M, D, eps, x, shift, scale, out, stream=None):
+    _check(load().flashbon_op_ln_mod(dtype, M, D, eps, _ptr(x), _ptr(shift), _ptr(scale), _ptr(out),
+                                     _stream(stream)), "flashbon_op_ln_mod")
+
+
+def flashbon_op_proxy(count, h1, h2, h3, order, tau1, tau2, t_cur, out, stream=None):
+    _check(load().flashbon_op_proxy(count, _ptr(h1), _ptr(h2), _ptr(h3), order, tau1, tau2, t_cur, _ptr(out),
+                                    _stream(stream)), "flashbon_op_proxy")

@@ -1,0 +1,91 @@
+"""A candidate pool driven through the C ABI: torch device buffers + the S'-step loop.
+
+Holds the caller-owned state the library expects (latents, text, text K/V scratch, activation cache,
+cache metadata) and calls ``flashbon_draft_step`` / ``flashbon_refine_step`` once per step.  No
+arithmetic of the method happens here.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Callable, List, Optional, Tuple
+
+import numpy as np
+
+from . import flashbon as fb
+from . import synth
+
+
+class DraftPool:
+    def __init__(self, wl: synth.Workload, dtype: Optional[str] = None, weights: Optional[np.ndarray] = None,
+                 device: str = "cuda", max_n: Optional[int] = None, max_cond: Optional[int] = None):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.shape = wl.shape
+        self.dtype = dtype or wl.dtype
+        self.device = device
+        if weights is None:
+            weights, _ = synth.make_weights(wl.shape, wl.seed_w)
+        cfg = fb.make_config(wl.shape, fb.BF16 if self.dtype == "bf16" else fb.FP32,
+                             max_n or wl.n, wl.tokens, wl.text_len, max_cond or wl.n_cond)
+        self.cfg = cfg
+        self.model = fb.flashbon_init_model(cfg, weights)
+        L = wl.shape.num_blocks
+        self.L = L
+        self.latents = torch.empty((wl.n, wl.shape.latent_channels, wl.latent_h, wl.latent_w),
+                                   dtype=torch.float32, device=device)
+        self.text = torch.from_numpy(synth.make_text(wl.n_cond, wl.text_len, wl.shape.text_dim)).to(device)
+        self.cond_index = wl.cond_index()
+        self.text_kv = torch.empty(fb.flashbon_text_kv_bytes(self.model, wl.n_cond, wl.text_len),
+                                   dtype=torch.uint8, device=device)
+        self.cache = torch.empty(fb.flashbon_cache_bytes(self.model, wl.n, wl.tokens) // 4,
+                                 dtype=torch.float32, device=device)
+        self.text_kv_valid = ctypes.c_int32(0)
+        self.meta = fb.new_meta(L)
+        self.trace = fb.new_trace(L)
+        self.schedule = wl.schedule()
+
+    def reset(self, z0: Optional[np.ndarray] = None) -> None:
+        """Load initial latents (default: the seeded ones) and clear the cache metadata."""
+        wl = self.wl
+        if z0 is None:
+            z0 = synth.make_latents(wl.n, wl.shape.latent_channels, wl.latent_h, wl.latent_w)
+        self.latents.copy_(self.torch.from_numpy(np.ascontiguousarray(z0, np.float32)))
+        ctypes.memset(self.meta, 0, ctypes.sizeof(self.meta))
+
+    def draft_step(self, k: int, skip=None, proxy=None, hidden_dump=None, stream=None) -> list:
+        if skip is None or proxy is None:
+            s, p = self.wl.masks(k)
+            skip = s if skip is None else skip
+            proxy = p if proxy is None else proxy
+        fb.flashbon_draft_step(self.model, self.latents, self.schedule[k], self.schedule[k + 1], self.text,
+                               self.cond_index, self.text_kv, self.text_kv_valid, skip, proxy, self.cache,
+                               self.meta, self.trace, hidden_dump, stream)
+        return fb.trace_list(self.trace)
+
+    def refine_step(self, k: int, latents=None, cond_index=None, hidden_dump=None, stream=None) -> list:
+        lat = self.latents if latents is None else latents
+        cond = self.cond_index if cond_index is None else cond_index
+        fb.flashbon_refine_step(self.model, lat, self.schedule[k], self.schedule[k + 1], self.text, cond,
+                                self.text_kv, self.text_kv_valid, self.trace, hidden_dump, stream)
+        return fb.trace_list(self.trace)
+
+    def draft(self, steps: Optional[int] = None, on_step: Optional[Callable] = None) -> List[list]:
+        traces = []
+        for k in range(self.wl.steps_draft if steps is None else steps):
+            traces.append(self.draft_step(k))
+            if on_step is not None:
+                on_step(k, self)
+        return traces
+
+    def close(self) -> None:
+        if self.model:
+            fb.flashbon_free(self.model)
+            self.model = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+

@@ -225,6 +225,16 @@ def random_cache_entries(shape: Tuple[int, ...], seed: int) -> np.ndarray:
     return np.random.default_rng(seed).standard_normal((3,) + tuple(shape), dtype=np.float32)
 
 
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even), returned as float32.
+
+    Used to draw test operands that are exactly representable in bf16, so that a bf16 kernel and
+    an fp64 reference see identical input values."""
+    u = np.ascontiguousarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
 def random_matrix(shape: Tuple[int, ...], seed: int, scale: float = 1.0) -> np.ndarray:
     """~N(0, scale^2) float32 tensor."""
     a = np.random.default_rng(seed).standard_normal(shape, dtype=np.float32)

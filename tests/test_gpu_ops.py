@@ -1,0 +1,205 @@
+"""Kernel-level parity on the GPU: each HIP kernel of the draft step against the CPU oracle's op on
+identical seeded inputs, at small ragged shapes (every element) and at the real model shapes
+(sampled rows / all elements where cheap).
+
+Tolerances (relative L2 over the compared elements):
+  * fp32 operands, fp32 result: 2e-6 (fp32 rounding over K <= 8960 accumulations);
+  * bf16 operands (exactly representable, drawn via round_to_bf16), fp32 result: 2e-6;
+  * bf16 result: 6e-3 (one bf16 rounding of the output, 2^-9 relative, is the dominant term);
+  * attention with bf16 operands: 1e-2 (bf16 rounding of the probabilities before P.V plus output).
+"""
+import numpy as np
+import pytest
+
+from oracle import dit as odit
+from paper_2607_04461_amd import synth
+from tests._util import rel_l2
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_04461_amd import flashbon
+    flashbon.load()
+
+
+def fb():
+    from paper_2607_04461_amd import flashbon
+    return flashbon
+
+
+def _dev(x, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    return t.to("cuda").to(torch.bfloat16 if dtype == "bf16" else torch.float32)
+
+
+def _operand(shape, seed, dtype, scale=1.0):
+    a = synth.random_matrix(shape, seed, scale)
+    return synth.round_to_bf16(a) if dtype == "bf16" else a
+
+
+LINEAR_SMALL = [(200, 136, 72), (1, 4, 8), (130, 64, 64), (257, 260, 264)]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("M,N,K", LINEAR_SMALL)
+@pytest.mark.parametrize("epi", ["store", "gelu", "store_f32", "residual"])
+def test_linear_small(dtype, M, N, K, epi):
+    F = fb()
+    dt = F.BF16 if dtype == "bf16" else F.FP32
+    A = _operand((M, K), 1, dtype)
+    W = _operand((N, K), 2, dtype, 0.05)
+    bias = synth.random_matrix((N,), 3)
+    gate = synth.random_matrix((N,), 4)
+    h0 = synth.random_matrix((M, N), 5)
+    ref = odit.linear(A.astype(np.float64), W, bias)
+    dA, dW, db, dg = _dev(A, dtype), _dev(W, dtype), _dev(bias, "fp32"), _dev(gate, "fp32")
+    if epi in ("store", "gelu"):
+        out = torch.empty((M, N), device="cuda", dtype=dA.dtype)
+        code = F.EPI_STORE if epi == "store" else F.EPI_GELU
+        F.flashbon_op_linear(dt, M, N, K, dA, dW, db, code, out)
+        if epi == "gelu":
+            ref = odit.gelu_tanh(ref)
+        tol = 6e-3 if dtype == "bf16" else 2e-6
+    elif epi == "store_f32":
+        out = torch.empty((M, N), device="cuda", dtype=torch.float32)
+        F.flashbon_op_linear(dt, M, N, K, dA, dW, db, F.EPI_STORE_F32, out)
+        tol = 2e-6
+    else:
+        out = _dev(h0, "fp32")
+        cache = torch.zeros((M, N), device="cuda", dtype=torch.float32)
+        F.flashbon_op_linear(dt, M, N, K, dA, dW, db, F.EPI_RESIDUAL, out, dg, cache)
+        ref = h0 + gate * ref
+        torch.cuda.synchronize()
+        assert torch.equal(cache, out)
+        tol = 2e-6
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    assert rel_l2(got, ref) <= tol
+
+
+@pytest.mark.parametrize("M,N,K", [(24960, 4608, 1536), (24960, 8960, 1536), (24960, 1536, 8960),
+                                   (24960, 64, 1536), (16384, 15360, 5120)])
+def test_linear_full_shapes_bf16_sampled_rows(M, N, K):
+    F = fb()
+    A = _operand((M, K), 11, "bf16")
+    W = _operand((N, K), 12, "bf16", 0.02)
+    bias = synth.random_matrix((N,), 13)
+    out = torch.empty((M, N), device="cuda", dtype=torch.float32)
+    F.flashbon_op_linear(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"),
+                         F.EPI_STORE_F32, out)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.random.default_rng(14).integers(0, M, 48), [0, 127, 128, M - 1]]))
+    got = out[torch.from_numpy(rows).cuda()].cpu().numpy()
+    ref = odit.linear(A[rows].astype(np.float64), W, bias)
+    assert rel_l2(got, ref) <= 2e-6
+
+
+def _attn_ref(q, k, v, heads):
+    return odit.multi_head_attention(q.astype(np.float64), k.astype(np.float64), v.astype(np.float64), heads)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("heads,dh,tq,tk", [(2, 128, 130, 130), (4, 16, 16, 8), (3, 64, 70, 200),
+                                            (1, 128, 1, 1), (2, 128, 67, 40)])
+def test_attention_small(dtype, heads, dh, tq, tk):
+    F = fb()
+    dt = F.BF16 if dtype == "bf16" else F.FP32
+    B = 3
+    D = heads * dh
+    q = _operand((B, tq, D), 21, dtype)
+    k = _operand((B, tk, D), 22, dtype)
+    v = _operand((B, tk, D), 23, dtype)
+    out = torch.empty((B, tq, D), device="cuda", dtype=torch.bfloat16 if dtype == "bf16" else torch.float32)
+    F.flashbon_op_attention(dt, B, heads, dh, tq, tk, _dev(q, dtype), tq * D, D, _dev(k, dtype), _dev(v, dtype),
+                            tk * D, D, None, 0, out, tq * D, D)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    ref = np.stack([_attn_ref(q[b], k[b], v[b], heads) for b in range(B)])
+    assert rel_l2(got, ref) <= (1e-2 if dtype == "bf16" else 2e-6)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_cross_attention_kv_index(dtype):
+    F = fb()
+    dt = F.BF16 if dtype == "bf16" else F.FP32
+    B, NC, heads, dh, tq, tk = 5, 3, 2, 128, 33, 40
+    D = heads * dh
+    q = _operand((B, tq, D), 31, dtype)
+    kv = _operand((NC, tk, 2 * D), 32, dtype)       # per prompt rows [K | V]
+    idx = np.array([2, 0, 1, 1, 2], np.int32)
+    dkv = _dev(kv, dtype)
+    out = torch.empty((B, tq, D), device="cuda", dtype=torch.bfloat16 if dtype == "bf16" else torch.float32)
+    F.flashbon_op_attention(dt, B, heads, dh, tq, tk, _dev(q, dtype), tq * D, D, dkv, dkv[..., D:],
+                            tk * 2 * D, 2 * D, torch.from_numpy(idx).cuda(), NC, out, tq * D, D)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    ref = np.stack([_attn_ref(q[b], kv[idx[b], :, :D], kv[idx[b], :, D:], heads) for b in range(B)])
+    assert rel_l2(got, ref) <= (1e-2 if dtype == "bf16" else 2e-6)
+
+
+@pytest.mark.parametrize("B,heads,T,tk", [(16, 12, 1560, 1560), (16, 12, 1560, 512), (4, 40, 4096, 4096)])
+def test_attention_full_shapes_bf16_sampled_queries(B, heads, T, tk):
+    F = fb()
+    dh = 128
+    D = heads * dh
+    q = _operand((B, T, D), 41, "bf16")
+    k = _operand((B, tk, D), 42, "bf16")
+    v = _operand((B, tk, D), 43, "bf16")
+    out = torch.empty((B, T, D), device="cuda", dtype=torch.bfloat16)
+    F.flashbon_op_attention(F.BF16, B, heads, dh, T, tk, _dev(q, "bf16"), T * D, D, _dev(k, "bf16"),
+                            _dev(v, "bf16"), tk * D, D, None, 0, out, T * D, D)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(44)
+    for b in (0, B - 1):
+        rows = np.unique(np.concatenate([rng.integers(0, T, 24), [0, T - 1]]))
+        got = out[b][torch.from_numpy(rows).cuda()].float().cpu().numpy()
+        ref = _attn_ref(q[b][rows], k[b], v[b], heads)
+        assert rel_l2(got, ref) <= 1e-2
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("M,D,mod", [(37, 64, True), (24960, 1536, True), (300, 5120, False), (5, 256, False)])
+def test_ln_mod(dtype, M, D, mod):
+    F = fb()
+    dt = F.BF16 if dtype == "bf16" else F.FP32
+    x = synth.random_matrix((M, D), 51) * 3 + 1
+    sh = synth.random_matrix((D,), 52) if mod else None
+    sc = synth.random_matrix((D,), 53) if mod else None
+    out = torch.empty((M, D), device="cuda", dtype=torch.bfloat16 if dtype == "bf16" else torch.float32)
+    F.flashbon_op_ln_mod(dt, M, D, 1e-6, _dev(x, "fp32"), None if sh is None else _dev(sh, "fp32"),
+                         None if sc is None else _dev(sc, "fp32"), out)
+    torch.cuda.synchronize()
+    ref = odit.layer_norm(x.astype(np.float64), 1e-6)
+    if mod:
+        ref = ref * (1 + sc) + sh
+    assert rel_l2(out.float().cpu().numpy(), ref) <= (6e-3 if dtype == "bf16" else 2e-6)
+
+
+@pytest.mark.parametrize("count", [38_338_560, 1001])
+@pytest.mark.parametrize("order", [0, 1, 2])
+def test_proxy_kernel(count, order):
+    F = fb()
+    h = synth.random_cache_entries((count,), 61)
+    taus, t = (0.62, 0.7, 0.78), 0.5
+    d = [_dev(h[i], "fp32") for i in range(3)]
+    out = torch.empty(count, device="cuda", dtype=torch.float32)
+    F.flashbon_op_proxy(count, d[0], d[1], d[2], order, taus[0], taus[1], t, out)
+    torch.cuda.synchronize()
+    entries = [(h[i], np.float32(taus[i])) for i in range(3)]
+    ref = odit.taylor_proxy(entries, np.float32(t), order)
+    assert rel_l2(out.cpu().numpy(), ref) <= 2e-6
+
+
+def test_proxy_kernel_constant_is_exact():
+    F = fb()
+    c = torch.full((4099,), 0.3712, device="cuda", dtype=torch.float32)
+    out = torch.empty_like(c)
+    F.flashbon_op_proxy(4099, c, c, c, 2, 0.25, 0.5, 0.125, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, c)

@@ -1,0 +1,115 @@
+"""Host-only checks of the C-ABI library (no GPU): it loads, exports every declared symbol, its
+dispatcher is bit-exact with the oracle's, and its validation rejects bad configurations."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import dispatch as od
+from paper_2607_04461_amd import flashbon as fb
+from paper_2607_04461_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in ("flashbon.h", "flashbon_ops.h"):
+        txt = open(os.path.join(ROOT, "include", h)).read()
+        txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)          # drop comments
+        names |= set(re.findall(r"(?:flashbon_status|size_t|void|const char)\s*\*?\s*(flashbon_[a-z_0-9]+)\s*\(", txt))
+    return sorted(names)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = fb.load()
+    names = _declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(fb.EXPORTS)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "wan1.3b_pool16", "wan14b_pool4", "wan1.3b_pool64"])
+def test_plan_step_matches_oracle_on_workloads(name):
+    wl = synth.WORKLOADS[name]
+    L = wl.shape.num_blocks
+    meta_c = fb.new_meta(L)
+    meta_o = od.empty_meta(L)
+    sched = wl.schedule()
+    for k in range(wl.steps_draft):
+        skip, proxy = wl.masks(k)
+        tr_c = fb.trace_list(fb.flashbon_plan_step(skip, proxy, meta_c, sched[k]))
+        tr_o, meta_o = od.plan_step(skip, proxy, meta_o, sched[k])
+        assert tr_c == [tuple(e) for e in tr_o], f"step {k}"
+        for l in range(L):
+            assert (meta_c[l].count, meta_c[l].head) == (meta_o[l]["count"], meta_o[l]["head"])
+            assert list(meta_c[l].t) == meta_o[l]["t"]
+
+
+def test_plan_step_random_masks_bit_exact():
+    rng = np.random.default_rng(42)
+    for trial in range(200):
+        L = int(rng.integers(1, 12))
+        meta_c = fb.new_meta(L)
+        meta_o = od.empty_meta(L)
+        t = 1.0
+        for k in range(int(rng.integers(1, 9))):
+            skip = (rng.random(L) < rng.random()).astype(np.uint8)
+            proxy = (rng.random(L) < rng.random()).astype(np.uint8)
+            tr_c = fb.trace_list(fb.flashbon_plan_step(skip, proxy, meta_c, t))
+            tr_o, meta_o = od.plan_step(skip, proxy, meta_o, t)
+            assert tr_c == [tuple(e) for e in tr_o]
+            t -= float(rng.random()) * 0.1
+
+
+def test_plan_step_rejects_bad_meta():
+    meta = fb.new_meta(3)
+    meta[1].count = 4
+    with pytest.raises(fb.FlashbonError) as e:
+        fb.flashbon_plan_step(np.zeros(3), np.zeros(3), meta, 0.5)
+    assert e.value.status == fb.ESTATE
+    meta[1].count = 2
+    meta[1].head = 3
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_plan_step(np.zeros(3), np.zeros(3), meta, 0.5)
+
+
+@pytest.mark.parametrize("shape", [synth.TINY, synth.MID, synth.WAN_1_3B, synth.WAN_14B])
+def test_weight_count_matches_packing(shape):
+    cfg = fb.make_config(shape, fb.BF16, 1, 16, 8, 1)
+    assert fb.flashbon_weight_count(cfg) == synth.weight_count(shape)
+
+
+def test_weight_count_of_published_shapes():
+    # the blocks of the 1.3B-shaped model hold 1.39e9 parameters, of the 14B-shaped one 14.05e9;
+    # the shared timestep / text / patch / head layers add a little on top
+    for shape, blocks in ((synth.WAN_1_3B, 1.39e9), (synth.WAN_14B, 14.05e9)):
+        D, F = shape.hidden, shape.mlp_hidden
+        assert abs(shape.num_blocks * (8 * D * D + 2 * D * F) - blocks) < 0.01e9
+        assert blocks < synth.weight_count(shape) < 1.03 * blocks
+
+
+@pytest.mark.parametrize("field,value", [("hidden", 60), ("heads", 5), ("mlp_hidden", 12), ("dtype", 7),
+                                         ("max_n", 0), ("ln_eps", 0.0), ("freq_dim", 6), ("num_blocks", 0)])
+def test_invalid_config_rejected(field, value):
+    cfg = fb.make_config(synth.TINY, fb.FP32, 2, 16, 8, 1)
+    setattr(cfg, field, value)
+    assert fb.flashbon_weight_count(cfg) == 0
+
+
+def test_init_rejects_wrong_weight_count_without_device():
+    cfg = fb.make_config(synth.TINY, fb.FP32, 2, 16, 8, 1)
+    w = np.zeros(10, np.float32)
+    with pytest.raises(fb.FlashbonError) as e:
+        fb.flashbon_init_model(cfg, w)
+    assert e.value.status == fb.ESHAPE
+
+
+def test_round_to_bf16_is_rne():
+    x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 3.0e38], np.float32)
+    y = synth.round_to_bf16(x)
+    assert list(y[:3]) == [1.0, 1.0, 1.0 + 2 ** -6]   # ties to even, then round up past the tie
+    assert y[3] == -2.5
