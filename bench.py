@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched draft step on one MI355X.
+
+One bench step = one whole draft of the pool: the truncated S'-step loop of the 1.3B-shaped DiT over
+N = 16 seed-distinct candidates (1560 image tokens, 512 text tokens), every third block skipped and
+activation proxies on odd steps -- every row of the hot path (truncation, dispatch, computed blocks,
+cache stores, proxies, skips, head + Euler update).  Inputs are resident in HBM and the prompt's
+cross-attention K/V is prepared before the timed region (it is timed separately, as is the
+refinement of the selected candidate).
+
+Prints one JSON line.  ``value`` = candidates drafted per second.  ``roofline`` reports the dominant
+kernel (the MLP up-projection GEMM, the largest single launch) timed live with HIP events on the
+library's stream inside the timed region; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CUs x 4096 bf16 FLOP/clk (dense MFMA) x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+
+
+def block_flops(shape, T, text_len):
+    D, F = shape.hidden, shape.mlp_hidden
+    gemm = 2 * T * D * (3 * D) + 2 * T * D * D + 2 * T * D * D + 2 * T * D * D + 2 * 2 * T * D * F
+    attn = 4 * T * T * D + 4 * T * text_len * D
+    return gemm + attn
+
+
+def draft_flops(wl, traces):
+    """Algorithmic FLOPs of one draft of the pool: computed blocks only, plus patch embed and head
+    (the embed only where it is live)."""
+    s = wl.shape
+    T = wl.tokens
+    per_block = block_flops(s, T, wl.text_len)
+    total = 0
+    for tr in traces:
+        n_comp = sum(1 for e in tr if e[0] == 0)
+        first = next((e[0] for e in tr if e[0] != 1), 0)
+        embed = 2 * T * s.patch_dim * s.hidden if first == 0 else 0
+        total += n_comp * per_block + embed + 2 * T * s.hidden * s.patch_dim
+    return total * wl.n
+
+
+def cpu_baseline(wl, W, z0, text):
+    """The oracle, as it stands, on candidate 0: step 0 (computed blocks) and step 1 (proxies),
+    extrapolated to the draft's steps."""
+    from oracle import dit as odit
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    sched = wl.schedule()
+    t0 = time.time()
+    kv = odit.prepare_text(W, wl.shape, text)
+    cache = odit.PoolCache(wl.shape.num_blocks)
+    t1 = time.time()
+    z = z0.astype(np.float64)
+    times = []
+    for k in range(2):
+        skip, proxy = wl.masks(k)
+        ts = time.time()
+        z, _ = odit.draft_step(W, wl.shape, z, sched[k], sched[k + 1], kv, wl.cond_index(), skip, proxy,
+                               cache, candidates=[0])
+        times.append(time.time() - ts)
+    n_compute_steps = sum(1 for k in range(wl.steps_draft) if k % 2 == 0)
+    per_cand = n_compute_steps * times[0] + (wl.steps_draft - n_compute_steps) * times[1]
+    return {"value": 1.0 / per_cand, "unit": "candidates/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"candidate 0 of the pool: step 0 (all computed blocks) {times[0]:.1f} s and step 1 "
+                       f"(proxies) {times[1]:.2f} s, extrapolated to the {wl.steps_draft}-step draft "
+                       f"({n_compute_steps} computed + {wl.steps_draft - n_compute_steps} proxy steps); "
+                       f"text preparation {t1 - t0:.1f} s excluded; fp64 numpy")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="wan1.3b_pool16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-breakdown", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the draft pool runs on a single MI355X and no multi-GPU path "
+              "is built; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_04461_amd import flashbon as fb
+    from paper_2607_04461_amd import synth
+    from paper_2607_04461_amd.pool import DraftPool
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    fb.load()
+    wl = synth.WORKLOADS[args.workload]
+    t_gen = time.time()
+    flat, W = synth.make_weights(wl.shape, wl.seed_w, threads=16)
+    z0 = synth.make_latents(wl.n, wl.shape.latent_channels, wl.latent_h, wl.latent_w)
+    text = synth.make_text(wl.n_cond, wl.text_len, wl.shape.text_dim)
+    print(f"# inputs generated in {time.time() - t_gen:.1f} s", file=sys.stderr, flush=True)
+    pool = DraftPool(wl, dtype="bf16", weights=flat)
+    z0_dev = torch.from_numpy(z0).cuda()
+    stream = torch.cuda.current_stream()
+
+    def one_draft():
+        pool.latents.copy_(z0_dev)
+        ctypes.memset(pool.meta, 0, ctypes.sizeof(pool.meta))
+        return [pool.draft_step(k) for k in range(wl.steps_draft)]
+
+    # text preparation (once per prompt), timed on its own
+    fb.flashbon_set_timing(pool.model, ["text"])
+    pool.text_kv_valid.value = 0
+    traces = one_draft()
+    torch.cuda.synchronize()
+    text_ms, _ = fb.flashbon_read_timing(pool.model, "text")
+    fb.flashbon_set_timing(pool.model, [])
+    for _ in range(max(0, args.warmup - 1)):
+        one_draft()
+    torch.cuda.synchronize()
+    print(f"# warm-up done", file=sys.stderr, flush=True)
+
+    # timed region: K whole drafts; the dominant kernel is timed in place
+    fb.flashbon_set_timing(pool.model, ["mlp_up"])
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        one_draft()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    up_ms, up_n = fb.flashbon_read_timing(pool.model, "mlp_up")
+    fb.flashbon_set_timing(pool.model, [])
+    ms_per_step = total_ms / args.steps
+    value = wl.n / (ms_per_step / 1e3)
+    flops = draft_flops(wl, traces)
+    tflops = flops / (ms_per_step / 1e3) / 1e12
+    M = wl.n * wl.tokens
+    up_flops = 2.0 * M * wl.shape.mlp_hidden * wl.shape.hidden
+    up_avg_ms = up_ms / max(up_n, 1)
+    up_tflops = up_flops / (up_avg_ms / 1e3) / 1e12
+    print(f"# {args.steps} drafts in {total_ms:.1f} ms; mlp_up {up_n} launches avg {up_avg_ms:.3f} ms",
+          file=sys.stderr, flush=True)
+
+    breakdown = None
+    if not args.no_breakdown:
+        fb.flashbon_set_timing(pool.model, fb.SITES)
+        one_draft()
+        torch.cuda.synchronize()
+        breakdown = {}
+        for site in fb.SITES:
+            ms, n = fb.flashbon_read_timing(pool.model, site)
+            if n:
+                breakdown[site] = {"ms": round(ms, 3), "launches": n}
+        fb.flashbon_set_timing(pool.model, [])
+
+    # refinement of the selected candidate (seeded stand-in verifier score, argmax, lowest index on ties)
+    scores = synth.make_scores(wl.n, seed=7)
+    sel = int(np.argmax(scores))
+    one_draft()
+    lat = pool.latents[sel:sel + 1].clone()
+    cond = wl.cond_index()[sel:sel + 1]
+    torch.cuda.synchronize()
+    r0 = time.time()
+    for k in range(wl.steps_draft, wl.steps_total):
+        pool.refine_step(k, latents=lat, cond_index=cond)
+    torch.cuda.synchronize()
+    refine_ms = (time.time() - r0) * 1e3
+
+    result = {
+        "metric": "draft candidates/sec (1.3B-shaped DiT, N=16) + % bf16 MFMA peak",
+        "value": round(value, 3),
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) latents and text, N(0,0.02^2) random-init weights)",
+        "config": {
+            "workload": (f"{wl.name}: 1.3B-shaped DiT ({wl.shape.num_blocks} blocks, D={wl.shape.hidden}, "
+                         f"{wl.shape.heads} heads x {wl.shape.head_dim}, MLP {wl.shape.mlp_hidden}), "
+                         f"N={wl.n} candidates, {wl.tokens} image tokens, {wl.text_len} text tokens, "
+                         f"S'={wl.steps_draft} of {wl.steps_total} steps, every 3rd block skipped, "
+                         f"proxies on odd steps"),
+            "global_batch": wl.n, "seq_len": wl.tokens, "parallelism": "none (1 GPU)",
+        },
+        "tflops_end_to_end": round(tflops, 2),
+        "mfma_frac_end_to_end": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "algorithmic_tflop_per_step": round(flops / 1e12, 3),
+        "roofline": {
+            "kernel": "k_linear_mfma<EPI_GELU> (MLP up-projection, M=%d N=%d K=%d)" % (M, wl.shape.mlp_hidden,
+                                                                                   wl.shape.hidden),
+            "bound": "mfma", "achieved": round(up_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "avg_launch_ms": round(up_avg_ms, 4), "launches": up_n,
+        },
+        "text_prep_ms": round(text_ms, 3),
+        "refine_ms": round(refine_ms, 2),
+        "refine_steps": wl.steps_total - wl.steps_draft,
+        "site_breakdown_one_draft": breakdown,
+    }
+    pool.close()
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(wl, W, z0, text)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

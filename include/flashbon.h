@@ -61,7 +61,7 @@ typedef enum {
 typedef struct {
   int32_t num_blocks;      /* L */
   int32_t hidden;          /* D */
-  int32_t heads;           /* H; hidden % heads == 0, head_dim <= 128 and a multiple of 8 */
+  int32_t heads;           /* H; hidden % heads == 0, head_dim in {8, 16, 32, 64, 128} */
   int32_t mlp_hidden;      /* F */
   int32_t latent_channels; /* C */
   int32_t patch;           /* p (2): token = p x p patch of every channel */
@@ -176,6 +176,35 @@ void flashbon_free(void *model);
 flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, const uint8_t *proxy,
                                    flashbon_cache_meta *meta, float t_cur,
                                    flashbon_trace_entry *trace);
+
+/* Launch sites of the draft step whose device time can be measured (bit i of a site mask). */
+enum {
+  FLASHBON_SITE_QKV = 0,        /* self-attention q/k/v projection        */
+  FLASHBON_SITE_ATTN_SELF = 1,  /* self-attention                         */
+  FLASHBON_SITE_OUT = 2,        /* self-attention output projection       */
+  FLASHBON_SITE_CROSS_Q = 3,    /* cross-attention query projection       */
+  FLASHBON_SITE_ATTN_CROSS = 4, /* cross-attention                        */
+  FLASHBON_SITE_OUT_CROSS = 5,  /* cross-attention output projection      */
+  FLASHBON_SITE_MLP_UP = 6,     /* MLP up projection + GELU               */
+  FLASHBON_SITE_MLP_DOWN = 7,   /* MLP down projection + gate + residual + cache store */
+  FLASHBON_SITE_NORM = 8,       /* the three adaLN / LN launches of a block and the head's */
+  FLASHBON_SITE_PROXY = 9,      /* activation proxy                       */
+  FLASHBON_SITE_EMBED = 10,     /* patchify + patch embedding             */
+  FLASHBON_SITE_HEAD = 11,      /* head projection + unpatchify + Euler   */
+  FLASHBON_SITE_TIME = 12,      /* timestep conditioning                  */
+  FLASHBON_SITE_TEXT = 13,      /* text projection and per-block cross K/V */
+  FLASHBON_NUM_SITES = 14
+};
+
+/* Enable device timing of the sites in `site_mask` for later calls on this model: the library then
+ * records a HIP event pair on the step's stream around every launch at those sites (a few
+ * microseconds of host time per launch; 0 disables).  Accumulated results are read, and reset, by
+ * flashbon_read_timing. */
+flashbon_status flashbon_set_timing(void *model, uint32_t site_mask);
+
+/* Synchronise on the recorded events and return, for one site, the summed device time (ms) and the
+ * number of launches timed since the last read; resets that site's record. */
+flashbon_status flashbon_read_timing(void *model, int32_t site, double *total_ms, int64_t *launches);
 
 /* Description of the calling thread's last failure ("" if none).  Valid until the next call. */
 const char *flashbon_last_error(void);

@@ -3,6 +3,15 @@
 //   * k_attn_valu: one lane per query, online softmax over 16-key sub-tiles staged in LDS as fp32;
 //     any head_dim <= 128 (multiple of 8); fp32 or bf16 operands.  Used by the fp32 mode and for
 //     head dims the MFMA kernel does not take.
+//   * k_attn_mfma: bf16, head_dim 128, gfx950 matrix cores (v_mfma_f32_32x32x16_bf16).  Each wave owns
+//     32 queries.  Scores are formed transposed, S^T = K Q^T, so every lane holds 16 scores of one
+//     query (its partner lane l^32 holds the other 16 of a 32-key slab): the online-softmax max is a
+//     single cross-lane exchange and the running sum stays per lane until the end.  The output is
+//     accumulated transposed as well, O^T += V^T P^T: the probabilities feed the second MFMA straight
+//     from the first one's accumulator registers (the key order inside each 16-key chunk is permuted
+//     identically on both operands), and every lane rescales only its own query.  K tiles are staged
+//     in LDS row-major with an XOR swizzle, V tiles transposed (padded rows) so V^T fragments are two
+//     8-byte reads.
 #include "common.h"
 #include "kernels.h"
 
@@ -83,6 +92,142 @@ __global__ __launch_bounds__(64) void k_attn_valu(AttnP p) {
   for (int d = 0; d < DH; ++d) O[d] = from_f32<T>(o[d] * inv);
 }
 
+namespace fa {
+constexpr int DH = 128;
+constexpr int KT = 64;          // keys per LDS tile
+constexpr int QW = 32;          // queries per wave
+constexpr int WAVES = 4;
+constexpr int QB = QW * WAVES;  // queries per workgroup
+constexpr int VT_LD = KT + 4;   // padded row of the transposed V tile (136 B: conflict-free reads)
+__device__ __forceinline__ int k_off(int r, int c) { return r * DH + ((c ^ (r & 15)) << 3); }
+}  // namespace fa
+
+__global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
+  using namespace fa;
+  __shared__ __attribute__((aligned(16))) bf16 sK[KT * DH];
+  __shared__ __attribute__((aligned(16))) bf16 sVt[DH * VT_LD];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, li = lane & 31;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int q0 = blockIdx.x * QB + w * QW;
+  const int kb = kv_batch(p, b);
+  const bf16 *Q = (const bf16 *)p.q + (int64_t)b * p.q_bs + h * DH;
+  const bf16 *K = (const bf16 *)p.k + (int64_t)kb * p.kv_bs + h * DH;
+  const bf16 *V = (const bf16 *)p.v + (int64_t)kb * p.kv_bs + h * DH;
+
+  // this lane's query row, as the B operand of S^T = K Q^T: 8 k-steps of 16 head dims
+  const int qi = min(q0 + li, p.tq - 1);
+  bf16x8 qf[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks)
+    qf[ks] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qi * p.q_rs + 16 * ks + 8 * g);
+
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) o[dt][j] = 0.f;
+  float mrun = -INFINITY, lsum = 0.f;
+
+  // global -> LDS staging: 64 keys x 16 chunks of 8 head dims; 4 chunks per thread for K and for V
+  const int lr = tid >> 4, lc = tid & 15;
+  u32x4 rk[4], rv[4];
+  auto gload = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int key = min(j0 + lr + 16 * i, p.tk - 1);
+      rk[i] = *reinterpret_cast<const u32x4 *>(K + (int64_t)key * p.kv_rs + 8 * lc);
+      rv[i] = *reinterpret_cast<const u32x4 *>(V + (int64_t)key * p.kv_rs + 8 * lc);
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int r = lr + 16 * i;
+      *reinterpret_cast<u32x4 *>(&sK[k_off(r, lc)]) = rk[i];
+      bf16x8 v8 = __builtin_bit_cast(bf16x8, rv[i]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sVt[(8 * lc + e) * VT_LD + r] = v8[e];
+    }
+  };
+
+  gload(0);
+  for (int j0 = 0; j0 < p.tk; j0 += KT) {
+    __syncthreads();
+    lstore();
+    __syncthreads();
+    if (j0 + KT < p.tk) gload(j0 + KT);
+
+    // S^T for two 32-key slabs: lane holds query li, keys 32 st + (j/4)*8 + 4 g + (j%4)
+    f32x16 sc[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sc[st][j] = 0.f;
+      const int r = 32 * st + li;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        bf16x8 kf = *reinterpret_cast<const bf16x8 *>(&sK[k_off(r, 2 * ks + g)]);
+        sc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[st], 0, 0, 0);
+      }
+    }
+    // online softmax (base 2, scale folded in)
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        int key = j0 + 32 * st + (j >> 2) * 8 + 4 * g + (j & 3);
+        float v = key < p.tk ? sc[st][j] * p.qscale : -INFINITY;
+        sc[st][j] = v;
+        tmax = fmaxf(tmax, v);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mnew = fmaxf(mrun, tmax);
+    const float corr = exp2f(mrun - mnew);
+    mrun = mnew;
+    lsum *= corr;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) o[dt][j] *= corr;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float e = exp2f(sc[st][j] - mnew);
+        lsum += e;
+        sc[st][j] = e;
+      }
+    // O^T += V^T P^T over four 16-key chunks; k-slot i of group g <-> key 16c + (i/4)*8 + 4g + i%4
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      bf16x8 pf;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pf[i] = (bf16)sc[c >> 1][8 * (c & 1) + i];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        const bf16 *vr = &sVt[(32 * dt + li) * VT_LD + 16 * c + 4 * g];
+        bf16x4 v0 = *reinterpret_cast<const bf16x4 *>(vr);
+        bf16x4 v1 = *reinterpret_cast<const bf16x4 *>(vr + 8);
+        bf16x8 vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+      }
+    }
+  }
+  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  const float inv = 1.0f / ltot;
+  if (q0 + li >= p.tq) return;
+  bf16 *O = (bf16 *)p.out + (int64_t)b * p.o_bs + (int64_t)(q0 + li) * p.o_rs + h * DH;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      bf16x4 w4 = {(bf16)(o[dt][4 * jq] * inv), (bf16)(o[dt][4 * jq + 1] * inv),
+                   (bf16)(o[dt][4 * jq + 2] * inv), (bf16)(o[dt][4 * jq + 3] * inv)};
+      *reinterpret_cast<bf16x4 *>(O + 32 * dt + 8 * jq + 4 * g) = w4;
+    }
+}
+
 template <typename T>
 static hipError_t launch_valu(const AttnP &p, int dh, hipStream_t s) {
   dim3 grid((p.tq + 63) / 64, p.heads, p.batch), block(64);
@@ -105,6 +250,11 @@ hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s) {
   p.kv_index = a.kv_index; p.n_kv = a.n_kv;
   p.out = a.out; p.o_bs = a.o_bs; p.o_rs = a.o_rs;
   p.qscale = (float)(1.4426950408889634 / sqrt((double)a.head_dim));
+  if (t == ACT_BF16 && a.head_dim == fa::DH) {
+    dim3 grid((p.tq + fa::QB - 1) / fa::QB, p.heads, p.batch);
+    hipLaunchKernelGGL(k_attn_mfma, grid, dim3(256), 0, s, p);
+    return hipGetLastError();
+  }
   if (t == ACT_BF16) return launch_valu<bf16>(p, a.head_dim, s);
   return launch_valu<float>(p, a.head_dim, s);
 }

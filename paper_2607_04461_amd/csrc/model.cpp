@@ -174,6 +174,9 @@ void flashbon_free(void *model) {
   if (!model) return;
   Model *m = (Model *)model;
   (void)hipDeviceSynchronize();
+  for (auto &site : m->sites)
+    for (auto &pr : site.pending) { (void)hipEventDestroy(pr.first); (void)hipEventDestroy(pr.second); }
+  for (hipEvent_t e : m->spare_events) (void)hipEventDestroy(e);
   if (m->w32) (void)hipFree(m->w32);
   if (m->w16) (void)hipFree(m->w16);
   if (m->ws) (void)hipFree(m->ws);
@@ -195,6 +198,49 @@ size_t flashbon_cache_bytes(const void *model, int32_t n, int32_t tokens) {
 }  // extern "C"
 
 namespace fb {
+
+static hipError_t take_event(Model *m, hipEvent_t *e) {
+  if (!m->spare_events.empty()) {
+    *e = m->spare_events.back();
+    m->spare_events.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
+
+// Drain the finished event pairs of one site into its totals.
+static hipError_t harvest(Model *m, int site) {
+  Model::Site &st = m->sites[site];
+  for (auto &pr : st.pending) {
+    hipError_t e = hipEventSynchronize(pr.second);
+    if (e != hipSuccess) return e;
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, pr.first, pr.second);
+    if (e != hipSuccess) return e;
+    st.total_ms += ms;
+    st.launches += 1;
+    m->spare_events.push_back(pr.first);
+    m->spare_events.push_back(pr.second);
+  }
+  st.pending.clear();
+  return hipSuccess;
+}
+
+// Run `launch` (returning hipError_t), bracketed by events when the site is timed.
+template <typename F>
+static hipError_t timed(Model *m, int site, hipStream_t s, F &&launch) {
+  if (!(m->timing_mask & (1u << site))) return launch();
+  hipEvent_t e0, e1;
+  hipError_t e = take_event(m, &e0);
+  if (e == hipSuccess) e = take_event(m, &e1);
+  if (e != hipSuccess) return e;
+  if ((e = hipEventRecord(e0, s)) != hipSuccess) return e;
+  if ((e = launch()) != hipSuccess) return e;
+  if ((e = hipEventRecord(e1, s)) != hipSuccess) return e;
+  m->sites[site].pending.emplace_back(e0, e1);
+  if (m->sites[site].pending.size() > 65536) return harvest(m, site);
+  return hipSuccess;
+}
 
 static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draft) {
   if (!m) return fail(FLASHBON_EINVAL, "model is NULL");
@@ -268,26 +314,26 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   if (*a->text_kv_valid == 0) {
     const void *txt = a->text;
     if (act == ACT_BF16) {
-      HIPCHK(launch_f32_to_bf16((int64_t)NC * Lt * m->Dt, a->text, m->txt, s), "text convert");
+      HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_f32_to_bf16((int64_t)NC * Lt * m->Dt, a->text, m->txt, s); }), "text convert");
       txt = m->txt;
     }
     EpiArgs e;
     e.out = m->ctx; e.ldo = D; e.bias = Bp(m->lay.txt_b);
-    HIPCHK(launch_linear(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s), "text projection");
+    HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s); }), "text projection");
     for (int l = 0; l < L; ++l) {
       EpiArgs k;
       k.out = (char *)a->text_kv + (size_t)l * kv_block * asz; k.ldo = 2 * D; k.bias = Bp(m->lay.blk[l].bkvc);
-      HIPCHK(launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, m->ctx, Wp(m->lay.blk[l].wkvc), k, s), "text K/V");
+      HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, m->ctx, Wp(m->lay.blk[l].wkvc), k, s); }), "text K/V");
     }
   }
 
   // timestep conditioning, shared by all candidates
-  HIPCHK(launch_time_features((double)a->t_cur, m->fd, m->tf, s), "time features");
-  HIPCHK(launch_gemv(D, m->fd, m->w32 + m->lay.t_w1, Bp(m->lay.t_b1), m->tf, m->e1, 0, 1, s), "time mlp 1");
-  HIPCHK(launch_gemv(D, D, m->w32 + m->lay.t_w2, Bp(m->lay.t_b2), m->e1, m->e, 0, 0, s), "time mlp 2");
-  HIPCHK(launch_gemv(6 * D, D, m->w32 + m->lay.mod_w, Bp(m->lay.mod_b), m->e, m->m6, 1, 0, s), "modulation");
-  HIPCHK(launch_gemv(2 * D, D, m->w32 + m->lay.hmod_w, Bp(m->lay.hmod_b), m->e, m->hmod, 1, 0, s), "head modulation");
-  HIPCHK(launch_block_mods(L, 6 * D, m->m6, m->w32 + m->lay.blk[0].mod, (int64_t)m->lay.block_stride, m->bmods, s),
+  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_time_features((double)a->t_cur, m->fd, m->tf, s); }), "time features");
+  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(D, m->fd, m->w32 + m->lay.t_w1, Bp(m->lay.t_b1), m->tf, m->e1, 0, 1, s); }), "time mlp 1");
+  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(D, D, m->w32 + m->lay.t_w2, Bp(m->lay.t_b2), m->e1, m->e, 0, 0, s); }), "time mlp 2");
+  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(6 * D, D, m->w32 + m->lay.mod_w, Bp(m->lay.mod_b), m->e, m->m6, 1, 0, s); }), "modulation");
+  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(2 * D, D, m->w32 + m->lay.hmod_w, Bp(m->lay.hmod_b), m->e, m->hmod, 1, 0, s); }), "head modulation");
+  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_block_mods(L, 6 * D, m->m6, m->w32 + m->lay.blk[0].mod, (int64_t)m->lay.block_stride, m->bmods, s); }),
          "block modulation");
 
   const int64_t MD = M * D;
@@ -303,10 +349,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   for (int l = 0; l < L; ++l)
     if (trace[l].action != FLASHBON_SKIP) { embed_live = trace[l].action == FLASHBON_COMPUTE; break; }
   if (embed_live) {
-    HIPCHK(launch_patchify(act, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s), "patchify");
+    HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s); }), "patchify");
     EpiArgs e;
     e.out = m->h; e.ldo = D; e.bias = Bp(m->lay.pe_b);
-    HIPCHK(launch_linear(act, EPI_STORE_F32, (int)M, D, P, m->tok, Wp(m->lay.pe_w), e, s), "patch embed");
+    HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, D, P, m->tok, Wp(m->lay.pe_w), e, s); }), "patch embed");
     if ((st = dump(0)) != FLASHBON_OK) return st;
   }
 
@@ -324,16 +370,16 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       const flashbon_cache_meta &mb = a->meta[l];
       const int s1 = (mb.head + 2) % 3, s2 = (mb.head + 1) % 3, s3 = mb.head;
       auto slot_ptr = [&](int sl) { return a->cache + ((int64_t)l * 3 + sl) * MD; };
-      HIPCHK(launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s),
+      HIPCHK(timed(m, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s); }),
              "activation proxy");
       if ((st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
     }
     // COMPUTE (Eq. 7)
-    HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 0 * D, mod + 1 * D, m->a, s), "adaLN 1");
+    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 0 * D, mod + 1 * D, m->a, s); }), "adaLN 1");
     {
       EpiArgs e; e.out = m->qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
-      HIPCHK(launch_linear(act, EPI_STORE, (int)M, 3 * D, D, m->a, Wp(b.wqkv), e, s), "qkv projection");
+      HIPCHK(timed(m, FLASHBON_SITE_QKV, s, [&] { return launch_linear(act, EPI_STORE, (int)M, 3 * D, D, m->a, Wp(b.wqkv), e, s); }), "qkv projection");
     }
     {
       AttnArgs at;
@@ -342,16 +388,16 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       at.k = (const char *)m->qkv + (size_t)D * asz; at.v = (const char *)m->qkv + (size_t)2 * D * asz;
       at.kv_bs = (int64_t)T * 3 * D; at.kv_rs = 3 * D; at.kv_index = nullptr; at.n_kv = a->n;
       at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
-      HIPCHK(launch_attention(act, at, s), "self-attention");
+      HIPCHK(timed(m, FLASHBON_SITE_ATTN_SELF, s, [&] { return launch_attention(act, at, s); }), "self-attention");
     }
     {
       EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.bo); e.gate = mod + 2 * D;
-      HIPCHK(launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.wo), e, s), "self-attn out projection");
+      HIPCHK(timed(m, FLASHBON_SITE_OUT, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.wo), e, s); }), "self-attn out projection");
     }
-    HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, nullptr, nullptr, m->a, s), "cross LN");
+    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, nullptr, nullptr, m->a, s); }), "cross LN");
     {
       EpiArgs e; e.out = m->qkv; e.ldo = D; e.bias = Bp(b.bqc);
-      HIPCHK(launch_linear(act, EPI_STORE, (int)M, D, D, m->a, Wp(b.wqc), e, s), "cross q projection");
+      HIPCHK(timed(m, FLASHBON_SITE_CROSS_Q, s, [&] { return launch_linear(act, EPI_STORE, (int)M, D, D, m->a, Wp(b.wqc), e, s); }), "cross q projection");
     }
     {
       const char *kv = (const char *)a->text_kv + (size_t)l * kv_block * asz;
@@ -361,32 +407,32 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       at.k = kv; at.v = kv + (size_t)D * asz; at.kv_bs = (int64_t)Lt * 2 * D; at.kv_rs = 2 * D;
       at.kv_index = m->d_cond; at.n_kv = NC;
       at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
-      HIPCHK(launch_attention(act, at, s), "cross-attention");
+      HIPCHK(timed(m, FLASHBON_SITE_ATTN_CROSS, s, [&] { return launch_attention(act, at, s); }), "cross-attention");
     }
     {
       EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.boc);
-      HIPCHK(launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.woc), e, s), "cross out projection");
+      HIPCHK(timed(m, FLASHBON_SITE_OUT_CROSS, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.woc), e, s); }), "cross out projection");
     }
-    HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 3 * D, mod + 4 * D, m->a, s), "adaLN 2");
+    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 3 * D, mod + 4 * D, m->a, s); }), "adaLN 2");
     {
       EpiArgs e; e.out = m->u; e.ldo = F; e.bias = Bp(b.b1);
-      HIPCHK(launch_linear(act, EPI_GELU, (int)M, F, D, m->a, Wp(b.w1), e, s), "mlp up");
+      HIPCHK(timed(m, FLASHBON_SITE_MLP_UP, s, [&] { return launch_linear(act, EPI_GELU, (int)M, F, D, m->a, Wp(b.w1), e, s); }), "mlp up");
     }
     {
       EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
       if (draft) e.cache = a->cache + ((int64_t)l * 3 + tr.slot) * MD;
-      HIPCHK(launch_linear(act, EPI_RESIDUAL, (int)M, D, F, m->u, Wp(b.w2), e, s), "mlp down");
+      HIPCHK(timed(m, FLASHBON_SITE_MLP_DOWN, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, F, m->u, Wp(b.w2), e, s); }), "mlp down");
     }
     if ((st = dump(l + 1)) != FLASHBON_OK) return st;
   }
 
   // head + unpatchify + Euler update of the latents
-  HIPCHK(launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, m->hmod, m->hmod + D, m->a, s), "head adaLN");
+  HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, m->hmod, m->hmod + D, m->a, s); }), "head adaLN");
   {
     EpiArgs e;
     e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;
     e.C = m->C; e.H = a->latent_h; e.W = a->latent_w; e.p = p; e.T = T;
-    HIPCHK(launch_linear(act, EPI_EULER, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s), "head + Euler");
+    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_EULER, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head + Euler");
   }
 
   // ---------------------------------------------------------------- commit host state
@@ -407,6 +453,27 @@ flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args)
 
 flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args) {
   return run_step((Model *)model, args, false);
+}
+
+flashbon_status flashbon_set_timing(void *model, uint32_t site_mask) {
+  if (!model) return fail(FLASHBON_EINVAL, "model is NULL");
+  if (site_mask >> FLASHBON_NUM_SITES) return fail(FLASHBON_EINVAL, "unknown site in mask");
+  ((Model *)model)->timing_mask = site_mask;
+  g_err.clear();
+  return FLASHBON_OK;
+}
+
+flashbon_status flashbon_read_timing(void *model, int32_t site, double *total_ms, int64_t *launches) {
+  if (!model || !total_ms || !launches) return fail(FLASHBON_EINVAL, "model, total_ms and launches are required");
+  if (site < 0 || site >= FLASHBON_NUM_SITES) return fail(FLASHBON_EINVAL, "unknown site");
+  Model *m = (Model *)model;
+  HIPCHK(harvest(m, site), "timing events");
+  *total_ms = m->sites[site].total_ms;
+  *launches = m->sites[site].launches;
+  m->sites[site].total_ms = 0;
+  m->sites[site].launches = 0;
+  g_err.clear();
+  return FLASHBON_OK;
 }
 
 }  // extern "C"

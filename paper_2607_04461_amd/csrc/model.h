@@ -38,6 +38,14 @@ struct Model {
   float *tf, *e1, *e, *m6, *bmods, *hmod;   // timestep path (fp32)
   int32_t *d_cond;
   std::vector<int32_t> last_cond;
+  // device timing of launch sites (flashbon_set_timing)
+  uint32_t timing_mask = 0;
+  struct Site {
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
+    double total_ms = 0;
+    int64_t launches = 0;
+  } sites[FLASHBON_NUM_SITES];
+  std::vector<hipEvent_t> spare_events;
 };
 
 flashbon_status fail(flashbon_status st, const std::string &msg);

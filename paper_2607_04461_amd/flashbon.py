@@ -20,6 +20,8 @@ OK, EINVAL, ESHAPE, ENOMEM, EHIP, ESTATE = 0, -1, -2, -3, -4, -5
 FP32, BF16 = 0, 1
 COMPUTE, SKIP, PROXY = 0, 1, 2
 EPI_STORE, EPI_GELU, EPI_STORE_F32, EPI_RESIDUAL = 0, 1, 2, 3
+SITES = ["qkv", "attn_self", "out", "cross_q", "attn_cross", "out_cross", "mlp_up", "mlp_down", "norm",
+         "proxy", "embed", "head", "time", "text"]
 
 
 class FlashbonError(RuntimeError):
@@ -62,7 +64,7 @@ class StepArgs(ctypes.Structure):
 EXPORTS = [
     "flashbon_weight_count", "flashbon_init_model", "flashbon_text_kv_bytes", "flashbon_cache_bytes",
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
-    "flashbon_last_error", "flashbon_op_linear", "flashbon_op_attention", "flashbon_op_ln_mod",
+    "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_attention", "flashbon_op_ln_mod",
     "flashbon_op_proxy",
 ]
 
@@ -97,6 +99,10 @@ def load() -> ctypes.CDLL:
     L.flashbon_plan_step.argtypes = [i32, ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_uint8),
                                      ctypes.POINTER(CacheMeta), f32, ctypes.POINTER(TraceEntry)]
     L.flashbon_plan_step.restype = i32
+    L.flashbon_set_timing.argtypes = [vp, ctypes.c_uint32]
+    L.flashbon_set_timing.restype = i32
+    L.flashbon_read_timing.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+    L.flashbon_read_timing.restype = i32
     L.flashbon_last_error.argtypes = []
     L.flashbon_last_error.restype = ctypes.c_char_p
     L.flashbon_op_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
@@ -231,6 +237,22 @@ def flashbon_plan_step(skip, proxy, meta, t_cur: float, trace=None):
         trace = new_trace(L)
     _check(load().flashbon_plan_step(L, skp, pxp, meta, float(t_cur), trace), "flashbon_plan_step")
     return trace
+
+
+def flashbon_set_timing(model: int, sites) -> None:
+    """Time the named launch sites (see SITES) on later steps; empty = off."""
+    mask = 0
+    for name in sites:
+        mask |= 1 << SITES.index(name)
+    _check(load().flashbon_set_timing(model, mask), "flashbon_set_timing")
+
+
+def flashbon_read_timing(model: int, site: str):
+    """(total device ms, launches) of one site since the last read."""
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    _check(load().flashbon_read_timing(model, SITES.index(site), ctypes.byref(ms), ctypes.byref(n)),
+           "flashbon_read_timing")
+    return ms.value, n.value
 
 
 # --------------------------------------------------------------------------- kernel-level entry points
