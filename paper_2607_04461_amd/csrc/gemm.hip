@@ -1,11 +1,16 @@
 // Linear layers of the DiT step: C[m][n] = sum_k A[m][k] Wt[n][k] with fused epilogues.
 //   * k_linear_mfma: bf16 operands on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16), fp32
-//     accumulation, LDS-staged 128x128x64 tiles with an XOR swizzle, register prefetch of the next
-//     K tile.  Operands are swapped (the weight tile feeds the MFMA "A" side) so that every lane
-//     ends up owning four consecutive output columns of one row, which the epilogues store as one
-//     vector.
+//     accumulation.  Workgroup tiles of 256x256 (8 waves of 128x64) or 128x128 (4 waves of 64x64),
+//     chosen per shape; K tiles of 64 staged through double-buffered, XOR-swizzled LDS with the next
+//     tile(s) prefetched into registers (one barrier per K tile); XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) so that every lane ends
+//     up owning four consecutive output columns of one row, which the epilogues store as one vector.
 //   * k_linear_valu: fp32 (or bf16) operands on the vector ALUs, 64x64 tiles; used by the fp32 mode
 //     and for shapes the MFMA tiling does not take.
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -62,99 +67,151 @@ __device__ __forceinline__ void epilogue4(const EpiArgs &e, int m, int n, float 
 
 // ---------------------------------------------------------------------------------- MFMA path
 namespace mf {
-constexpr int BM = 128;  // activation rows per workgroup
-constexpr int BN = 128;  // weight rows (output columns) per workgroup
 constexpr int BK = 64;
-constexpr int THREADS = 256;
-// LDS tile: [rows][64] bf16 = 8 chunks of 16 B per row, chunk c of row r stored at c ^ swz(r).
+// A workgroup is a WGM x WGN grid of waves, each computing a (16 WTM) x (16 WTN) tile of C.
+// LDS tile: [rows][64] bf16 = 8 chunks of 16 B per row, chunk c of row r stored at c ^ swz(r): the
+// 16 lanes of one ds_read_b128 phase (16 consecutive rows, one chunk) then cover all 64 banks.
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
-__device__ __forceinline__ int lds_off(int r, int c) { return r * 64 + ((c ^ swz(r)) << 3); }
+__device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ swz(r)) << 3); }
+
+// Workgroup id -> (m tile, n tile).  Workgroups are dispatched round-robin over the 8 XCDs; each XCD
+// is given a contiguous range of tiles, and tiles are ordered in groups of GROUP_M m-tiles sweeping
+// all n-tiles, so the workgroups resident on one XCD share A rows and W rows in that XCD's L2.
+constexpr int GROUP_M = 8;
+__device__ __forceinline__ void tile_of(int bid, int MT, int NT, int &mt, int &nt) {
+  const int total = MT * NT;
+  const int xcd = bid & 7, local = bid >> 3;
+  const int base = total >> 3, rem = total & 7;
+  const int t = xcd * base + min(xcd, rem) + local;
+  const int per_group = GROUP_M * NT;
+  const int group = t / per_group, first_m = group * GROUP_M;
+  const int gm = min(MT - first_m, GROUP_M);
+  const int r = t - group * per_group;
+  mt = first_m + r % gm;
+  nt = r / gm;
+}
 }  // namespace mf
 
-template <int EPI, typename TO>
-__global__ __launch_bounds__(256) void k_linear_mfma(int M, int N, int K,
-                                                     const bf16 *__restrict__ A,
-                                                     const bf16 *__restrict__ Wt, EpiArgs e) {
+template <int WTM, int WTN, int WGM, int WGN, int DEPTH, int EPI, typename TO>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N, int K,
+                                                                   const bf16 *__restrict__ A,
+                                                                   const bf16 *__restrict__ Wt,
+                                                                   EpiArgs e, int MT, int NT) {
   using namespace mf;
-  __shared__ __attribute__((aligned(16))) bf16 sA[BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sW[BN * BK];
+  constexpr int THREADS = 64 * WGM * WGN, ROWS = THREADS / 8;  // rows covered per load pass
+  constexpr int BM = 16 * WTM * WGM, BN = 16 * WTN * WGN;
+  constexpr int LA = BM / ROWS, LW = BN / ROWS;  // 16-byte chunks per thread per K tile
+  constexpr int STAGE = (BM + BN) * BK;  // elements of one LDS stage: A tile then W tile
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;  // wave tile: rows 64*wm.., cols 64*wn..
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int wm = wave / WGN, wn = wave % WGN;
+  int mt, nt;
+  tile_of(blockIdx.x, MT, NT, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
 
-  // global -> register staging: each thread moves 4 chunks of A and 4 of W per K tile
-  const int ld_r = tid >> 3, ld_c = tid & 7;  // row 0..31 (+32 i), chunk 0..7
-  const bf16 *pa[4];
-  const bf16 *pw[4];
+  const int ld_r = tid >> 3, ld_c = tid & 7;  // row 0..ROWS-1 (+ROWS i), chunk 0..7
+  // per-row element offsets (rows past the edge are clamped; their results are never stored)
+  const bf16 *Ab = A + (int64_t)m0 * K + ld_c * 8;
+  const bf16 *Wb = Wt + (int64_t)n0 * K + ld_c * 8;
+  uint32_t oa[LA], ow[LW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int ra = min(m0 + ld_r + 32 * i, M - 1);
-    int rw = min(n0 + ld_r + 32 * i, N - 1);
-    pa[i] = A + (int64_t)ra * K + ld_c * 8;
-    pw[i] = Wt + (int64_t)rw * K + ld_c * 8;
-  }
-  u32x4 ra[4], rw[4];
-  auto load_tile = [&](int k0) {
-    const bool ok = (k0 + ld_c * 8) < K;
+  for (int i = 0; i < LA; ++i) oa[i] = (uint32_t)(min(ld_r + ROWS * i, M - 1 - m0) * K);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = ok ? *reinterpret_cast<const u32x4 *>(pa[i] + k0) : u32x4{0, 0, 0, 0};
-      rw[i] = ok ? *reinterpret_cast<const u32x4 *>(pw[i] + k0) : u32x4{0, 0, 0, 0};
-    }
+  for (int i = 0; i < LW; ++i) ow[i] = (uint32_t)(min(ld_r + ROWS * i, N - 1 - n0) * K);
+  // Staging registers: DEPTH sets, so that a K tile's global loads are issued DEPTH tiles before
+  // they are stored to LDS.  K tail: chunks past K are loaded from a valid address and zeroed at
+  // store time (a select, so freshly issued loads are never waited on early).
+  u32x4 ra[DEPTH][LA], rw[DEPTH][LW];
+  bool okk[DEPTH];
+  auto load_tile = [&](int k0, int set) {
+    okk[set] = (k0 + ld_c * 8) < K;
+    const int kk = okk[set] ? k0 : K - 8 - ld_c * 8;
+#pragma unroll
+    for (int i = 0; i < LA; ++i) ra[set][i] = *reinterpret_cast<const u32x4 *>(Ab + oa[i] + kk);
+#pragma unroll
+    for (int i = 0; i < LW; ++i) rw[set][i] = *reinterpret_cast<const u32x4 *>(Wb + ow[i] + kk);
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](bf16 *sA, int set) {
+    bf16 *sW = sA + BM * BK;
+    const u32x4 z = {0, 0, 0, 0};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int r = ld_r + 32 * i;
-      *reinterpret_cast<u32x4 *>(&sA[lds_off(r, ld_c)]) = ra[i];
-      *reinterpret_cast<u32x4 *>(&sW[lds_off(r, ld_c)]) = rw[i];
-    }
+    for (int i = 0; i < LA; ++i) *reinterpret_cast<u32x4 *>(&sA[lds_off(ld_r + ROWS * i, ld_c)]) = okk[set] ? ra[set][i] : z;
+#pragma unroll
+    for (int i = 0; i < LW; ++i) *reinterpret_cast<u32x4 *>(&sW[lds_off(ld_r + ROWS * i, ld_c)]) = okk[set] ? rw[set][i] : z;
   };
 
-  f32x4 acc[4][4];  // [n tile i][m tile j]
+  f32x4 acc[WTN][WTM];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < WTN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+    for (int j = 0; j < WTM; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
 
-  const int fr = lane & 15, fq = lane >> 4;  // fragment row within 16, k-chunk quarter
-  const int ktiles = (K + BK - 1) / BK;
-  load_tile(0);
-  for (int kt = 0; kt < ktiles; ++kt) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kt + 1 < ktiles) load_tile((kt + 1) * BK);
+  const int fr = lane & 15, fq = lane >> 4;
+  const int rowW = 16 * WTN * wn + fr, rowA = 16 * WTM * wm + fr;
+  // All fragments of a 32-wide K substep are requested before its MFMA chain starts, so the LDS
+  // latency is paid once per substep rather than once per few MFMAs.
+  auto compute = [&](const bf16 *sA) {
+    const bf16 *sW = sA + BM * BK;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 fw[4], fa[4];
+      bf16x8 fw[WTN], fa[WTM];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int r = 64 * wn + 16 * i + fr;
-        fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(r, fq + 4 * ks)]);
-      }
+      for (int i = 0; i < WTN; ++i)
+        fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(rowW + 16 * i, fq + 4 * ks)]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int r = 64 * wm + 16 * j + fr;
-        fa[j] = *reinterpret_cast<const bf16x8 *>(&sA[lds_off(r, fq + 4 * ks)]);
-      }
+      for (int j = 0; j < WTM; ++j)
+        fa[j] = *reinterpret_cast<const bf16x8 *>(&sA[lds_off(rowA + 16 * j, fq + 4 * ks)]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < WTM; ++j)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int i = 0; i < WTN; ++i)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
+  };
+
+  const int ktiles = (K + BK - 1) / BK;
+  if constexpr (DEPTH == 1) {
+    load_tile(0, 0);
+    store_tile(smem, 0);
+    __syncthreads();
+    for (int kt = 0; kt < ktiles; ++kt) {
+      const bool more = kt + 1 < ktiles;
+      if (more) load_tile((kt + 1) * BK, 0);
+      compute(smem + (kt & 1) * STAGE);
+      if (more) store_tile(smem + ((kt + 1) & 1) * STAGE, 0);
+      __syncthreads();
+    }
+  } else {
+    // tile t is loaded into register set t % 2 during iteration t - 2 and stored during t - 1
+    load_tile(0, 0);
+    if (ktiles > 1) load_tile(BK, 1);
+    store_tile(smem, 0);
+    __syncthreads();
+    auto iter = [&](int kt, int set_next) {   // set_next = (kt + 1) % 2, compile-time per call site
+      if (kt + 2 < ktiles) load_tile((kt + 2) * BK, set_next ^ 1);
+      compute(smem + (kt & 1) * STAGE);
+      if (kt + 1 < ktiles) store_tile(smem + ((kt + 1) & 1) * STAGE, set_next);
+      __syncthreads();
+    };
+    int kt = 0;
+    for (; kt + 1 < ktiles; kt += 2) {
+      iter(kt, 1);
+      iter(kt + 1, 0);
+    }
+    if (kt < ktiles) iter(kt, 1);
   }
 
-  // acc[i][j] lane layout (C^T tile 16x16): column = m index (lane & 15), rows = 4 consecutive n.
+  // acc[i][j] (C^T tile 16x16): lane column = m index (lane & 15), rows = 4 consecutive n.
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = n0 + 64 * wn + 16 * i + 4 * fq;
+  for (int i = 0; i < WTN; ++i) {
+    const int n = n0 + 16 * WTN * wn + 16 * i + 4 * fq;
     if (n >= N) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = m0 + 64 * wm + 16 * j + fr;
+    for (int j = 0; j < WTM; ++j) {
+      const int m = m0 + 16 * WTM * wm + 16 * j + fr;
       if (m < M) epilogue4<EPI, TO>(e, m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
@@ -203,18 +260,46 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
   }
 }
 
+// Tile choice: a 256x256 workgroup tile (8 waves, 2 per SIMD) or a 128x128 one (4 waves, two
+// workgroups per CU, loads issued two K tiles ahead).  Estimated time = rounds of resident
+// workgroups x work per round / relative efficiency; the efficiencies are measured on MI355X
+// (the 128x128 tile reaches 0.88 of the 256x256 tile's throughput per CU).
+static bool pick_big_tile(int M, int N) {
+  const char *force = getenv("FLASHBON_LINEAR_TILE");  // "256x256" or "128x128": tests and tuning
+  if (force) return strcmp(force, "128x128") != 0;
+  const double t256 = ceil((double)((M + 255) / 256) * ((N + 255) / 256) / 256.0) * 256.0 * 256.0;
+  const double t128 = ceil((double)((M + 127) / 128) * ((N + 127) / 128) / 512.0) * 2.0 * 128.0 * 128.0 / 0.88;
+  return t256 <= t128;
+}
+
+template <int WTM, int WTN, int WGM, int WGN, int EPI, int DEPTH>
+static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
+                              hipStream_t s) {
+  constexpr int BM = 16 * WTM * WGM, BN = 16 * WTN * WGN;
+  const size_t lds = (size_t)2 * (BM + BN) * mf::BK * sizeof(bf16);
+  auto kern = k_linear_mfma<WTM, WTN, WGM, WGN, DEPTH, EPI, bf16>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int MT = (M + BM - 1) / BM, NT = (N + BN - 1) / BN;
+  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(64 * WGM * WGN), lds, s, M, N, K, (const bf16 *)A,
+                     (const bf16 *)Wt, e, MT, NT);
+  return hipGetLastError();
+}
+
 template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
-    dim3 grid((M + mf::BM - 1) / mf::BM, (N + mf::BN - 1) / mf::BN);
-    hipLaunchKernelGGL((k_linear_mfma<EPI, bf16>), grid, dim3(mf::THREADS), 0, s, M, N, K,
-                       (const bf16 *)A, (const bf16 *)Wt, e);
-  } else {
-    dim3 grid((M + 63) / 64, (N + 63) / 64);
-    hipLaunchKernelGGL((k_linear_valu<float, EPI, float>), grid, dim3(256), 0, s, M, N, K,
-                       (const float *)A, (const float *)Wt, e);
+    if (pick_big_tile(M, N)) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+    return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
   }
+  dim3 grid((M + 63) / 64, (N + 63) / 64);
+  hipLaunchKernelGGL((k_linear_valu<float, EPI, float>), grid, dim3(256), 0, s, M, N, K,
+                     (const float *)A, (const float *)Wt, e);
   return hipGetLastError();
 }
 

@@ -83,6 +83,32 @@ def test_linear_small(dtype, M, N, K, epi):
     assert rel_l2(got, ref) <= tol
 
 
+@pytest.mark.parametrize("tile", ["256x256", "128x128"])
+@pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8)])
+@pytest.mark.parametrize("epi", ["gelu", "residual"])
+def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
+    """Both MFMA tilings (forced) on ragged M, N and K tails, against the oracle."""
+    monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
+    F = fb()
+    A = _operand((M, K), 71, "bf16")
+    W = _operand((N, K), 72, "bf16", 0.05)
+    bias = synth.random_matrix((N,), 73)
+    ref = odit.linear(A.astype(np.float64), W, bias)
+    if epi == "gelu":
+        out = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        F.flashbon_op_linear(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"), F.EPI_GELU, out)
+        ref, tol = odit.gelu_tanh(ref), 6e-3
+    else:
+        h0 = synth.random_matrix((M, N), 74)
+        gate = synth.random_matrix((N,), 75)
+        out = _dev(h0, "fp32")
+        F.flashbon_op_linear(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"),
+                             F.EPI_RESIDUAL, out, _dev(gate, "fp32"))
+        ref, tol = h0 + gate * ref, 2e-6
+    torch.cuda.synchronize()
+    assert rel_l2(out.float().cpu().numpy(), ref) <= tol
+
+
 @pytest.mark.parametrize("M,N,K", [(24960, 4608, 1536), (24960, 8960, 1536), (24960, 1536, 8960),
                                    (24960, 64, 1536), (16384, 15360, 5120)])
 def test_linear_full_shapes_bf16_sampled_rows(M, N, K):
