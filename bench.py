@@ -50,6 +50,23 @@ def draft_flops(wl, traces):
     return total * wl.n
 
 
+def recorded_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter summary, or None if
+    the kernel source has changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "linear_mlp_up_traffic.md")
+    src = os.path.join(ROOT, "paper_2607_04461_amd", "csrc", "gemm.hip")
+    try:
+        txt = open(path).read()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        rec = re.search(r"gemm_source_sha256 \| ([0-9a-f]{64})", txt).group(1)
+        val = float(re.search(r"traffic_bytes_per_launch \| ([0-9.e+]+)", txt).group(1))
+    except (OSError, AttributeError, ValueError):
+        return None
+    return val if rec == sha else None
+
+
 def cpu_baseline(wl, W, z0, text):
     """The oracle, as it stands, on candidate 0: step 0 (computed blocks) and step 1 (proxies),
     extrapolated to the draft's steps."""
@@ -89,6 +106,9 @@ def main():
     ap.add_argument("--workload", default="wan1.3b_pool16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-breakdown", action="store_true")
+    ap.add_argument("--no-refine", action="store_true", help="skip timing the refinement")
+    ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
+                    help="also run a plain device copy of this many MiB three times (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the draft pool runs on a single MI355X and no multi-GPU path "
@@ -168,17 +188,28 @@ def main():
         fb.flashbon_set_timing(pool.model, [])
 
     # refinement of the selected candidate (seeded stand-in verifier score, argmax, lowest index on ties)
-    scores = synth.make_scores(wl.n, seed=7)
-    sel = int(np.argmax(scores))
-    one_draft()
-    lat = pool.latents[sel:sel + 1].clone()
-    cond = wl.cond_index()[sel:sel + 1]
-    torch.cuda.synchronize()
-    r0 = time.time()
-    for k in range(wl.steps_draft, wl.steps_total):
-        pool.refine_step(k, latents=lat, cond_index=cond)
-    torch.cuda.synchronize()
-    refine_ms = (time.time() - r0) * 1e3
+    refine_ms = None
+    if not args.no_refine:
+        scores = synth.make_scores(wl.n, seed=7)
+        sel = int(np.argmax(scores))
+        one_draft()
+        lat = pool.latents[sel:sel + 1].clone()
+        cond = wl.cond_index()[sel:sel + 1]
+        torch.cuda.synchronize()
+        r0 = time.time()
+        for k in range(wl.steps_draft, wl.steps_total):
+            pool.refine_step(k, latents=lat, cond_index=cond)
+        torch.cuda.synchronize()
+        refine_ms = round((time.time() - r0) * 1e3, 2)
+
+    if args.calibration_copy:
+        n = args.calibration_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     result = {
         "metric": "draft candidates/sec (1.3B-shaped DiT, N=16) + % bf16 MFMA peak",
@@ -208,11 +239,12 @@ def main():
             "kernel": "k_linear_mfma<EPI_GELU> (MLP up-projection, M=%d N=%d K=%d)" % (M, wl.shape.mlp_hidden,
                                                                                    wl.shape.hidden),
             "bound": "mfma", "achieved": round(up_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
+            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_ms": round(up_avg_ms, 4), "launches": up_n,
         },
         "text_prep_ms": round(text_ms, 3),
-        "refine_ms": round(refine_ms, 2),
+        "refine_ms": refine_ms,
         "refine_steps": wl.steps_total - wl.steps_draft,
         "site_breakdown_one_draft": breakdown,
     }

@@ -6,10 +6,9 @@
 namespace fb {
 
 // ------------------------------------------------------------------------------------------ adaLN
-// One wave per row; the row stays in registers between the two statistics passes (D <= 64*4*MAXV).
-constexpr int LN_MAXV = 24;  // float4 per lane -> D <= 6144
-
-template <typename T>
+// One wave per row; the row stays in registers between the two statistics passes.  NV = float4s
+// per lane, a compile-time bound (D <= 256 NV), so register use matches the row length.
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void k_ln_mod(int M, int D, float eps, const float *__restrict__ x,
                                                 const float *__restrict__ shift,
                                                 const float *__restrict__ scale, T *__restrict__ out) {
@@ -18,20 +17,18 @@ __global__ __launch_bounds__(256) void k_ln_mod(int M, int D, float eps, const f
   if (row >= M) return;
   const float4 *xr = reinterpret_cast<const float4 *>(x + row * D);
   const int nv = D >> 2;
-  float4 v[LN_MAXV];
+  float4 v[NV];
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i) {
+  for (int i = 0; i < NV; ++i) {
     int c = lane + i * 64;
-    if (c < nv) {
-      v[i] = xr[c];
-      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
-    }
+    v[i] = c < nv ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   }
   const float mean = wave_sum(s) / (float)D;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i) {
+  for (int i = 0; i < NV; ++i) {
     int c = lane + i * 64;
     if (c < nv) {
       float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
@@ -41,7 +38,7 @@ __global__ __launch_bounds__(256) void k_ln_mod(int M, int D, float eps, const f
   const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
   T *orow = out + row * D;
 #pragma unroll
-  for (int i = 0; i < LN_MAXV; ++i) {
+  for (int i = 0; i < NV; ++i) {
     int c = lane + i * 64;
     if (c < nv) {
       float r[4] = {(v[i].x - mean) * rstd, (v[i].y - mean) * rstd, (v[i].z - mean) * rstd,
@@ -64,14 +61,32 @@ __global__ __launch_bounds__(256) void k_ln_mod(int M, int D, float eps, const f
   }
 }
 
+template <typename T>
+static hipError_t launch_ln_t(int M, int D, float eps, const float *x, const float *shift,
+                              const float *scale, void *out, hipStream_t s) {
+  dim3 grid((M + 3) / 4), block(256);
+  const int nv = (D / 4 + 63) / 64;
+#define FB_LN(NVC)                                                                                  \
+  case NVC:                                                                                         \
+    hipLaunchKernelGGL((k_ln_mod<T, NVC>), grid, block, 0, s, M, D, eps, x, shift, scale, (T *)out); \
+    break;
+  switch (nv) {
+    FB_LN(1) FB_LN(2) FB_LN(3) FB_LN(4) FB_LN(5) FB_LN(6) FB_LN(8) FB_LN(12) FB_LN(16) FB_LN(20) FB_LN(24)
+    default:
+      if (nv <= 8) { hipLaunchKernelGGL((k_ln_mod<T, 8>), grid, block, 0, s, M, D, eps, x, shift, scale, (T *)out); }
+      else if (nv <= 12) { hipLaunchKernelGGL((k_ln_mod<T, 12>), grid, block, 0, s, M, D, eps, x, shift, scale, (T *)out); }
+      else if (nv <= 16) { hipLaunchKernelGGL((k_ln_mod<T, 16>), grid, block, 0, s, M, D, eps, x, shift, scale, (T *)out); }
+      else if (nv <= 20) { hipLaunchKernelGGL((k_ln_mod<T, 20>), grid, block, 0, s, M, D, eps, x, shift, scale, (T *)out); }
+      else { hipLaunchKernelGGL((k_ln_mod<T, 24>), grid, block, 0, s, M, D, eps, x, shift, scale, (T *)out); }
+  }
+#undef FB_LN
+  return hipGetLastError();
+}
+
 hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, const float *shift,
                          const float *scale, void *out, hipStream_t s) {
-  dim3 grid((M + 3) / 4), block(256);
-  if (t == ACT_BF16)
-    hipLaunchKernelGGL(k_ln_mod<bf16>, grid, block, 0, s, M, D, eps, x, shift, scale, (bf16 *)out);
-  else
-    hipLaunchKernelGGL(k_ln_mod<float>, grid, block, 0, s, M, D, eps, x, shift, scale, (float *)out);
-  return hipGetLastError();
+  if (t == ACT_BF16) return launch_ln_t<bf16>(M, D, eps, x, shift, scale, out, s);
+  return launch_ln_t<float>(M, D, eps, x, shift, scale, out, s);
 }
 
 // ------------------------------------------------------------------------------ activation proxy

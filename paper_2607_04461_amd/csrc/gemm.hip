@@ -264,9 +264,11 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
 // workgroups per CU, loads issued two K tiles ahead).  Estimated time = rounds of resident
 // workgroups x work per round / relative efficiency; the efficiencies are measured on MI355X
 // (the 128x128 tile reaches 0.88 of the 256x256 tile's throughput per CU).
-static bool pick_big_tile(int M, int N) {
+static bool pick_big_tile(int M, int N, int K) {
   const char *force = getenv("FLASHBON_LINEAR_TILE");  // "256x256" or "128x128": tests and tuning
   if (force) return strcmp(force, "128x128") != 0;
+  // long K amortises the big tile's prologue/epilogue (measured: 24960 x 1536 x 8960 runs 6% faster)
+  if (K >= 4096 && N >= 1024 && M >= 4096) return true;
   const double t256 = ceil((double)((M + 255) / 256) * ((N + 255) / 256) / 256.0) * 256.0 * 256.0;
   const double t128 = ceil((double)((M + 127) / 128) * ((N + 127) / 128) / 512.0) * 2.0 * 128.0 * 128.0 / 0.88;
   return t256 <= t128;
@@ -294,7 +296,7 @@ template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
-    if (pick_big_tile(M, N)) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+    if (pick_big_tile(M, N, K)) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
     return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
   }
   dim3 grid((M + 63) / 64, (N + 63) / 64);
