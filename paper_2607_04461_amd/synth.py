@@ -98,6 +98,11 @@ WORKLOADS: Dict[str, Workload] = {
     # 1.3B-shaped large pool: N=64 at 1024 tokens, 4 prompts x 16, 12 of 50 steps, varying masks
     "wan1.3b_pool64": Workload("wan1.3b_pool64", WAN_1_3B, n=64, latent_h=64, latent_w=64,
                                text_len=512, n_cond=4, steps_total=50, steps_draft=12, dtype="bf16"),
+    # 14B-shaped layers (D=5120, 40 heads, MLP 13824, 4096 tokens, N=4) in a 2-block model, so the
+    # oracle can follow a full step at these shapes in seconds
+    "wan14b_2block": Workload("wan14b_2block", dataclasses.replace(WAN_14B, num_blocks=2), n=4,
+                              latent_h=128, latent_w=128, text_len=512, n_cond=1, steps_total=50,
+                              steps_draft=2, dtype="bf16"),
     # mid-size parity pool (head_dim 128, ragged token count 130, 2 prompts)
     "mid": Workload("mid", MID, n=3, latent_h=10, latent_w=52, text_len=40, n_cond=2,
                     steps_total=8, steps_draft=8, dtype="fp32"),
@@ -128,6 +133,10 @@ def step_masks(name: str, num_blocks: int, k: int) -> Tuple[np.ndarray, np.ndarr
         skip[perm[:n_k]] = 1
         if k % 2 == 1:
             proxy[:] = 1
+    elif name == "wan14b_2block":
+        if k == 1:
+            skip[1] = 1
+            proxy[0] = 1
     elif name == "mid":
         # exercises the empty-cache fallback, warm-up orders 0/1/2, dead and live proxies,
         # skip-over-proxy and proxies over unequally spaced cached steps
