@@ -1,8 +1,9 @@
 // Linear layers of the DiT step: C[m][n] = sum_k A[m][k] Wt[n][k] with fused epilogues.
-//   * k_linear_mfma: bf16 operands on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16), fp32
-//     accumulation.  Workgroup tiles of 256x256 (8 waves of 128x64) or 128x128 (4 waves of 64x64),
-//     chosen per shape; K tiles of 64 staged through double-buffered, XOR-swizzled LDS with the next
-//     tile(s) prefetched into registers (one barrier per K tile); XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) so that every lane ends
+//   * k_linear_ilv / k_linear_mfma: bf16 operands on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16),
+//     fp32 accumulation.  Workgroup tiles of 256x256 (8 waves of 128x64; explicitly interleaved
+//     schedule when K % 64 == 0) or 128x128 (4 waves of 64x64, loads two K tiles ahead), chosen per
+//     shape; K tiles of 64 staged through double-buffered, XOR-swizzled LDS (one barrier per K
+//     tile); XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) so that every lane ends
 //     up owning four consecutive output columns of one row, which the epilogues store as one vector.
 //   * k_linear_valu: fp32 (or bf16) operands on the vector ALUs, 64x64 tiles; used by the fp32 mode
 //     and for shapes the MFMA tiling does not take.
@@ -92,7 +93,7 @@ __device__ __forceinline__ void tile_of(int bid, int MT, int NT, int &mt, int &n
 }
 }  // namespace mf
 
-template <int WTM, int WTN, int WGM, int WGN, int DEPTH, int EPI, typename TO>
+template <int WTM, int WTN, int WGM, int WGN, int DEPTH, bool KTAIL, int EPI, typename TO>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N, int K,
                                                                    const bf16 *__restrict__ A,
                                                                    const bf16 *__restrict__ Wt,
@@ -101,31 +102,38 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
   constexpr int THREADS = 64 * WGM * WGN, ROWS = THREADS / 8;  // rows covered per load pass
   constexpr int BM = 16 * WTM * WGM, BN = 16 * WTN * WGN;
   constexpr int LA = BM / ROWS, LW = BN / ROWS;  // 16-byte chunks per thread per K tile
-  constexpr int STAGE = (BM + BN) * BK;  // elements of one LDS stage: A tile then W tile
+  constexpr int STAGE = (BM + BN) * BK;          // elements of one LDS stage: A tile then W tile
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
-  int mt, nt;
-  tile_of(blockIdx.x, MT, NT, mt, nt);
-  const int m0 = mt * BM, n0 = nt * BN;
-
+  const int total = MT * NT;
   const int ld_r = tid >> 3, ld_c = tid & 7;  // row 0..ROWS-1 (+ROWS i), chunk 0..7
-  // per-row element offsets (rows past the edge are clamped; their results are never stored)
-  const bf16 *Ab = A + (int64_t)m0 * K + ld_c * 8;
-  const bf16 *Wb = Wt + (int64_t)n0 * K + ld_c * 8;
+
+  // Per-tile load addressing (rows past the edge are clamped; their results are never stored).
+  int m0 = 0, n0 = 0;
+  const bf16 *Ab = A, *Wb = Wt;
   uint32_t oa[LA], ow[LW];
+  auto setup_tile = [&](int t) {
+    int mt, nt;
+    tile_of(t, MT, NT, mt, nt);
+    m0 = mt * BM;
+    n0 = nt * BN;
+    Ab = A + (int64_t)m0 * K + ld_c * 8;
+    Wb = Wt + (int64_t)n0 * K + ld_c * 8;
 #pragma unroll
-  for (int i = 0; i < LA; ++i) oa[i] = (uint32_t)(min(ld_r + ROWS * i, M - 1 - m0) * K);
+    for (int i = 0; i < LA; ++i) oa[i] = (uint32_t)(min(ld_r + ROWS * i, M - 1 - m0) * K);
 #pragma unroll
-  for (int i = 0; i < LW; ++i) ow[i] = (uint32_t)(min(ld_r + ROWS * i, N - 1 - n0) * K);
+    for (int i = 0; i < LW; ++i) ow[i] = (uint32_t)(min(ld_r + ROWS * i, N - 1 - n0) * K);
+  };
+
   // Staging registers: DEPTH sets, so that a K tile's global loads are issued DEPTH tiles before
   // they are stored to LDS.  K tail: chunks past K are loaded from a valid address and zeroed at
   // store time (a select, so freshly issued loads are never waited on early).
   u32x4 ra[DEPTH][LA], rw[DEPTH][LW];
   bool okk[DEPTH];
   auto load_tile = [&](int k0, int set) {
-    okk[set] = (k0 + ld_c * 8) < K;
+    okk[set] = !KTAIL || (k0 + ld_c * 8) < K;
     const int kk = okk[set] ? k0 : K - 8 - ld_c * 8;
 #pragma unroll
     for (int i = 0; i < LA; ++i) ra[set][i] = *reinterpret_cast<const u32x4 *>(Ab + oa[i] + kk);
@@ -136,17 +144,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
     bf16 *sW = sA + BM * BK;
     const u32x4 z = {0, 0, 0, 0};
 #pragma unroll
-    for (int i = 0; i < LA; ++i) *reinterpret_cast<u32x4 *>(&sA[lds_off(ld_r + ROWS * i, ld_c)]) = okk[set] ? ra[set][i] : z;
+    for (int i = 0; i < LA; ++i) *reinterpret_cast<u32x4 *>(&sA[lds_off(ld_r + ROWS * i, ld_c)]) = (!KTAIL || okk[set]) ? ra[set][i] : z;
 #pragma unroll
-    for (int i = 0; i < LW; ++i) *reinterpret_cast<u32x4 *>(&sW[lds_off(ld_r + ROWS * i, ld_c)]) = okk[set] ? rw[set][i] : z;
+    for (int i = 0; i < LW; ++i) *reinterpret_cast<u32x4 *>(&sW[lds_off(ld_r + ROWS * i, ld_c)]) = (!KTAIL || okk[set]) ? rw[set][i] : z;
   };
 
   f32x4 acc[WTN][WTM];
-#pragma unroll
-  for (int i = 0; i < WTN; ++i)
-#pragma unroll
-    for (int j = 0; j < WTM; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
-
   const int fr = lane & 15, fq = lane >> 4;
   const int rowW = 16 * WTN * wn + fr, rowA = 16 * WTM * wm + fr;
   // All fragments of a 32-wide K substep are requested before its MFMA chain starts, so the LDS
@@ -171,9 +174,30 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  // acc[i][j] (C^T tile 16x16): lane column = m index (lane & 15), rows = 4 consecutive n.
+  auto epilogue = [&](int em0, int en0) {
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) {
+      const int n = en0 + 16 * WTN * wn + 16 * i + 4 * fq;
+      if (n >= N) continue;
+#pragma unroll
+      for (int j = 0; j < WTM; ++j) {
+        const int m = em0 + 16 * WTM * wm + 16 * j + fr;
+        if (m < M) epilogue4<EPI, TO>(e, m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
+    }
+  };
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int i = 0; i < WTN; ++i)
+#pragma unroll
+      for (int j = 0; j < WTM; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+  };
 
   const int ktiles = (K + BK - 1) / BK;
   if constexpr (DEPTH == 1) {
+    setup_tile(blockIdx.x);
+    zero_acc();
     load_tile(0, 0);
     store_tile(smem, 0);
     __syncthreads();
@@ -184,8 +208,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
       if (more) store_tile(smem + ((kt + 1) & 1) * STAGE, 0);
       __syncthreads();
     }
+    epilogue(m0, n0);
   } else {
     // tile t is loaded into register set t % 2 during iteration t - 2 and stored during t - 1
+    setup_tile(blockIdx.x);
+    zero_acc();
     load_tile(0, 0);
     if (ktiles > 1) load_tile(BK, 1);
     store_tile(smem, 0);
@@ -202,9 +229,116 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
       iter(kt + 1, 0);
     }
     if (kt < ktiles) iter(kt, 1);
+    epilogue(m0, n0);
   }
+}
 
-  // acc[i][j] (C^T tile 16x16): lane column = m index (lane & 15), rows = 4 consecutive n.
+// ------------------------------------------------------- MFMA path, explicitly interleaved 256x256
+// 8 waves of 128 (m) x 64 (n), K tiles of 64 (K % 64 == 0), register-staged double-buffered LDS.
+// The instruction order inside a K tile is pinned: the next tile's global loads first; substep-1 W
+// fragments; substep 0's MFMAs with substep-1 A fragments read in place between MFMA groups (so
+// each fragment register is refilled right after its last use); half of substep 1; the staged
+// stores and the barrier; the next tile's substep-0 fragments, again refilled in place, overlapping
+// the second half of substep 1.  LDS latency is then hidden behind MFMA groups instead of exposed
+// at each substep, and the barrier drain overlaps 16 MFMAs.
+template <int EPI, typename TO>
+__global__ __launch_bounds__(512, 1) void k_linear_ilv(int M, int N, int K, const bf16 *__restrict__ A,
+                                                const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT) {
+  using namespace mf;
+  constexpr int BM = 256, BN = 256, WTM = 8, WTN = 4, ROWS = 64, LA = 4, LW = 4;
+  constexpr int STAGE = (BM + BN) * BK;
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  int mt, nt;
+  tile_of(blockIdx.x, MT, NT, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int ld_r = tid >> 3, ld_c = tid & 7;
+  const bf16 *Ab = A + (int64_t)m0 * K + ld_c * 8, *Wb = Wt + (int64_t)n0 * K + ld_c * 8;
+  uint32_t oa[LA], ow[LW];
+#pragma unroll
+  for (int i = 0; i < LA; ++i) oa[i] = (uint32_t)(min(ld_r + ROWS * i, M - 1 - m0) * K);
+#pragma unroll
+  for (int i = 0; i < LW; ++i) ow[i] = (uint32_t)(min(ld_r + ROWS * i, N - 1 - n0) * K);
+  u32x4 ra[LA], rw[LW];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < LA; ++i) ra[i] = *reinterpret_cast<const u32x4 *>(Ab + oa[i] + k0);
+#pragma unroll
+    for (int i = 0; i < LW; ++i) rw[i] = *reinterpret_cast<const u32x4 *>(Wb + ow[i] + k0);
+  };
+  auto lstore = [&](bf16 *sA) {
+    bf16 *sW = sA + BM * BK;
+#pragma unroll
+    for (int i = 0; i < LA; ++i) *reinterpret_cast<u32x4 *>(&sA[lds_off(ld_r + ROWS * i, ld_c)]) = ra[i];
+#pragma unroll
+    for (int i = 0; i < LW; ++i) *reinterpret_cast<u32x4 *>(&sW[lds_off(ld_r + ROWS * i, ld_c)]) = rw[i];
+  };
+  f32x4 acc[WTN][WTM];
+#pragma unroll
+  for (int i = 0; i < WTN; ++i)
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+  const int fr = lane & 15, fq = lane >> 4;
+  const int rowW = 16 * WTN * wn + fr, rowA = 16 * WTM * wm + fr;
+  bf16x8 fw0[WTN], fw1[WTN], fa[WTM];
+  auto rd_w = [&](const bf16 *st, int ks, bf16x8 *fw) {
+    const bf16 *sW = st + BM * BK;
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(rowW + 16 * i, fq + 4 * ks)]);
+  };
+  auto rd_a = [&](const bf16 *st, int ks, int j) {
+    fa[j] = *reinterpret_cast<const bf16x8 *>(&st[lds_off(rowA + 16 * j, fq + 4 * ks)]);
+  };
+  auto mm = [&](const bf16x8 *fw, int j) {
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
+  };
+  const int KT = K / BK;
+  gload(0);
+  lstore(smem);
+  __syncthreads();
+  rd_w(smem, 0, fw0);
+#pragma unroll
+  for (int j = 0; j < WTM; ++j) rd_a(smem, 0, j);
+  for (int kt = 0; kt < KT; ++kt) {
+    const bool more = kt + 1 < KT;
+    const bf16 *cur = smem + (kt & 1) * STAGE;
+    bf16 *nxt = smem + ((kt + 1) & 1) * STAGE;
+    if (more) gload((kt + 1) * BK);
+    rd_w(cur, 1, fw1);
+    __builtin_amdgcn_sched_barrier(0);
+    // substep 0; substep-1 A fragments replace substep-0 ones in place
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+      mm(fw0, j);
+      rd_a(cur, 1, j);
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // substep 1, first half
+#pragma unroll
+    for (int j = 0; j < WTM / 2; ++j) mm(fw1, j);
+    __builtin_amdgcn_sched_barrier(0);
+    if (more) lstore(nxt);
+    __syncthreads();
+    if (more) {
+      rd_w(nxt, 0, fw0);
+#pragma unroll
+      for (int j = 0; j < WTM / 2; ++j) rd_a(nxt, 0, j);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // substep 1, second half; next tile's A fragments replace these in place
+#pragma unroll
+    for (int j = WTM / 2; j < WTM; ++j) {
+      mm(fw1, j);
+      if (more) rd_a(nxt, 0, j);
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
 #pragma unroll
   for (int i = 0; i < WTN; ++i) {
     const int n = n0 + 16 * WTN * wn + 16 * i + 4 * fq;
@@ -216,7 +350,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
     }
   }
 }
-
 // ---------------------------------------------------------------------------------- VALU path
 template <typename TI, int EPI, typename TO>
 __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const TI *__restrict__ A,
@@ -279,12 +412,13 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
                               hipStream_t s) {
   constexpr int BM = 16 * WTM * WGM, BN = 16 * WTN * WGN;
   const size_t lds = (size_t)2 * (BM + BN) * mf::BK * sizeof(bf16);
-  auto kern = k_linear_mfma<WTM, WTN, WGM, WGN, DEPTH, EPI, bf16>;
-  static bool attr_set = false;
-  if (!attr_set) {
+  auto kern = K % mf::BK ? k_linear_mfma<WTM, WTN, WGM, WGN, DEPTH, true, EPI, bf16>
+                          : k_linear_mfma<WTM, WTN, WGM, WGN, DEPTH, false, EPI, bf16>;
+  static bool attr_set[2] = {false, false};
+  if (!attr_set[K % mf::BK ? 1 : 0]) {
     hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (err != hipSuccess) return err;
-    attr_set = true;
+    attr_set[K % mf::BK ? 1 : 0] = true;
   }
   const int MT = (M + BM - 1) / BM, NT = (N + BN - 1) / BN;
   hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(64 * WGM * WGN), lds, s, M, N, K, (const bf16 *)A,
@@ -293,10 +427,30 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
 }
 
 template <int EPI>
+static hipError_t launch_ilv(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
+                             hipStream_t s) {
+  const size_t lds = (size_t)2 * (256 + 256) * mf::BK * sizeof(bf16);
+  auto kern = k_linear_ilv<EPI, bf16>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int MT = (M + 255) / 256, NT = (N + 255) / 256;
+  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(512), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
+                     MT, NT);
+  return hipGetLastError();
+}
+
+template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
-    if (pick_big_tile(M, N, K)) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+    if (pick_big_tile(M, N, K)) {
+      if (K % mf::BK == 0) return launch_ilv<EPI>(M, N, K, A, Wt, e, s);
+      return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+    }
     return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
   }
   dim3 grid((M + 63) / 64, (N + 63) / 64);

@@ -84,10 +84,11 @@ def test_linear_small(dtype, M, N, K, epi):
 
 
 @pytest.mark.parametrize("tile", ["256x256", "128x128"])
-@pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8)])
+@pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
 def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
-    """Both MFMA tilings (forced) on ragged M, N and K tails, against the oracle."""
+    """Every MFMA kernel (forced tiling; the 256x256 one is the interleaved kernel when K % 64 == 0)
+    on ragged M, N and K tails, against the oracle."""
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
     F = fb()
     A = _operand((M, K), 71, "bf16")
