@@ -9,9 +9,11 @@
 //     single cross-lane exchange and the running sum stays per lane until the end.  The output is
 //     accumulated transposed as well, O^T += V^T P^T: the probabilities feed the second MFMA straight
 //     from the first one's accumulator registers (the key order inside each 16-key chunk is permuted
-//     identically on both operands), and every lane rescales only its own query.  K tiles are staged
-//     in LDS row-major with an XOR swizzle, V tiles transposed (padded rows) so V^T fragments are two
-//     8-byte reads.
+//     identically on both operands), and every lane rescales only its own query.  K and V tiles are
+//     staged in LDS row-major with 16-byte stores and XOR swizzles; V^T fragments come from gfx950's
+//     LDS transpose read (ds_read_b64_tr_b16): in each group of 16 lanes, lane j addresses 4
+//     consecutive head dims of one key and lane 4a + b receives element b of the pieces addressed by
+//     lanes a, a + 4, a + 8, a + 12 -- i.e. one head dim across four keys.
 #include "common.h"
 #include "kernels.h"
 
@@ -98,14 +100,16 @@ constexpr int KT = 64;          // keys per LDS tile
 constexpr int QW = 32;          // queries per wave
 constexpr int WAVES = 4;
 constexpr int QB = QW * WAVES;  // queries per workgroup
-constexpr int VT_LD = KT + 4;   // padded row of the transposed V tile (136 B: conflict-free reads)
 __device__ __forceinline__ int k_off(int r, int c) { return r * DH + ((c ^ (r & 15)) << 3); }
+// V rows: 16-byte chunk c of key r at c ^ (2 r mod 16); keeps the four keys of a transpose-read group
+// on distinct banks
+__device__ __forceinline__ int v_off(int r, int c) { return r * DH + ((c ^ ((r << 1) & 14)) << 3); }
 }  // namespace fa
 
 __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
   using namespace fa;
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * DH];
-  __shared__ __attribute__((aligned(16))) bf16 sVt[DH * VT_LD];
+  __shared__ __attribute__((aligned(16))) bf16 sV[KT * DH];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, li = lane & 31;
   const int b = blockIdx.z, h = blockIdx.y;
   const int q0 = blockIdx.x * QB + w * QW;
@@ -144,9 +148,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
     for (int i = 0; i < 4; ++i) {
       int r = lr + 16 * i;
       *reinterpret_cast<u32x4 *>(&sK[k_off(r, lc)]) = rk[i];
-      bf16x8 v8 = __builtin_bit_cast(bf16x8, rv[i]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sVt[(8 * lc + e) * VT_LD + r] = v8[e];
+      *reinterpret_cast<u32x4 *>(&sV[v_off(r, lc)]) = rv[i];
     }
   };
 
@@ -198,7 +200,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
         lsum += e;
         sc[st][j] = e;
       }
-    // O^T += V^T P^T over four 16-key chunks; k-slot i of group g <-> key 16c + (i/4)*8 + 4g + i%4
+    // O^T += V^T P^T over four 16-key chunks; k-slot i of group g <-> key 16c + (i/4)*8 + 4g + i%4.
+    // Transpose-read addressing: lane (16-lane group h = bit 4, q = low 4 bits) addresses key
+    // 16c + 4g + (q >> 2) (+8 for k-slots 4..7) at head dims 32 dt + 16 h + 4 (q & 3) .. + 3, so lane l
+    // receives head dim 32 dt + (l & 31) for those four keys.
+    const int tq = lane & 15, th = (lane >> 4) & 1;
+    const int tkey = 4 * g + (tq >> 2), tdim = 16 * th + 4 * (tq & 3);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       bf16x8 pf;
@@ -206,10 +213,14 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
       for (int i = 0; i < 8; ++i) pf[i] = (bf16)sc[c >> 1][8 * (c & 1) + i];
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        const bf16 *vr = &sVt[(32 * dt + li) * VT_LD + 16 * c + 4 * g];
-        bf16x4 v0 = *reinterpret_cast<const bf16x4 *>(vr);
-        bf16x4 v1 = *reinterpret_cast<const bf16x4 *>(vr + 8);
-        bf16x8 vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        const int d = 32 * dt + tdim, k0 = 16 * c + tkey;
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4 *)&sV[v_off(k0, d >> 3) + (d & 7)]);
+        s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4 *)&sV[v_off(k0 + 8, d >> 3) + (d & 7)]);
+        bf16x4 w0 = __builtin_bit_cast(bf16x4, v0), w1 = __builtin_bit_cast(bf16x4, v1);
+        bf16x8 vf = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
       }
     }
