@@ -108,8 +108,7 @@ __device__ __forceinline__ int v_off(int r, int c) { return r * DH + ((c ^ ((r <
 
 __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
   using namespace fa;
-  __shared__ __attribute__((aligned(16))) bf16 sK[KT * DH];
-  __shared__ __attribute__((aligned(16))) bf16 sV[KT * DH];
+  __shared__ __attribute__((aligned(16))) bf16 sKV[2][2][KT * DH];  // [stage][K, V]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, li = lane & 31;
   const int b = blockIdx.z, h = blockIdx.y;
   const int q0 = blockIdx.x * QB + w * QW;
@@ -143,21 +142,25 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
       rv[i] = *reinterpret_cast<const u32x4 *>(V + (int64_t)key * p.kv_rs + 8 * lc);
     }
   };
-  auto lstore = [&]() {
+  auto lstore = [&](int stage) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       int r = lr + 16 * i;
-      *reinterpret_cast<u32x4 *>(&sK[k_off(r, lc)]) = rk[i];
-      *reinterpret_cast<u32x4 *>(&sV[v_off(r, lc)]) = rv[i];
+      *reinterpret_cast<u32x4 *>(&sKV[stage][0][k_off(r, lc)]) = rk[i];
+      *reinterpret_cast<u32x4 *>(&sKV[stage][1][v_off(r, lc)]) = rv[i];
     }
   };
 
+  // two LDS stages: tile t+1 is loaded into registers while tile t is consumed, then stored to the
+  // other stage; one barrier per tile
   gload(0);
-  for (int j0 = 0; j0 < p.tk; j0 += KT) {
-    __syncthreads();
-    lstore();
-    __syncthreads();
-    if (j0 + KT < p.tk) gload(j0 + KT);
+  lstore(0);
+  __syncthreads();
+  for (int j0 = 0, it = 0; j0 < p.tk; j0 += KT, ++it) {
+    const int st = it & 1;
+    const bf16 *sK = sKV[st][0], *sV = sKV[st][1];
+    const bool more = j0 + KT < p.tk;
+    if (more) gload(j0 + KT);
 
     // S^T for two 32-key slabs: lane holds query li, keys 32 st + (j/4)*8 + 4 g + (j%4)
     f32x16 sc[2];
@@ -172,31 +175,40 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
         sc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[st], 0, 0, 0);
       }
     }
-    // online softmax (base 2, scale folded in)
+    // online softmax in base 2: running max of the raw scores (the scale is positive), exponent
+    // argument formed by one FMA; keys past tk are masked only on the ragged last tile; the
+    // accumulators are rescaled only when some lane's maximum moved
+    if (j0 + KT > p.tk) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          int key = j0 + 32 * st + (j >> 2) * 8 + 4 * g + (j & 3);
+          if (key >= p.tk) sc[st][j] = -INFINITY;
+        }
+    }
     float tmax = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        int key = j0 + 32 * st + (j >> 2) * 8 + 4 * g + (j & 3);
-        float v = key < p.tk ? sc[st][j] * p.qscale : -INFINITY;
-        sc[st][j] = v;
-        tmax = fmaxf(tmax, v);
-      }
+      for (int j = 0; j < 16; ++j) tmax = fmaxf(tmax, sc[st][j]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float mnew = fmaxf(mrun, tmax);
-    const float corr = exp2f(mrun - mnew);
-    mrun = mnew;
-    lsum *= corr;
+    if (__any(mnew > mrun)) {
+      const float corr = __builtin_amdgcn_exp2f((mrun - mnew) * p.qscale);
+      lsum *= corr;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+      for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) o[dt][j] *= corr;
+        for (int j = 0; j < 16; ++j) o[dt][j] *= corr;
+      mrun = mnew;
+    }
+    const float mb = mrun * p.qscale;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        float e = exp2f(sc[st][j] - mnew);
+        float e = __builtin_amdgcn_exp2f(fmaf(sc[st][j], p.qscale, -mb));
         lsum += e;
         sc[st][j] = e;
       }
@@ -224,6 +236,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
       }
     }
+    if (more) lstore(st ^ 1);
+    __syncthreads();
   }
   const float ltot = lsum + __shfl_xor(lsum, 32, 64);
   const float inv = 1.0f / ltot;
