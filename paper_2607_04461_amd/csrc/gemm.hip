@@ -66,6 +66,64 @@ __device__ __forceinline__ void epilogue4(const EpiArgs &e, int m, int n, float 
   }
 }
 
+// Eight consecutive output columns n .. n+7 of row m: one 16-byte bf16 store or two 16-byte fp32
+// stores per lane.
+template <int EPI, typename TO>
+__device__ __forceinline__ void epilogue8(const EpiArgs &e, int m, int n, const float *v_in) {
+  if constexpr (EPI == EPI_EULER) {
+    epilogue4<EPI, TO>(e, m, n, v_in[0], v_in[1], v_in[2], v_in[3]);
+    epilogue4<EPI, TO>(e, m, n + 4, v_in[4], v_in[5], v_in[6], v_in[7]);
+  } else {
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = v_in[q];
+    if (e.bias) {
+      float4 b0 = *reinterpret_cast<const float4 *>(e.bias + n);
+      float4 b1 = *reinterpret_cast<const float4 *>(e.bias + n + 4);
+      v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+      v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+    }
+    if constexpr (EPI == EPI_STORE || EPI == EPI_GELU) {
+      if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = gelu_tanh(v[q]);
+      }
+      TO *o = reinterpret_cast<TO *>(e.out) + (int64_t)m * e.ldo + n;
+      if constexpr (sizeof(TO) == 4) {
+        reinterpret_cast<float4 *>(o)[0] = make_float4(v[0], v[1], v[2], v[3]);
+        reinterpret_cast<float4 *>(o)[1] = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        bf16x8 w = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
+                    (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+        *reinterpret_cast<bf16x8 *>(o) = w;
+      }
+    } else if constexpr (EPI == EPI_STORE_F32) {
+      float *o = reinterpret_cast<float *>(e.out) + (int64_t)m * e.ldo + n;
+      reinterpret_cast<float4 *>(o)[0] = make_float4(v[0], v[1], v[2], v[3]);
+      reinterpret_cast<float4 *>(o)[1] = make_float4(v[4], v[5], v[6], v[7]);
+    } else if constexpr (EPI == EPI_RESIDUAL) {
+      float *o = reinterpret_cast<float *>(e.out) + (int64_t)m * e.ldo + n;
+      float4 h0 = reinterpret_cast<float4 *>(o)[0], h1 = reinterpret_cast<float4 *>(o)[1];
+      if (e.gate) {
+        float4 g0 = *reinterpret_cast<const float4 *>(e.gate + n);
+        float4 g1 = *reinterpret_cast<const float4 *>(e.gate + n + 4);
+        h0.x += g0.x * v[0]; h0.y += g0.y * v[1]; h0.z += g0.z * v[2]; h0.w += g0.w * v[3];
+        h1.x += g1.x * v[4]; h1.y += g1.y * v[5]; h1.z += g1.z * v[6]; h1.w += g1.w * v[7];
+      } else {
+        h0.x += v[0]; h0.y += v[1]; h0.z += v[2]; h0.w += v[3];
+        h1.x += v[4]; h1.y += v[5]; h1.z += v[6]; h1.w += v[7];
+      }
+      reinterpret_cast<float4 *>(o)[0] = h0;
+      reinterpret_cast<float4 *>(o)[1] = h1;
+      if (e.cache) {
+        float *c = e.cache + (int64_t)m * e.ldo + n;
+        reinterpret_cast<float4 *>(c)[0] = h0;
+        reinterpret_cast<float4 *>(c)[1] = h1;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------- MFMA path
 namespace mf {
 constexpr int BK = 64;
@@ -280,12 +338,15 @@ __global__ __launch_bounds__(512, 1) void k_linear_ilv(int M, int N, int K, cons
 #pragma unroll
     for (int j = 0; j < WTM; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
   const int fr = lane & 15, fq = lane >> 4;
-  const int rowW = 16 * WTN * wn + fr, rowA = 16 * WTM * wm + fr;
+  // MFMA tile i of this wave takes W rows 32 (i/2) + 8 (fr/4) + 4 (i%2) + fr%4 (fr = lane & 15), so
+  // the C^T rows a lane ends up with for tiles 2a and 2a+1 are 8 consecutive output columns
+  const int rowA = 16 * WTM * wm + fr;
+  auto w_row = [&](int i) { return 16 * WTN * wn + 32 * (i >> 1) + 8 * (fr >> 2) + 4 * (i & 1) + (fr & 3); };
   bf16x8 fw0[WTN], fw1[WTN], fa[WTM];
   auto rd_w = [&](const bf16 *st, int ks, bf16x8 *fw) {
     const bf16 *sW = st + BM * BK;
 #pragma unroll
-    for (int i = 0; i < WTN; ++i) fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(rowW + 16 * i, fq + 4 * ks)]);
+    for (int i = 0; i < WTN; ++i) fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(w_row(i), fq + 4 * ks)]);
   };
   auto rd_a = [&](const bf16 *st, int ks, int j) {
     fa[j] = *reinterpret_cast<const bf16x8 *>(&st[lds_off(rowA + 16 * j, fq + 4 * ks)]);
@@ -340,13 +401,18 @@ __global__ __launch_bounds__(512, 1) void k_linear_ilv(int M, int N, int K, cons
     __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
-  for (int i = 0; i < WTN; ++i) {
-    const int n = n0 + 16 * WTN * wn + 16 * i + 4 * fq;
-    if (n >= N) continue;
+  for (int pa = 0; pa < WTN / 2; ++pa) {
+    const int n = n0 + 16 * WTN * wn + 32 * pa + 8 * fq;
 #pragma unroll
     for (int j = 0; j < WTM; ++j) {
       const int m = m0 + 16 * WTM * wm + 16 * j + fr;
-      if (m < M) epilogue4<EPI, TO>(e, m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      const float v[8] = {acc[2 * pa][j][0], acc[2 * pa][j][1], acc[2 * pa][j][2], acc[2 * pa][j][3],
+                          acc[2 * pa + 1][j][0], acc[2 * pa + 1][j][1], acc[2 * pa + 1][j][2],
+                          acc[2 * pa + 1][j][3]};
+      if (m < M && n < N) {
+        if (n + 8 <= N) epilogue8<EPI, TO>(e, m, n, v);
+        else epilogue4<EPI, TO>(e, m, n, v[0], v[1], v[2], v[3]);   // N % 8 == 4 edge
+      }
     }
   }
 }
