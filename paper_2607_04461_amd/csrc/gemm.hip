@@ -209,7 +209,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
 
   f32x4 acc[WTN][WTM];
   const int fr = lane & 15, fq = lane >> 4;
-  const int rowW = 16 * WTN * wn + fr, rowA = 16 * WTM * wm + fr;
+  const int rowA = 16 * WTM * wm + fr;
+  // MFMA tile i takes W rows 32 (i/2) + 8 (fr/4) + 4 (i%2) + fr%4, so a lane's outputs of tiles 2a
+  // and 2a+1 are 8 consecutive columns (WTN is even)
+  auto w_row = [&](int i) { return 16 * WTN * wn + 32 * (i >> 1) + 8 * (fr >> 2) + 4 * (i & 1) + (fr & 3); };
   // All fragments of a 32-wide K substep are requested before its MFMA chain starts, so the LDS
   // latency is paid once per substep rather than once per few MFMAs.
   auto compute = [&](const bf16 *sA) {
@@ -219,7 +222,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
       bf16x8 fw[WTN], fa[WTM];
 #pragma unroll
       for (int i = 0; i < WTN; ++i)
-        fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(rowW + 16 * i, fq + 4 * ks)]);
+        fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(w_row(i), fq + 4 * ks)]);
 #pragma unroll
       for (int j = 0; j < WTM; ++j)
         fa[j] = *reinterpret_cast<const bf16x8 *>(&sA[lds_off(rowA + 16 * j, fq + 4 * ks)]);
@@ -235,13 +238,18 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N,
   // acc[i][j] (C^T tile 16x16): lane column = m index (lane & 15), rows = 4 consecutive n.
   auto epilogue = [&](int em0, int en0) {
 #pragma unroll
-    for (int i = 0; i < WTN; ++i) {
-      const int n = en0 + 16 * WTN * wn + 16 * i + 4 * fq;
-      if (n >= N) continue;
+    for (int pa = 0; pa < WTN / 2; ++pa) {
+      const int n = en0 + 16 * WTN * wn + 32 * pa + 8 * fq;
 #pragma unroll
       for (int j = 0; j < WTM; ++j) {
         const int m = em0 + 16 * WTM * wm + 16 * j + fr;
-        if (m < M) epilogue4<EPI, TO>(e, m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        const float v[8] = {acc[2 * pa][j][0], acc[2 * pa][j][1], acc[2 * pa][j][2], acc[2 * pa][j][3],
+                            acc[2 * pa + 1][j][0], acc[2 * pa + 1][j][1], acc[2 * pa + 1][j][2],
+                            acc[2 * pa + 1][j][3]};
+        if (m < M && n < N) {
+          if (n + 8 <= N) epilogue8<EPI, TO>(e, m, n, v);
+          else epilogue4<EPI, TO>(e, m, n, v[0], v[1], v[2], v[3]);   // N % 8 == 4 edge
+        }
       }
     }
   };
