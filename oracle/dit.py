@@ -12,7 +12,7 @@ What it follows:
   * layer skipping: a skipped block is the identity on the residual stream (Sec. 4.1 (3), Eq. 6);
     a computed block is h = B_l(h, x, t) (Eq. 7);
   * the flow-matching update: the Euler-Maruyama rule of App. A.1 (Eq. 20) with a = 0, i.e.
-    z <- z + (t_next - t_cur) * v;
+    z <- z + (t_next - t_cur) * v; optionally the stochastic rule with a > 0 (oracle/sde.py);
   * refinement resumes from the draft's latent with every knob off (Sec. 4.2, Stage 3, Eq. 13).
 
 The paper does not describe the DiT block.  The block used here (and by the library) is a Wan-shaped
@@ -34,6 +34,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 from .dispatch import COMPUTE, PROXY, SKIP, plan_step, recent_slots
+from . import sde
 
 f64 = np.float64
 
@@ -197,8 +198,13 @@ class PoolCache:
 def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
                    kv: List[Tuple[np.ndarray, np.ndarray]], block_mod: np.ndarray,
                    head_mod: np.ndarray, trace, meta_before: List[Dict], cache: Optional[PoolCache],
-                   cand: int, hidden: Optional[List[np.ndarray]] = None) -> np.ndarray:
-    """One denoising step of one candidate under an already-planned trace; returns z_next [C, H, W]."""
+                   cand: int, hidden: Optional[List[np.ndarray]] = None,
+                   noise: Optional[Tuple[float, int, int]] = None) -> np.ndarray:
+    """One denoising step of one candidate under an already-planned trace; returns z_next [C, H, W].
+
+    ``noise = (a, seed, step)`` replaces the Euler update by the stochastic one of App. A.1 (Eq. 20)
+    with the normals of candidate ``cand`` at counter ``step`` (oracle/sde.py).
+    """
     C, H, Wd = z.shape
     p = shape.patch
     tok = patchify(np.asarray(z, f64), p)
@@ -223,6 +229,10 @@ def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float,
     a = layer_norm(h, shape.ln_eps) * (1.0 + sc) + sh
     out = linear(a, W["head_w"], W["head_b"])
     v = unpatchify(out, C, H, Wd, p)
+    if noise is not None:
+        a, seed, step = noise
+        eps = sde.latent_normals(z.shape, cand, step, seed)
+        return sde.sde_update(z, v, t_cur, t_next, a, eps)
     return np.asarray(z, f64) + (f64(t_next) - f64(t_cur)) * v
 
 
@@ -230,11 +240,14 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
                kv_per_cond: List[List[Tuple[np.ndarray, np.ndarray]]], cond_index: np.ndarray,
                skip: np.ndarray, proxy: np.ndarray, cache: PoolCache,
                candidates: Optional[Sequence[int]] = None,
-               hidden: Optional[Dict[int, List[np.ndarray]]] = None):
+               hidden: Optional[Dict[int, List[np.ndarray]]] = None,
+               sde_args: Optional[Tuple[float, int, int]] = None):
     """One draft step over the pool (Eq. 2 with the knobs of Sec. 4.1).
 
     z [N, C, H, W]; returns (z_next [N, C, H, W] fp64 -- rows not in ``candidates`` are left as z --,
     trace).  The cache metadata advances once per step, as all candidates share the masks.
+    ``sde_args = (a, seed, step)`` selects the stochastic update (Eq. 20), candidate n drawing the
+    normals of counter (n, step).
     """
     trace, new_meta = plan_step(skip, proxy, cache.meta, t_cur)
     block_mod, head_mod = modulations(W, shape.num_blocks, shape.freq_dim, t_cur)
@@ -242,14 +255,17 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
     for n in (range(z.shape[0]) if candidates is None else candidates):
         hid = None if hidden is None else hidden.setdefault(n, [])
         out[n] = candidate_step(W, shape, z[n], t_cur, t_next, kv_per_cond[int(cond_index[n])],
-                                block_mod, head_mod, trace, cache.meta, cache, n, hid)
+                                block_mod, head_mod, trace, cache.meta, cache, n, hid, sde_args)
     cache.meta = new_meta
     return out, trace
 
 
 def refine_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
-                kv_per_cond, cond_index: np.ndarray, candidates: Optional[Sequence[int]] = None):
-    """Full-quality step (phi_full of Eq. 13): no skipping, no proxies, no cache."""
+                kv_per_cond, cond_index: np.ndarray, candidates: Optional[Sequence[int]] = None,
+                sde_args: Optional[Tuple[float, int, int]] = None):
+    """Full-quality step (phi_full of Eq. 13): no skipping, no proxies, no cache.
+
+    ``sde_args`` as in ``draft_step``."""
     L = shape.num_blocks
     zeros = np.zeros(L, np.uint8)
     trace, _ = plan_step(zeros, zeros, [{"count": 0, "head": 0, "t": [0.0] * 3} for _ in range(L)],
@@ -258,7 +274,7 @@ def refine_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_
     out = np.asarray(z, f64).copy()
     for n in (range(z.shape[0]) if candidates is None else candidates):
         out[n] = candidate_step(W, shape, z[n], t_cur, t_next, kv_per_cond[int(cond_index[n])],
-                                block_mod, head_mod, trace, None, None, n)
+                                block_mod, head_mod, trace, None, None, n, None, sde_args)
     return out
 
 
