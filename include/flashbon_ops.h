@@ -58,6 +58,21 @@ flashbon_status flashbon_op_proxy(int64_t count, const float *h1, const float *h
                                   int32_t order, float tau1, float tau2, float t_cur, float *out,
                                   void *stream);
 
+/* Counter-based normals of the stochastic update (App. A.1, Eq. 20), as flashbon_step_args defines
+ * them, for `count` flat elements of one candidate row at one step: words (device uint32
+ * [ceil(count / 4)][4], the Philox4x32-10 outputs of counters (q, candidate, step, 0)) and normals
+ * (device fp32 [count]); either may be NULL. */
+flashbon_status flashbon_op_normals(int64_t count, int32_t candidate, int32_t step, uint64_t seed,
+                                    uint32_t *words, float *normals, void *stream);
+
+/* Unpatchify + stochastic update (Eq. 20) as the step performs it: v is the head output, device fp32
+ * [n (H/p)(W/p)][C p p] (token i (W/p) + j of candidate b, column c p^2 + p di + dj <-> z[b][c][p i +
+ * di][p j + dj]); z device fp32 [n][C][H][W] updated in place; the rest as in flashbon_step_args.
+ * H, W positive multiples of p. */
+flashbon_status flashbon_op_unpatch_sde(int32_t n, int32_t C, int32_t H, int32_t W, int32_t p,
+                                        const float *v, float *z, float t_cur, float t_next, float a,
+                                        uint64_t seed, int32_t step, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -66,4 +66,20 @@ hipError_t launch_block_mods(int L, int width, const float *m, const float *tabl
 
 hipError_t launch_f32_to_bf16(int64_t count, const float *x, void *y, hipStream_t s);
 
+// Stochastic update (App. A.1, Eq. 20): z <- z + dt [v + k (z + omt v)] + g eps, eps from Philox4x32-10
+// with key (key0, key1) and counter (element / 4, candidate, step, 0) through Box-Muller.
+struct SdeArgs {
+  float dt, k, omt, g;
+  uint32_t key0, key1, step;
+};
+// Host: coefficients for noise level a at (t_cur, t_next); false if a < 0, t_cur outside (0, 1] or
+// sigma_t is not finite.
+bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, SdeArgs *out);
+// z [n][C][H][W] fp32 updated in place from v = head output [n T][C p p] fp32 (unpatchified here)
+hipError_t launch_unpatch_sde(int n, int C, int H, int W, int p, const float *v, float *z,
+                              const SdeArgs &a, hipStream_t s);
+// the words (uint32 [ceil(count/4)][4], or null) and normals (fp32 [count], or null) of one candidate
+hipError_t launch_normals(int64_t count, uint32_t cand, uint32_t step, uint64_t seed, uint32_t *words,
+                          float *normals, hipStream_t s);
+
 }  // namespace fb

@@ -148,7 +148,8 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
          o_o = carve(M * D * a), o_u = carve(M * F * a), o_tok = carve(M * P * a),
          o_txt = carve(m->act == ACT_BF16 ? txt_rows * m->Dt * a : 0), o_ctx = carve(txt_rows * D * a),
          o_tf = carve(m->fd * 4), o_e1 = carve(D * 4), o_e = carve(D * 4), o_m6 = carve(6 * D * 4),
-         o_bm = carve((size_t)m->L * 6 * D * 4), o_hm = carve(2 * D * 4), o_cond = carve(cfg->max_n * 4);
+         o_bm = carve((size_t)m->L * 6 * D * 4), o_hm = carve(2 * D * 4), o_cond = carve(cfg->max_n * 4),
+         o_v = carve(M * P * 4);
   if (hipMalloc(&m->ws, off) != hipSuccess) return cleanup(FLASHBON_ENOMEM, "workspace of " + std::to_string(off) + " bytes");
   m->ws_bytes = off;
   char *w = (char *)m->ws;
@@ -156,7 +157,7 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
   m->tok = w + o_tok; m->txt = w + o_txt; m->ctx = w + o_ctx;
   m->tf = (float *)(w + o_tf); m->e1 = (float *)(w + o_e1); m->e = (float *)(w + o_e);
   m->m6 = (float *)(w + o_m6); m->bmods = (float *)(w + o_bm); m->hmod = (float *)(w + o_hm);
-  m->d_cond = (int32_t *)(w + o_cond);
+  m->d_cond = (int32_t *)(w + o_cond); m->vtok = (float *)(w + o_v);
 
   if (hipMemcpy(m->w32, host_weights, total * 4, hipMemcpyHostToDevice) != hipSuccess)
     return cleanup(FLASHBON_EHIP, "weight upload");
@@ -291,6 +292,11 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     taylor_coefficients(mb, a->t_cur, trace[l].order, &ca[l], &cb[l]);
   }
+  SdeArgs sde;
+  const bool stochastic = a->sde_a != 0.f;
+  if (stochastic && a->sde_step < 0) return fail(FLASHBON_EINVAL, "sde_step must be >= 0");
+  if (stochastic && !sde_coefficients(a->t_cur, a->t_next, a->sde_a, a->sde_seed, a->sde_step, &sde))
+    return fail(FLASHBON_EINVAL, "stochastic update needs sde_a >= 0, finite, and 0 < t_cur <= 1 (t_next < 1 when t_cur = 1)");
 
   // ---------------------------------------------------------------- enqueue
   hipStream_t s = (hipStream_t)a->stream;
@@ -426,9 +432,14 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     if ((st = dump(l + 1)) != FLASHBON_OK) return st;
   }
 
-  // head + unpatchify + Euler update of the latents
+  // head + unpatchify + Euler update of the latents (or the stochastic update of Eq. 20)
   HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, m->hmod, m->hmod + D, m->a, s); }), "head adaLN");
-  {
+  if (stochastic) {
+    EpiArgs e;
+    e.out = m->vtok; e.ldo = P; e.bias = Bp(m->lay.head_b);
+    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head");
+    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_unpatch_sde(a->n, m->C, a->latent_h, a->latent_w, p, m->vtok, a->latents, sde, s); }), "unpatchify + stochastic update");
+  } else {
     EpiArgs e;
     e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;
     e.C = m->C; e.H = a->latent_h; e.W = a->latent_w; e.p = p; e.T = T;

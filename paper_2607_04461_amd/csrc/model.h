@@ -35,6 +35,7 @@ struct Model {
   size_t ws_bytes = 0;
   float *h;              // residual stream [maxM][D] fp32
   void *a, *qkv, *o, *u, *tok, *txt, *ctx;  // act buffers
+  float *vtok;           // head output [maxM][C p p] fp32 (stochastic update only)
   float *tf, *e1, *e, *m6, *bmods, *hmod;   // timestep path (fp32)
   int32_t *d_cond;
   std::vector<int32_t> last_cond;

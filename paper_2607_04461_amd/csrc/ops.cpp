@@ -1,6 +1,7 @@
 // Kernel-level entry points (flashbon_ops.h): validation, then one launch each.
 #include <hip/hip_runtime.h>
 
+#include <climits>
 #include <cmath>
 #include <string>
 
@@ -80,6 +81,29 @@ flashbon_status flashbon_op_proxy(int64_t count, const float *h1, const float *h
   float ca, cb;
   taylor_coefficients(mb, t_cur, order, &ca, &cb);
   return launched(launch_proxy(count, h1, h2, h3, order, ca, cb, out, (hipStream_t)stream), "proxy");
+}
+
+flashbon_status flashbon_op_normals(int64_t count, int32_t candidate, int32_t step, uint64_t seed,
+                                    uint32_t *words, float *normals, void *stream) {
+  if (count < 1 || count > ((int64_t)1 << 34)) return fail(FLASHBON_ESHAPE, "count outside [1, 2^34]");
+  if (candidate < 0 || step < 0) return fail(FLASHBON_EINVAL, "candidate and step must be >= 0");
+  if (!words && !normals) return fail(FLASHBON_EINVAL, "words or normals is required");
+  return launched(launch_normals(count, (uint32_t)candidate, (uint32_t)step, seed, words, normals,
+                                 (hipStream_t)stream), "normals");
+}
+
+flashbon_status flashbon_op_unpatch_sde(int32_t n, int32_t C, int32_t H, int32_t W, int32_t p,
+                                        const float *v, float *z, float t_cur, float t_next, float a,
+                                        uint64_t seed, int32_t step, void *stream) {
+  if (n < 1 || n > 65535 || C < 1 || p < 1 || H < p || W < p || H % p || W % p)
+    return fail(FLASHBON_ESHAPE, "need 1 <= n <= 65535, C >= 1, H and W positive multiples of p");
+  if ((int64_t)C * H * W > INT32_MAX) return fail(FLASHBON_ESHAPE, "C H W must fit in int32");
+  if (!v || !z) return fail(FLASHBON_EINVAL, "v and z are required");
+  if (step < 0) return fail(FLASHBON_EINVAL, "step must be >= 0");
+  SdeArgs s;
+  if (!sde_coefficients(t_cur, t_next, a, seed, step, &s))
+    return fail(FLASHBON_EINVAL, "need a >= 0, finite, and 0 < t_cur <= 1 (t_next < 1 when t_cur = 1)");
+  return launched(launch_unpatch_sde(n, C, H, W, p, v, z, s, (hipStream_t)stream), "unpatch_sde");
 }
 
 }  // extern "C"

@@ -58,6 +58,7 @@ class StepArgs(ctypes.Structure):
         ("cache", ctypes.c_void_p), ("meta", ctypes.POINTER(CacheMeta)),
         ("trace", ctypes.POINTER(TraceEntry)), ("hidden_dump", ctypes.c_void_p),
         ("stream", ctypes.c_void_p),
+        ("sde_a", ctypes.c_float), ("sde_step", ctypes.c_int32), ("sde_seed", ctypes.c_uint64),
     ]
 
 
@@ -65,7 +66,7 @@ EXPORTS = [
     "flashbon_weight_count", "flashbon_init_model", "flashbon_text_kv_bytes", "flashbon_cache_bytes",
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
     "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_attention", "flashbon_op_ln_mod",
-    "flashbon_op_proxy",
+    "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde",
 ]
 
 
@@ -114,6 +115,11 @@ def load() -> ctypes.CDLL:
     L.flashbon_op_ln_mod.restype = i32
     L.flashbon_op_proxy.argtypes = [i64, vp, vp, vp, i32, f32, f32, f32, vp, vp]
     L.flashbon_op_proxy.restype = i32
+    L.flashbon_op_normals.argtypes = [i64, i32, i32, ctypes.c_uint64, vp, vp, vp]
+    L.flashbon_op_normals.restype = i32
+    L.flashbon_op_unpatch_sde.argtypes = [i32, i32, i32, i32, i32, vp, vp, f32, f32, f32, ctypes.c_uint64,
+                                          i32, vp]
+    L.flashbon_op_unpatch_sde.restype = i32
     _lib = L
     return L
 
@@ -188,7 +194,7 @@ def trace_list(trace) -> list:
 
 def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
           skip=None, proxy=None, cache=None, meta=None, trace=None, hidden_dump=None, stream=None,
-          num_blocks=None):
+          num_blocks=None, sde=None):
     n, C, H, W = (int(x) for x in latents.shape)
     n_cond, text_len = int(text.shape[0]), int(text.shape[1])
     cond = np.ascontiguousarray(np.asarray(cond_index, dtype=np.int32))
@@ -212,21 +218,24 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
     a.trace = trace
     a.hidden_dump = _ptr(hidden_dump)
     a.stream = _stream(stream)
+    if sde is not None:
+        a.sde_a, a.sde_seed, a.sde_step = float(sde[0]), int(sde[1]), int(sde[2])
     _check(fn(model, ctypes.byref(a)), where)
 
 
 def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
-                        skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None):
-    """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays."""
+                        skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None, sde=None):
+    """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays;
+    ``sde = (a, seed, step)`` selects the stochastic update (None or a = 0: Euler)."""
     _step(load().flashbon_draft_step, "flashbon_draft_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, skip, proxy, cache, meta, trace, hidden_dump, stream,
-          num_blocks=len(meta))
+          num_blocks=len(meta), sde=sde)
 
 
 def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
-                         trace=None, hidden_dump=None, stream=None):
+                         trace=None, hidden_dump=None, stream=None, sde=None):
     _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
-          cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream)
+          cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde)
 
 
 def flashbon_plan_step(skip, proxy, meta, t_cur: float, trace=None):
@@ -277,3 +286,13 @@ def flashbon_op_ln_mod(dtype, M, D, eps, x, shift, scale, out, stream=None):
 def flashbon_op_proxy(count, h1, h2, h3, order, tau1, tau2, t_cur, out, stream=None):
     _check(load().flashbon_op_proxy(count, _ptr(h1), _ptr(h2), _ptr(h3), order, tau1, tau2, t_cur, _ptr(out),
                                     _stream(stream)), "flashbon_op_proxy")
+
+
+def flashbon_op_normals(count, candidate, step, seed, words=None, normals=None, stream=None):
+    _check(load().flashbon_op_normals(count, candidate, step, seed, _ptr(words), _ptr(normals),
+                                      _stream(stream)), "flashbon_op_normals")
+
+
+def flashbon_op_unpatch_sde(n, C, H, W, p, v, z, t_cur, t_next, a, seed, step, stream=None):
+    _check(load().flashbon_op_unpatch_sde(n, C, H, W, p, _ptr(v), _ptr(z), t_cur, t_next, a, seed, step,
+                                          _stream(stream)), "flashbon_op_unpatch_sde")

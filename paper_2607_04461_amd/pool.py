@@ -53,21 +53,25 @@ class DraftPool:
         self.latents.copy_(self.torch.from_numpy(np.ascontiguousarray(z0, np.float32)))
         ctypes.memset(self.meta, 0, ctypes.sizeof(self.meta))
 
-    def draft_step(self, k: int, skip=None, proxy=None, hidden_dump=None, stream=None) -> list:
+    def draft_step(self, k: int, skip=None, proxy=None, hidden_dump=None, stream=None, sde=None) -> list:
+        """Step k of the schedule; ``sde = (a, seed)`` takes the stochastic update with counter k."""
         if skip is None or proxy is None:
             s, p = self.wl.masks(k)
             skip = s if skip is None else skip
             proxy = p if proxy is None else proxy
         fb.flashbon_draft_step(self.model, self.latents, self.schedule[k], self.schedule[k + 1], self.text,
                                self.cond_index, self.text_kv, self.text_kv_valid, skip, proxy, self.cache,
-                               self.meta, self.trace, hidden_dump, stream)
+                               self.meta, self.trace, hidden_dump, stream,
+                               None if sde is None else (sde[0], sde[1], k))
         return fb.trace_list(self.trace)
 
-    def refine_step(self, k: int, latents=None, cond_index=None, hidden_dump=None, stream=None) -> list:
+    def refine_step(self, k: int, latents=None, cond_index=None, hidden_dump=None, stream=None,
+                    sde=None) -> list:
         lat = self.latents if latents is None else latents
         cond = self.cond_index if cond_index is None else cond_index
         fb.flashbon_refine_step(self.model, lat, self.schedule[k], self.schedule[k + 1], self.text, cond,
-                                self.text_kv, self.text_kv_valid, self.trace, hidden_dump, stream)
+                                self.text_kv, self.text_kv_valid, self.trace, hidden_dump, stream,
+                                None if sde is None else (sde[0], sde[1], k))
         return fb.trace_list(self.trace)
 
     def draft(self, steps: Optional[int] = None, on_step: Optional[Callable] = None) -> List[list]:

@@ -113,3 +113,29 @@ def test_round_to_bf16_is_rne():
     y = synth.round_to_bf16(x)
     assert list(y[:3]) == [1.0, 1.0, 1.0 + 2 ** -6]   # ties to even, then round up past the tie
     assert y[3] == -2.5
+
+
+@pytest.mark.parametrize("t_cur,t_next,a", [(0.5, 0.4, -0.1), (0.0, -0.1, 0.3), (1.0, 1.0, 0.3),
+                                            (1.5, 1.0, 0.3), (0.5, 0.4, float("nan")),
+                                            (0.5, 0.4, float("inf"))])
+def test_unpatch_sde_rejects_bad_noise_arguments_before_device_work(t_cur, t_next, a):
+    """Host validation of the stochastic update (App. A.1, Eq. 20): no kernel is launched, so the
+    (never dereferenced) placeholder pointers are safe without a device."""
+    lib = fb.load()
+    st = lib.flashbon_op_unpatch_sde(1, 1, 8, 8, 2, 0x1000, 0x2000, t_cur, t_next, a, 1, 0, None)
+    assert st == fb.EINVAL
+    assert b"t_cur" in lib.flashbon_last_error()
+
+
+@pytest.mark.parametrize("args", [(0, 1, 8, 8, 2), (1, 1, 7, 8, 2), (1, 0, 8, 8, 2), (1, 1, 8, 8, 0)])
+def test_unpatch_sde_rejects_bad_shapes(args):
+    lib = fb.load()
+    st = lib.flashbon_op_unpatch_sde(*args, 0x1000, 0x2000, 0.5, 0.4, 0.3, 1, 0, None)
+    assert st == fb.ESHAPE
+
+
+def test_normals_rejects_bad_arguments():
+    lib = fb.load()
+    assert lib.flashbon_op_normals(0, 0, 0, 1, 0x1000, None, None) == fb.ESHAPE
+    assert lib.flashbon_op_normals(8, -1, 0, 1, 0x1000, None, None) == fb.EINVAL
+    assert lib.flashbon_op_normals(8, 0, 0, 1, None, None, None) == fb.EINVAL
