@@ -187,18 +187,20 @@ def main():
                 breakdown[site] = {"ms": round(ms, 3), "launches": n}
         fb.flashbon_set_timing(pool.model, [])
 
-    # refinement of the selected candidate (seeded stand-in verifier score, argmax, lowest index on ties)
-    refine_ms = None
+    # selection (multi-stage Elo over a seeded synthetic verifier) and refinement of the winner
+    refine_ms = selection = None
     if not args.no_refine:
-        scores = synth.make_scores(wl.n, seed=7)
-        sel = int(np.argmax(scores))
+        verifier = synth.SyntheticVerifier(wl.n, seed=7)
         one_draft()
-        lat = pool.latents[sel:sel + 1].clone()
-        cond = wl.cond_index()[sel:sel + 1]
+        torch.cuda.synchronize()
+        s0 = time.time()
+        sel = pool.select(verifier.scores, verifier.judge)
+        sel_ms = (time.time() - s0) * 1e3
+        selection = {"winner": sel, "pairwise_calls": pool.last_selection[2],
+                     "host_ms_incl_verifier": round(sel_ms, 3)}
         torch.cuda.synchronize()
         r0 = time.time()
-        for k in range(wl.steps_draft, wl.steps_total):
-            pool.refine_step(k, latents=lat, cond_index=cond)
+        pool.refine(sel)
         torch.cuda.synchronize()
         refine_ms = round((time.time() - r0) * 1e3, 2)
 
@@ -236,7 +238,7 @@ def main():
         "mfma_frac_end_to_end": round(tflops / PEAK_BF16_TFLOPS, 4),
         "algorithmic_tflop_per_step": round(flops / 1e12, 3),
         "roofline": {
-            "kernel": "k_linear_mfma<EPI_GELU> (MLP up-projection, M=%d N=%d K=%d)" % (M, wl.shape.mlp_hidden,
+            "kernel": "k_linear_ilv<EPI_GELU> (MLP up-projection, 256x256 tiles, M=%d N=%d K=%d)" % (M, wl.shape.mlp_hidden,
                                                                                    wl.shape.hidden),
             "bound": "mfma", "achieved": round(up_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
@@ -244,6 +246,7 @@ def main():
             "avg_launch_ms": round(up_avg_ms, 4), "launches": up_n,
         },
         "text_prep_ms": round(text_ms, 3),
+        "selection": selection,
         "refine_ms": refine_ms,
         "refine_steps": wl.steps_total - wl.steps_draft,
         "site_breakdown_one_draft": breakdown,

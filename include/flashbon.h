@@ -189,6 +189,28 @@ flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, cons
                                    flashbon_cache_meta *meta, float t_cur,
                                    flashbon_trace_entry *trace);
 
+/* Verifier callback of flashbon_select: judge candidate a (ranked above b) against candidate b.
+ * Returns the winner (a or b) and writes the verifier's confidence to *confidence: 0 high, 1 medium,
+ * 2 low.  Any other result aborts the selection with FLASHBON_EINVAL. */
+typedef int32_t (*flashbon_judge_fn)(void *ctx, int32_t a, int32_t b, int32_t *confidence);
+
+/* Multi-stage selection with Elo ratings (Sec. 4.2 Stage 2, Eq. 9-12), host only:
+ *   1. rating r_j = 1500 + 100 (scores[j] - 5) from the integer pointwise scores (1..10, host [m]);
+ *      keep the top ceil(rho1 m) -> M1 survivors;
+ *   2. ceil(kappa M1) verifier matches between neighbours of the rating order (sweeps over the
+ *      neighbour pairs, re-ordered by rating after each sweep; none if M1 < 2); keep the top
+ *      ceil(rho2 M1) -> M2 survivors;
+ *   3. every pair of the M2 survivors plays once (rating order at the stage's start, pairs (i, j),
+ *      i < j, lexicographically); *winner = the highest rating.
+ * Each match updates both ratings zero-sum by K c (S_a - E_a), E_a = 1 / (1 + 10^((r_b - r_a) / 400)),
+ * K = 32, c = 1.2 / 1.0 / 0.7 for high / medium / low confidence.  Orders break rating ties by the
+ * smaller index; ceil(x) is ceil(x - 1e-9).  rho1, rho2 in (0, 1], kappa >= 0 (paper: 0.5, 0.5, 1.5).
+ * ratings (host [m], final ratings) and pairwise_calls may be NULL.  Outputs are written only on
+ * success. */
+flashbon_status flashbon_select(int32_t m, const int32_t *scores, double rho1, double rho2, double kappa,
+                                flashbon_judge_fn judge, void *ctx, int32_t *winner, double *ratings,
+                                int32_t *pairwise_calls);
+
 /* Launch sites of the draft step whose device time can be measured (bit i of a site mask). */
 enum {
   FLASHBON_SITE_QKV = 0,        /* self-attention q/k/v projection        */

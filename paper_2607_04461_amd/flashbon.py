@@ -66,8 +66,11 @@ EXPORTS = [
     "flashbon_weight_count", "flashbon_init_model", "flashbon_text_kv_bytes", "flashbon_cache_bytes",
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
     "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_attention", "flashbon_op_ln_mod",
-    "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde",
+    "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde", "flashbon_select",
 ]
+
+JUDGE_FN = ctypes.CFUNCTYPE(ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                            ctypes.POINTER(ctypes.c_int32))
 
 
 def lib_path() -> str:
@@ -120,6 +123,10 @@ def load() -> ctypes.CDLL:
     L.flashbon_op_unpatch_sde.argtypes = [i32, i32, i32, i32, i32, vp, vp, f32, f32, f32, ctypes.c_uint64,
                                           i32, vp]
     L.flashbon_op_unpatch_sde.restype = i32
+    L.flashbon_select.argtypes = [i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_double, ctypes.c_double,
+                                  ctypes.c_double, JUDGE_FN, vp, ctypes.POINTER(ctypes.c_int32),
+                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
+    L.flashbon_select.restype = i32
     _lib = L
     return L
 
@@ -236,6 +243,34 @@ def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_k
                          trace=None, hidden_dump=None, stream=None, sde=None):
     _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde)
+
+
+def flashbon_select(scores, judge, rho1=0.5, rho2=0.5, kappa=1.5):
+    """Multi-stage Elo selection; ``judge(a, b) -> (winner, confidence)`` is the verifier.
+    Returns (winner, ratings [m] float64, pairwise calls)."""
+    sc = np.ascontiguousarray(np.asarray(scores, dtype=np.int32))
+    m = int(sc.size)
+    failure = []
+
+    def _cb(_ctx, a, b, conf):
+        try:
+            w, c = judge(int(a), int(b))
+            conf[0] = int(c)
+            return int(w)
+        except BaseException as e:  # the exception cannot cross the C frame; report it afterwards
+            failure.append(e)
+            return -1
+
+    cb = JUDGE_FN(_cb)
+    winner, calls = ctypes.c_int32(), ctypes.c_int32()
+    ratings = np.zeros(m, np.float64)
+    st = load().flashbon_select(m, sc.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), rho1, rho2, kappa, cb,
+                                None, ctypes.byref(winner),
+                                ratings.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ctypes.byref(calls))
+    if failure:
+        raise failure[0]
+    _check(st, "flashbon_select")
+    return int(winner.value), ratings, int(calls.value)
 
 
 def flashbon_plan_step(skip, proxy, meta, t_cur: float, trace=None):

@@ -82,6 +82,24 @@ class DraftPool:
                 on_step(k, self)
         return traces
 
+    def select(self, scores, judge, rho1: float = 0.5, rho2: float = 0.5, kappa: float = 1.5) -> int:
+        """Stage 2 (Sec. 4.2, Eq. 9-12): multi-stage Elo selection over the drafts, run by the library
+        on the host; ``scores`` are the verifier's pointwise scores, ``judge(a, b) -> (winner,
+        confidence)`` its pairwise calls.  Keeps (winner, ratings, pairwise calls) in
+        ``last_selection``."""
+        self.last_selection = fb.flashbon_select(scores, judge, rho1, rho2, kappa)
+        return self.last_selection[0]
+
+    def refine(self, j: int, out=None, stream=None):
+        """Stage 3 (Eq. 13): copy draft j's latent device-to-device (the pool stays intact for its
+        next use) and run the remaining steps S' .. S-1 with full computation.  Returns the latent."""
+        src = self.latents[j:j + 1]
+        z = src.clone() if out is None else out.copy_(src)
+        cond = self.cond_index[j:j + 1]
+        for k in range(self.wl.steps_draft, self.wl.steps_total):
+            self.refine_step(k, latents=z, cond_index=cond, stream=stream)
+        return z
+
     def close(self) -> None:
         if self.model:
             fb.flashbon_free(self.model)

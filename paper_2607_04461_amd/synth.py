@@ -224,11 +224,6 @@ def make_text(n_cond: int, text_len: int, text_dim: int, first_seed: int = 20_00
     return x
 
 
-def make_scores(n: int, seed: int) -> np.ndarray:
-    """Seeded stand-in verifier scores in [0, 1) for n candidates."""
-    return np.random.default_rng(seed).random(n)
-
-
 def random_cache_entries(shape: Tuple[int, ...], seed: int) -> np.ndarray:
     """Three ~N(0,1) cached activations stacked on axis 0 (for proxy-kernel tests)."""
     return np.random.default_rng(seed).standard_normal((3,) + tuple(shape), dtype=np.float32)
@@ -250,3 +245,36 @@ def random_matrix(shape: Tuple[int, ...], seed: int, scale: float = 1.0) -> np.n
     if scale != 1.0:
         a *= np.float32(scale)
     return a
+
+
+class SyntheticVerifier:
+    """Seeded stand-in for the paper's VLM verifier (Sec. 4.2 Stage 2), which is not part of this
+    library: every candidate has a hidden quality q_j ~ N(0, 1) (``default_rng(seed)``).
+
+    * pointwise score: integer 1..10, round(5.5 + 1.5 q_j + 0.75 n_j) clipped, n_j ~ N(0, 1) -- coarse
+      and tie-prone, like the integer scores the paper describes;
+    * pairwise judgement of (a, b): a wins with probability 1 / (1 + exp(-(q_a - q_b) / 0.5)), the
+      uniform draw coming from ``default_rng([seed, min(a, b), max(a, b), m])`` for the m-th meeting
+      of that pair, so an outcome depends only on the pair and how often it has met; confidence 0
+      (high) if |q_a - q_b| > 1, 1 (medium) if > 0.3, else 2 (low).
+    """
+
+    def __init__(self, m: int, seed: int):
+        rng = np.random.default_rng(seed)
+        self.seed = seed
+        self.quality = rng.standard_normal(m)
+        noise = rng.standard_normal(m)
+        self.scores = np.clip(np.rint(5.5 + 1.5 * self.quality + 0.75 * noise), 1, 10).astype(np.int32)
+        self.meetings: Dict[Tuple[int, int], int] = {}
+        self.calls = 0
+
+    def judge(self, a: int, b: int) -> Tuple[int, int]:
+        lo, hi = (a, b) if a < b else (b, a)
+        m = self.meetings.get((lo, hi), 0)
+        self.meetings[(lo, hi)] = m + 1
+        self.calls += 1
+        u = np.random.default_rng([self.seed, lo, hi, m]).random()
+        d = float(self.quality[a] - self.quality[b])
+        p_a = 1.0 / (1.0 + np.exp(-d / 0.5))
+        conf = 0 if abs(d) > 1.0 else (1 if abs(d) > 0.3 else 2)
+        return (a if u < p_a else b), conf

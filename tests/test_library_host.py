@@ -139,3 +139,41 @@ def test_normals_rejects_bad_arguments():
     assert lib.flashbon_op_normals(0, 0, 0, 1, 0x1000, None, None) == fb.ESHAPE
     assert lib.flashbon_op_normals(8, -1, 0, 1, 0x1000, None, None) == fb.EINVAL
     assert lib.flashbon_op_normals(8, 0, 0, 1, None, None, None) == fb.EINVAL
+
+
+@pytest.mark.parametrize("params", [(0.5, 0.5, 1.5), (0.25, 0.5, 1.0), (1.0, 1.0, 0.0), (0.3, 0.7, 2.5),
+                                    (1.0, 1.0, 3.0)])
+def test_select_matches_oracle_bit_exact(params):
+    """Host Elo selection (Sec. 4.2 Stage 2, Eq. 9-12) against the oracle: same matches in the same
+    order (the synthetic verifier's outcomes depend on the pair and its meeting count only), same
+    winner, bit-identical ratings and call count."""
+    from oracle import select as osel
+    for seed in range(6):
+        for m in (1, 2, 3, 5, 16, 33, 64, 100):
+            v_ref, v_lib = synth.SyntheticVerifier(m, seed), synth.SyntheticVerifier(m, seed)
+            w_ref, r_ref, st = osel.select(v_ref.scores, v_ref.judge, *params)
+            w, r, calls = fb.flashbon_select(v_lib.scores, v_lib.judge, *params)
+            assert (w, calls) == (w_ref, len(st["matches"])), (seed, m)
+            np.testing.assert_array_equal(r, np.array(r_ref))
+            assert v_lib.meetings == v_ref.meetings
+
+
+def test_select_rejects_bad_arguments():
+    judge = lambda a, b: (a, 0)
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_select([5, 11], judge)                        # score outside 1..10
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_select([5, 6], judge, rho1=0.0)
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_select([5, 6], judge, kappa=float("nan"))
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_select([], judge)
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_select([5, 6, 7, 8], lambda a, b: (99, 0))   # winner not a or b
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_select([5, 6, 7, 8], lambda a, b: (a, 3))    # unknown confidence
+
+    def broken(a, b):
+        raise KeyError("verifier down")
+    with pytest.raises(KeyError):
+        fb.flashbon_select([5, 6, 7, 8], broken)
