@@ -60,13 +60,13 @@ typedef enum {
  * LN is non-affine over `hidden`; head_dim = hidden / heads. */
 typedef struct {
   int32_t num_blocks;      /* L */
-  int32_t hidden;          /* D */
+  int32_t hidden;          /* D, multiple of 8, <= 6144 */
   int32_t heads;           /* H; hidden % heads == 0, head_dim in {8, 16, 32, 64, 128} */
-  int32_t mlp_hidden;      /* F */
+  int32_t mlp_hidden;      /* F, multiple of 8, <= 65536 */
   int32_t latent_channels; /* C */
   int32_t patch;           /* p (2): token = p x p patch of every channel */
   int32_t freq_dim;        /* width of the sinusoidal timestep features (even) */
-  int32_t text_dim;        /* width of the text-conditioning tokens */
+  int32_t text_dim;        /* width of the text-conditioning tokens, multiple of 8, <= 65536 */
   int32_t dtype;           /* flashbon_dtype */
   float ln_eps;            /* LayerNorm epsilon (1e-6) */
   int32_t max_n;           /* largest pool size a step may use */

@@ -27,7 +27,7 @@ enum {
 /* Linear layer: acc[m][n] = sum_k A[m][k] W[n][k] with fp32 accumulation (a DiT projection y = x W^T).
  * A: device act [M][K]; W: device act [N][K]; bias: device fp32 [N] or NULL (0);
  * out: device [M][N] (act or fp32 per epilogue); gate: device fp32 [N] or NULL; cache_out: device
- * fp32 [M][N] or NULL.  M, N >= 1; K >= 1 and K % 8 == 0. */
+ * fp32 [M][N] or NULL.  M, N >= 1, N % 4 == 0; 1 <= K <= 65536 and K % 8 == 0. */
 flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
                                    const void *W, const float *bias, int32_t epilogue, void *out,
                                    const float *gate, float *cache_out, void *stream);

@@ -21,13 +21,16 @@ template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
 
-// tanh-form GELU in fp32: 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))), with
-// tanh(u) = 1 - 2 / (exp(2u) + 1) so that large |u| saturates cleanly.
+// tanh-form GELU in fp32: 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).  Since
+// 0.5 (1 + tanh u) = 1 / (1 + exp(-2u)), it is x / (1 + 2^(-x (a + b x^2))) with
+// a = 2 sqrt(2/pi) log2(e) and b = 0.044715 a: one hardware exp2 and one hardware reciprocal
+// (about 1 ulp each) instead of an IEEE division.  Saturates cleanly: the exp2 overflows to +inf
+// for large negative x (result -0) and underflows to 0 for large positive x (result x).
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  float u = k0 * (x + 0.044715f * x * x * x);
-  float th = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
-  return 0.5f * x * (1.0f + th);
+  const float a = 2.302208198f;            // 2 sqrt(2/pi) / ln 2
+  const float b = 0.1029432396f;           // 0.044715 a
+  const float e = __builtin_amdgcn_exp2f(-x * fmaf(b, x * x, a));
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }

@@ -128,10 +128,19 @@ __device__ __forceinline__ void epilogue8(const EpiArgs &e, int m, int n, const 
 namespace mf {
 constexpr int BK = 64;
 // A workgroup is a WGM x WGN grid of waves, each computing a (16 WTM) x (16 WTN) tile of C.
-// LDS tile: [rows][64] bf16 = 8 chunks of 16 B per row, chunk c of row r stored at c ^ swz(r): the
-// 16 lanes of one ds_read_b128 phase (16 consecutive rows, one chunk) then cover all 64 banks.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+// LDS tile: [rows][64] bf16 = 8 chunks of 16 B per row, chunk c of row r stored at c ^ swz(r).  The
+// 16 lanes of one ds_read_b128 phase read one chunk of 16 rows and must land in 16 distinct 16-byte
+// slots of the 256-byte bank window, slot = (r & 1) 8 + (c ^ swz(r)).  With swz bits (r1, r2 ^ r4, r3)
+// that holds both for 16 consecutive rows (the A fragments) and for the permuted W fragment rows
+// {0..3, 8..11, 16..19, 24..27} (+ 4) of a 32-row group.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 5) | (((r >> 1) ^ (r >> 3)) & 2); }
 __device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ swz(r)) << 3); }
+
+// Raw buffer resource over `rows` rows of K bf16; loads past the range return zero.  The entry points
+// bound K by 65536, so 256 rows span at most 32 MiB, well inside the 32-bit range.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const bf16 *base, int rows, int K) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16 *>(base), (short)0, rows * K * 2, 0x00020000);
+}
 
 // Workgroup id -> (m tile, n tile).  Workgroups are dispatched round-robin over the 8 XCDs; each XCD
 // is given a contiguous range of tiles, and tiles are ordered in groups of GROUP_M m-tiles sweeping
@@ -151,8 +160,9 @@ __device__ __forceinline__ void tile_of(int bid, int MT, int NT, int &mt, int &n
 }
 }  // namespace mf
 
+// A 4-wave workgroup must leave room for a second one on the CU (2 waves per SIMD, <= 256 registers).
 template <int WTM, int WTN, int WGM, int WGN, int DEPTH, bool KTAIL, int EPI, typename TO>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void k_linear_mfma(int M, int N, int K,
+__global__ __launch_bounds__(64 * WGM * WGN, WGM * WGN <= 4 ? 2 : 1) void k_linear_mfma(int M, int N, int K,
                                                                    const bf16 *__restrict__ A,
                                                                    const bf16 *__restrict__ Wt,
                                                                    EpiArgs e, int MT, int NT) {
@@ -320,18 +330,17 @@ __global__ __launch_bounds__(512, 1) void k_linear_ilv(int M, int N, int K, cons
   tile_of(blockIdx.x, MT, NT, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
   const int ld_r = tid >> 3, ld_c = tid & 7;
-  const bf16 *Ab = A + (int64_t)m0 * K + ld_c * 8, *Wb = Wt + (int64_t)n0 * K + ld_c * 8;
-  uint32_t oa[LA], ow[LW];
-#pragma unroll
-  for (int i = 0; i < LA; ++i) oa[i] = (uint32_t)(min(ld_r + ROWS * i, M - 1 - m0) * K);
-#pragma unroll
-  for (int i = 0; i < LW; ++i) ow[i] = (uint32_t)(min(ld_r + ROWS * i, N - 1 - n0) * K);
+  // Buffer loads over the workgroup's rows: rows past M (N) fall outside the buffer's range and
+  // read as zero, so one VGPR offset per thread serves every load (row step and K step are scalar).
+  const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
+  const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
+  const int voff = (ld_r * K + ld_c * 8) * 2;
   u32x4 ra[LA], rw[LW];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < LA; ++i) ra[i] = *reinterpret_cast<const u32x4 *>(Ab + oa[i] + k0);
+    for (int i = 0; i < LA; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rsA, voff, (ROWS * i * K + k0) * 2, 0);
 #pragma unroll
-    for (int i = 0; i < LW; ++i) rw[i] = *reinterpret_cast<const u32x4 *>(Wb + ow[i] + k0);
+    for (int i = 0; i < LW; ++i) rw[i] = __builtin_amdgcn_raw_buffer_load_b128(rsW, voff, (ROWS * i * K + k0) * 2, 0);
   };
   auto lstore = [&](bf16 *sA) {
     bf16 *sW = sA + BM * BK;

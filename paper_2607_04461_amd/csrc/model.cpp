@@ -31,11 +31,13 @@ bool config_ok(const flashbon_model_config *c, std::string *why) {
   int dh = c->hidden / c->heads;
   if (dh != 8 && dh != 16 && dh != 32 && dh != 64 && dh != 128)
     return bad("head_dim must be one of 8, 16, 32, 64, 128");
-  if (c->mlp_hidden < 8 || c->mlp_hidden % 8) return bad("mlp_hidden must be a positive multiple of 8");
+  if (c->mlp_hidden < 8 || c->mlp_hidden % 8 || c->mlp_hidden > 65536)
+    return bad("mlp_hidden must be a positive multiple of 8, <= 65536");
   if (c->latent_channels < 1 || c->patch < 1) return bad("latent_channels and patch must be >= 1");
   if ((c->latent_channels * c->patch * c->patch) % 8) return bad("latent_channels*patch^2 must be a multiple of 8");
   if (c->freq_dim < 2 || c->freq_dim % 8) return bad("freq_dim must be a positive multiple of 8");
-  if (c->text_dim < 8 || c->text_dim % 8) return bad("text_dim must be a positive multiple of 8");
+  if (c->text_dim < 8 || c->text_dim % 8 || c->text_dim > 65536)
+    return bad("text_dim must be a positive multiple of 8, <= 65536");
   if (c->dtype != FLASHBON_FP32 && c->dtype != FLASHBON_BF16) return bad("dtype must be FP32 or BF16");
   if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return bad("ln_eps must be positive");
   if (c->max_n < 1 || c->max_tokens < 1 || c->max_text_len < 1 || c->max_cond < 1)

@@ -23,7 +23,8 @@ flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t 
                                    const void *W, const float *bias, int32_t epilogue, void *out,
                                    const float *gate, float *cache_out, void *stream) {
   if (dtype != FLASHBON_FP32 && dtype != FLASHBON_BF16) return fail(FLASHBON_EINVAL, "bad dtype");
-  if (M < 1 || N < 1 || K < 1 || K % 8 || N % 4) return fail(FLASHBON_ESHAPE, "need M,N,K >= 1, K % 8 == 0, N % 4 == 0");
+  if (M < 1 || N < 1 || K < 1 || K % 8 || N % 4 || K > 65536)
+    return fail(FLASHBON_ESHAPE, "need M,N,K >= 1, K <= 65536, K % 8 == 0, N % 4 == 0");
   if (!A || !W || !out) return fail(FLASHBON_EINVAL, "A, W and out are required");
   if (epilogue < FLASHBON_EPI_STORE || epilogue > FLASHBON_EPI_RESIDUAL) return fail(FLASHBON_EINVAL, "bad epilogue");
   EpiArgs e;

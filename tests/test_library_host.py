@@ -93,6 +93,7 @@ def test_weight_count_of_published_shapes():
 
 
 @pytest.mark.parametrize("field,value", [("hidden", 60), ("heads", 5), ("mlp_hidden", 12), ("dtype", 7),
+                                         ("mlp_hidden", 65544), ("text_dim", 65544), ("hidden", 6152),
                                          ("max_n", 0), ("ln_eps", 0.0), ("freq_dim", 6), ("num_blocks", 0)])
 def test_invalid_config_rejected(field, value):
     cfg = fb.make_config(synth.TINY, fb.FP32, 2, 16, 8, 1)
