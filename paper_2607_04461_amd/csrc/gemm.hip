@@ -480,6 +480,8 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
 // workgroups per CU, loads issued two K tiles ahead).  Estimated time = rounds of resident
 // workgroups x work per round / relative efficiency; the efficiencies are measured on MI355X
 // (the 128x128 tile reaches 0.88 of the 256x256 tile's throughput per CU).
+static bool tile_forced() { return getenv("FLASHBON_LINEAR_TILE") != nullptr; }
+
 static bool pick_big_tile(int M, int N, int K) {
   const char *force = getenv("FLASHBON_LINEAR_TILE");  // "256x256" or "128x128": tests and tuning
   if (force) return strcmp(force, "128x128") != 0;
@@ -526,13 +528,48 @@ static hipError_t launch_ilv(int M, int N, int K, const void *A, const void *Wt,
   return hipGetLastError();
 }
 
+static int cu_count() {
+  static int n = 0;
+  if (!n) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
+
+// The rows [m, M) of a problem: operand and output pointers moved down by m rows.
+template <int EPI>
+static EpiArgs rows_from(const EpiArgs &e, int m) {
+  EpiArgs r = e;
+  const size_t osz = (EPI == EPI_STORE || EPI == EPI_GELU) ? sizeof(bf16) : sizeof(float);
+  r.out = (char *)e.out + (size_t)m * e.ldo * osz;
+  if (r.cache) r.cache = e.cache + (size_t)m * e.ldo;
+  return r;
+}
+
 template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
     if (pick_big_tile(M, N, K)) {
-      if (K % mf::BK == 0) return launch_ilv<EPI>(M, N, K, A, Wt, e, s);
-      return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+      if (K % mf::BK) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+      // One 256x256 workgroup per CU: when the last round of tiles would leave most CUs idle, the
+      // whole rows of tiles that fit in full rounds take the 256x256 kernel and the remaining rows
+      // the 128x128 kernel (two workgroups per CU, a quarter of the work per tile).
+      const int MT = (M + 255) / 256, NT = (N + 255) / 256, T = MT * NT, cus = cu_count();
+      const int tail = T % cus, mt_big = (T - tail) / NT;
+      if (EPI != EPI_EULER && !tile_forced() && tail && 2 * tail < cus && mt_big >= 1 && mt_big < MT) {
+        const int rows = mt_big * 256;
+        hipError_t err = launch_ilv<EPI>(rows, N, K, A, Wt, e, s);
+        if (err != hipSuccess) return err;
+        return launch_mfma<4, 4, 2, 2, EPI, 2>(M - rows, N, K, (const bf16 *)A + (size_t)rows * K, Wt,
+                                               rows_from<EPI>(e, rows), s);
+      }
+      return launch_ilv<EPI>(M, N, K, A, Wt, e, s);
     }
     return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
   }

@@ -230,3 +230,33 @@ def test_proxy_kernel_constant_is_exact():
     F.flashbon_op_proxy(4099, c, c, c, 2, 0.25, 0.5, 0.125, out)
     torch.cuda.synchronize()
     assert torch.equal(out, c)
+
+
+@pytest.mark.parametrize("M,N,K,epi,split", [(24960, 1536, 8960, "residual", 21760), (24960, 8960, 1536, "gelu", 24320)])
+def test_linear_tail_rows_split(M, N, K, epi, split):
+    """On 256 CUs these shapes leave the last round of 256x256 tiles mostly idle, so rows from `split`
+    on run in the 128x128 kernel (a second launch on moved pointers).  Rows on both sides of the
+    split and the last row, against the oracle; the RESIDUAL cache copy must follow the output."""
+    F = fb()
+    A = _operand((M, K), 81, "bf16")
+    W = _operand((N, K), 82, "bf16", 0.02)
+    bias = synth.random_matrix((N,), 83)
+    rows = np.array([0, 255, split - 256, split - 1, split, split + 1, split + 127, split + 128, M - 2, M - 1])
+    ref = odit.linear(A[rows].astype(np.float64), W, bias)
+    idx = torch.from_numpy(rows).cuda()
+    if epi == "gelu":
+        out = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        F.flashbon_op_linear(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"), F.EPI_GELU, out)
+        torch.cuda.synchronize()
+        assert rel_l2(out[idx].float().cpu().numpy(), odit.gelu_tanh(ref)) <= 6e-3
+    else:
+        h0 = torch.from_numpy(synth.random_matrix((M, N), 84)).cuda()
+        gate = synth.random_matrix((N,), 85)
+        out = h0.clone()
+        cache = torch.zeros((M, N), device="cuda", dtype=torch.float32)
+        F.flashbon_op_linear(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"),
+                             F.EPI_RESIDUAL, out, _dev(gate, "fp32"), cache)
+        torch.cuda.synchronize()
+        assert torch.equal(cache, out)
+        expect = h0[idx].cpu().numpy().astype(np.float64) + gate * ref
+        assert rel_l2(out[idx].cpu().numpy(), expect) <= 2e-6
