@@ -476,20 +476,33 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
   }
 }
 
-// Tile choice: a 256x256 workgroup tile (8 waves, 2 per SIMD) or a 128x128 one (4 waves, two
-// workgroups per CU, loads issued two K tiles ahead).  Estimated time = rounds of resident
-// workgroups x work per round / relative efficiency; the efficiencies are measured on MI355X
-// (the 128x128 tile reaches 0.88 of the 256x256 tile's throughput per CU).
-static bool tile_forced() { return getenv("FLASHBON_LINEAR_TILE") != nullptr; }
+// Tile choice for bf16 operands.  The 256x256 kernel runs one workgroup per CU, the 128x128 kernel
+// two; a launch takes ceil(tiles / slots) rounds.  Measured on MI355X, a round of 128x128 tiles
+// costs 0.64 of a round of 256x256 tiles at the same K (so the small tile does 0.78 of the big
+// tile's work per CU).  Candidates: all 256x256; all 128x128; or the whole rows of 256x256 tiles
+// that fill complete rounds plus the remaining rows as 128x128 tiles (a second launch), which
+// trims a last round that would leave most CUs idle.
+enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT };
+static int cu_count();
 
-static bool pick_big_tile(int M, int N, int K) {
+static TilePlan pick_tiles(int M, int N, int K, int *split_rows) {
   const char *force = getenv("FLASHBON_LINEAR_TILE");  // "256x256" or "128x128": tests and tuning
-  if (force) return strcmp(force, "128x128") != 0;
-  // long K amortises the big tile's prologue/epilogue (measured: 24960 x 1536 x 8960 runs 6% faster)
-  if (K >= 4096 && N >= 1024 && M >= 4096) return true;
-  const double t256 = ceil((double)((M + 255) / 256) * ((N + 255) / 256) / 256.0) * 256.0 * 256.0;
-  const double t128 = ceil((double)((M + 127) / 128) * ((N + 127) / 128) / 512.0) * 2.0 * 128.0 * 128.0 / 0.88;
-  return t256 <= t128;
+  if (force) return strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL;
+  constexpr double kSmallRound = 0.64;
+  const int cus = cu_count();
+  const int64_t NT = (N + 255) / 256, T = (int64_t)((M + 255) / 256) * NT, NT2 = (N + 127) / 128;
+  const double t_big = (double)((T + cus - 1) / cus);
+  const double t_small = (double)((((M + 127) / 128) * NT2 + 2 * cus - 1) / (2 * cus)) * kSmallRound;
+  double t_split = 1e30;
+  const int64_t mt_big = (T - T % cus) / NT;
+  const int rows = (int)(mt_big * 256);
+  if (K % mf::BK == 0 && rows > 0 && rows < M) {
+    const int64_t T2 = ((M - rows + 127) / 128) * NT2;
+    t_split = (double)((mt_big * NT + cus - 1) / cus) + (double)((T2 + 2 * cus - 1) / (2 * cus)) * kSmallRound;
+  }
+  *split_rows = rows;
+  if (t_split < t_big && t_split < t_small) return PLAN_SPLIT;
+  return t_big <= t_small ? PLAN_BIG : PLAN_SMALL;
 }
 
 template <int WTM, int WTN, int WGM, int WGN, int EPI, int DEPTH>
@@ -555,23 +568,16 @@ template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
-    if (pick_big_tile(M, N, K)) {
-      if (K % mf::BK) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
-      // One 256x256 workgroup per CU: when the last round of tiles would leave most CUs idle, the
-      // whole rows of tiles that fit in full rounds take the 256x256 kernel and the remaining rows
-      // the 128x128 kernel (two workgroups per CU, a quarter of the work per tile).
-      const int MT = (M + 255) / 256, NT = (N + 255) / 256, T = MT * NT, cus = cu_count();
-      const int tail = T % cus, mt_big = (T - tail) / NT;
-      if (EPI != EPI_EULER && !tile_forced() && tail && 2 * tail < cus && mt_big >= 1 && mt_big < MT) {
-        const int rows = mt_big * 256;
-        hipError_t err = launch_ilv<EPI>(rows, N, K, A, Wt, e, s);
-        if (err != hipSuccess) return err;
-        return launch_mfma<4, 4, 2, 2, EPI, 2>(M - rows, N, K, (const bf16 *)A + (size_t)rows * K, Wt,
-                                               rows_from<EPI>(e, rows), s);
-      }
-      return launch_ilv<EPI>(M, N, K, A, Wt, e, s);
-    }
-    return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
+    int rows = 0;
+    TilePlan plan = pick_tiles(M, N, K, &rows);
+    if (plan == PLAN_SPLIT && EPI == EPI_EULER) plan = PLAN_BIG;   // the latent scatter needs whole rows
+    if (plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
+    if (K % mf::BK) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+    if (plan == PLAN_BIG) return launch_ilv<EPI>(M, N, K, A, Wt, e, s);
+    hipError_t err = launch_ilv<EPI>(rows, N, K, A, Wt, e, s);
+    if (err != hipSuccess) return err;
+    return launch_mfma<4, 4, 2, 2, EPI, 2>(M - rows, N, K, (const bf16 *)A + (size_t)rows * K, Wt,
+                                           rows_from<EPI>(e, rows), s);
   }
   dim3 grid((M + 63) / 64, (N + 63) / 64);
   hipLaunchKernelGGL((k_linear_valu<float, EPI, float>), grid, dim3(256), 0, s, M, N, K,
