@@ -107,6 +107,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-breakdown", action="store_true")
     ap.add_argument("--no-refine", action="store_true", help="skip timing the refinement")
+    ap.add_argument("--no-sde", action="store_true", help="skip timing the stochastic-update kernel")
     ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB three times (counter calibration)")
     args = ap.parse_args()
@@ -204,6 +205,31 @@ def main():
         torch.cuda.synchronize()
         refine_ms = round((time.time() - r0) * 1e3, 2)
 
+    # the stochastic update (App. A.1, Eq. 20) at the pool's latent shape: one fused unpatchify +
+    # update launch; HBM-bound, algorithmic bytes = read z, read v, write z (12 bytes per element)
+    sde = None
+    if not args.no_sde:
+        C, H, Wd, p = wl.shape.latent_channels, wl.latent_h, wl.latent_w, wl.shape.patch
+        v_tok = torch.randn(M, C * p * p, device="cuda")
+        z_sde = torch.randn(wl.n, C, H, Wd, device="cuda")
+        args_sde = (wl.n, C, H, Wd, p, v_tok, z_sde, 0.8, 0.78, 0.3, 1234, 0)
+        for _ in range(5):
+            fb.flashbon_op_unpatch_sde(*args_sde)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(200):
+            fb.flashbon_op_unpatch_sde(*args_sde)
+        e1.record()
+        torch.cuda.synchronize()
+        sde_us = e0.elapsed_time(e1) / 200 * 1e3
+        sde_bytes = 12.0 * z_sde.numel()
+        sde = {"kernel": "k_unpatch_sde (Philox4x32-10 + Box-Muller normals, unpatchify, Eq. 20 update)",
+               "elements": z_sde.numel(), "avg_launch_us": round(sde_us, 2), "bound": "hbm",
+               "achieved_GBs": round(sde_bytes / sde_us / 1e3, 1), "peak_GBs": PEAK_HBM_GBS,
+               "frac": round(sde_bytes / sde_us / 1e3 / PEAK_HBM_GBS, 4)}
+        del v_tok, z_sde
+
     if args.calibration_copy:
         n = args.calibration_copy * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -248,6 +274,7 @@ def main():
         },
         "text_prep_ms": round(text_ms, 3),
         "selection": selection,
+        "sde_update": sde,
         "refine_ms": refine_ms,
         "refine_steps": wl.steps_total - wl.steps_draft,
         "site_breakdown_one_draft": breakdown,

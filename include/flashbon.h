@@ -138,12 +138,14 @@ typedef struct {
    *   z <- z + dt [v + sigma^2 / (2 t) (z + (1 - t) v)] + sigma sqrt(|dt|) eps,
    *   t = t_cur, dt = t_next - t_cur, sigma = sde_a sqrt(t / (1 - t)) (1 - t_next when t = 1),
    * eps[b][e] (flat element e of candidate row b of this call) = normal e % 4 of Philox4x32-10 with
-   * key (sde_seed low 32 bits, high 32 bits) and counter (e / 4, b, sde_step, 0), through Box-Muller
+   * key (sde_seed low 32 bits, high 32 bits) and counter (e / 4, sde_row0 + b, sde_step, 0), through Box-Muller
    * (u1 = (w0 + 1) 2^-32, u2 = w1 2^-32; r = sqrt(-2 ln u1); r cos 2 pi u2, r sin 2 pi u2; then w2, w3).
    * Requires 0 < t_cur <= 1 (t_next < 1 if t_cur = 1); else FLASHBON_EINVAL before any device work. */
   float sde_a;       /* noise level a >= 0 */
   int32_t sde_step;  /* third counter word: a distinct value per step keeps draws independent */
   uint64_t sde_seed; /* Philox key */
+  int32_t sde_row0;  /* candidate index of row 0 in the counter (>= 0): a slice of a larger pool, or a
+                        single refined candidate, draws the normals of its place in the pool */
 } flashbon_step_args;
 
 /* Number of floats `host_weights` must hold for `cfg`. Returns 0 if cfg is invalid. */

@@ -67,11 +67,12 @@ flashbon_status flashbon_op_normals(int64_t count, int32_t candidate, int32_t st
 
 /* Unpatchify + stochastic update (Eq. 20) as the step performs it: v is the head output, device fp32
  * [n (H/p)(W/p)][C p p] (token i (W/p) + j of candidate b, column c p^2 + p di + dj <-> z[b][c][p i +
- * di][p j + dj]); z device fp32 [n][C][H][W] updated in place; the rest as in flashbon_step_args.
+ * di][p j + dj]); z device fp32 [n][C][H][W] updated in place; row b draws counter row row0 + b;
+ * the rest as in flashbon_step_args.
  * H, W positive multiples of p. */
 flashbon_status flashbon_op_unpatch_sde(int32_t n, int32_t C, int32_t H, int32_t W, int32_t p,
                                         const float *v, float *z, float t_cur, float t_next, float a,
-                                        uint64_t seed, int32_t step, void *stream);
+                                        uint64_t seed, int32_t step, int32_t row0, void *stream);
 
 #ifdef __cplusplus
 }

@@ -202,8 +202,8 @@ def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float,
                    noise: Optional[Tuple[float, int, int]] = None) -> np.ndarray:
     """One denoising step of one candidate under an already-planned trace; returns z_next [C, H, W].
 
-    ``noise = (a, seed, step)`` replaces the Euler update by the stochastic one of App. A.1 (Eq. 20)
-    with the normals of candidate ``cand`` at counter ``step`` (oracle/sde.py).
+    ``noise = (a, seed, step, row)`` replaces the Euler update by the stochastic one of App. A.1
+    (Eq. 20) with the normals of counter row ``row`` at counter ``step`` (oracle/sde.py).
     """
     C, H, Wd = z.shape
     p = shape.patch
@@ -230,10 +230,19 @@ def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float,
     out = linear(a, W["head_w"], W["head_b"])
     v = unpatchify(out, C, H, Wd, p)
     if noise is not None:
-        a, seed, step = noise
-        eps = sde.latent_normals(z.shape, cand, step, seed)
+        a, seed, step, row = noise
+        eps = sde.latent_normals(z.shape, row, step, seed)
         return sde.sde_update(z, v, t_cur, t_next, a, eps)
     return np.asarray(z, f64) + (f64(t_next) - f64(t_cur)) * v
+
+
+def _noise(sde_args, n: int):
+    """(a, seed, step[, row0]) -> the noise tuple of candidate row n, or None."""
+    if sde_args is None:
+        return None
+    a, seed, step = sde_args[:3]
+    row0 = sde_args[3] if len(sde_args) > 3 else 0
+    return a, seed, step, row0 + n
 
 
 def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
@@ -246,8 +255,8 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
 
     z [N, C, H, W]; returns (z_next [N, C, H, W] fp64 -- rows not in ``candidates`` are left as z --,
     trace).  The cache metadata advances once per step, as all candidates share the masks.
-    ``sde_args = (a, seed, step)`` selects the stochastic update (Eq. 20), candidate n drawing the
-    normals of counter (n, step).
+    ``sde_args = (a, seed, step[, row0])`` selects the stochastic update (Eq. 20), candidate n
+    drawing the normals of counter row row0 + n (row0 = 0 by default) at ``step``.
     """
     trace, new_meta = plan_step(skip, proxy, cache.meta, t_cur)
     block_mod, head_mod = modulations(W, shape.num_blocks, shape.freq_dim, t_cur)
@@ -255,7 +264,7 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
     for n in (range(z.shape[0]) if candidates is None else candidates):
         hid = None if hidden is None else hidden.setdefault(n, [])
         out[n] = candidate_step(W, shape, z[n], t_cur, t_next, kv_per_cond[int(cond_index[n])],
-                                block_mod, head_mod, trace, cache.meta, cache, n, hid, sde_args)
+                                block_mod, head_mod, trace, cache.meta, cache, n, hid, _noise(sde_args, n))
     cache.meta = new_meta
     return out, trace
 
@@ -274,7 +283,7 @@ def refine_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_
     out = np.asarray(z, f64).copy()
     for n in (range(z.shape[0]) if candidates is None else candidates):
         out[n] = candidate_step(W, shape, z[n], t_cur, t_next, kv_per_cond[int(cond_index[n])],
-                                block_mod, head_mod, trace, None, None, n, None, sde_args)
+                                block_mod, head_mod, trace, None, None, n, None, _noise(sde_args, n))
     return out
 
 

@@ -70,11 +70,12 @@ hipError_t launch_f32_to_bf16(int64_t count, const float *x, void *y, hipStream_
 // with key (key0, key1) and counter (element / 4, candidate, step, 0) through Box-Muller.
 struct SdeArgs {
   float dt, k, omt, g;
-  uint32_t key0, key1, step;
+  uint32_t key0, key1, step, row0;
 };
 // Host: coefficients for noise level a at (t_cur, t_next); false if a < 0, t_cur outside (0, 1] or
-// sigma_t is not finite.
-bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, SdeArgs *out);
+// sigma_t is not finite.  Row b of a launch draws counter row row0 + b.
+bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, int32_t row0,
+                      SdeArgs *out);
 // z [n][C][H][W] fp32 updated in place from v = head output [n T][C p p] fp32 (unpatchified here)
 hipError_t launch_unpatch_sde(int n, int C, int H, int W, int p, const float *v, float *z,
                               const SdeArgs &a, hipStream_t s);

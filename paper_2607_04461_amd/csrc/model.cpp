@@ -296,8 +296,9 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   }
   SdeArgs sde;
   const bool stochastic = a->sde_a != 0.f;
-  if (stochastic && a->sde_step < 0) return fail(FLASHBON_EINVAL, "sde_step must be >= 0");
-  if (stochastic && !sde_coefficients(a->t_cur, a->t_next, a->sde_a, a->sde_seed, a->sde_step, &sde))
+  if (stochastic && (a->sde_step < 0 || a->sde_row0 < 0))
+    return fail(FLASHBON_EINVAL, "sde_step and sde_row0 must be >= 0");
+  if (stochastic && !sde_coefficients(a->t_cur, a->t_next, a->sde_a, a->sde_seed, a->sde_step, a->sde_row0, &sde))
     return fail(FLASHBON_EINVAL, "stochastic update needs sde_a >= 0, finite, and 0 < t_cur <= 1 (t_next < 1 when t_cur = 1)");
 
   // ---------------------------------------------------------------- enqueue

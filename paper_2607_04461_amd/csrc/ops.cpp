@@ -95,14 +95,14 @@ flashbon_status flashbon_op_normals(int64_t count, int32_t candidate, int32_t st
 
 flashbon_status flashbon_op_unpatch_sde(int32_t n, int32_t C, int32_t H, int32_t W, int32_t p,
                                         const float *v, float *z, float t_cur, float t_next, float a,
-                                        uint64_t seed, int32_t step, void *stream) {
+                                        uint64_t seed, int32_t step, int32_t row0, void *stream) {
   if (n < 1 || n > 65535 || C < 1 || p < 1 || H < p || W < p || H % p || W % p)
     return fail(FLASHBON_ESHAPE, "need 1 <= n <= 65535, C >= 1, H and W positive multiples of p");
   if ((int64_t)C * H * W > INT32_MAX) return fail(FLASHBON_ESHAPE, "C H W must fit in int32");
   if (!v || !z) return fail(FLASHBON_EINVAL, "v and z are required");
-  if (step < 0) return fail(FLASHBON_EINVAL, "step must be >= 0");
+  if (step < 0 || row0 < 0) return fail(FLASHBON_EINVAL, "step and row0 must be >= 0");
   SdeArgs s;
-  if (!sde_coefficients(t_cur, t_next, a, seed, step, &s))
+  if (!sde_coefficients(t_cur, t_next, a, seed, step, row0, &s))
     return fail(FLASHBON_EINVAL, "need a >= 0, finite, and 0 < t_cur <= 1 (t_next < 1 when t_cur = 1)");
   return launched(launch_unpatch_sde(n, C, H, W, p, v, z, s, (hipStream_t)stream), "unpatch_sde");
 }

@@ -5,8 +5,9 @@
 //
 // eps for flat element e of candidate b's latent [C][H][W] at step s is normal e % 4 of one
 // Philox4x32-10 block (Salmon, Moraes, Dror, Shaw: "Parallel random numbers: as easy as 1, 2, 3",
-// SC'11) with key (seed low word, seed high word) and counter (e / 4, b, s, 0), the four 32-bit words
-// turned into four normals by the Box-Muller transform, computed in double:
+// SC'11) with key (seed low word, seed high word) and counter (e / 4, row0 + b, s, 0), where row0 is
+// the pool index of the launch's first row; the four 32-bit words become four normals by the
+// Box-Muller transform, computed in double:
 // u1 = (w0 + 1) 2^-32, u2 = w1 2^-32, r = sqrt(-2 ln u1), normals r cos(2 pi u2), r sin(2 pi u2);
 // (w2, w3) likewise.  One thread owns one counter, i.e. four consecutive latent elements, so every
 // generated normal is used once.  The kernel is HBM-bound: per element it reads z and v and writes z.
@@ -57,7 +58,7 @@ __global__ __launch_bounds__(256) void k_unpatch_sde(int C, int H, int W, int p,
   if (q >= quads) return;
   uint32_t w[4];
   float eps[4];
-  normals4((uint32_t)q, (uint32_t)b, s.step, s.key0, s.key1, w, eps);
+  normals4((uint32_t)q, s.row0 + (uint32_t)b, s.step, s.key0, s.key1, w, eps);
   const int hw = H * W, wp = W / p, pp = p * p;
   const int64_t T = (int64_t)(H / p) * wp, P = (int64_t)C * pp;
   float *zb = z + (int64_t)b * chw;
@@ -95,7 +96,8 @@ __global__ __launch_bounds__(256) void k_normals(int64_t count, uint32_t cand, u
   }
 }
 
-bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, SdeArgs *out) {
+bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, int32_t row0,
+                      SdeArgs *out) {
   const double tc = t_cur, tn = t_next, dt = tn - tc;
   if (!(a >= 0.f) || !std::isfinite(a) || !(tc > 0.0) || !(tc <= 1.0)) return false;
   const double one_minus = tc < 1.0 ? 1.0 - tc : 1.0 - tn;
@@ -108,6 +110,7 @@ bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t
   out->key0 = (uint32_t)(seed & 0xFFFFFFFFu);
   out->key1 = (uint32_t)(seed >> 32);
   out->step = (uint32_t)step;
+  out->row0 = (uint32_t)row0;
   return std::isfinite(out->k) && std::isfinite(out->g);
 }
 

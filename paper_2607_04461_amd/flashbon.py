@@ -59,6 +59,7 @@ class StepArgs(ctypes.Structure):
         ("trace", ctypes.POINTER(TraceEntry)), ("hidden_dump", ctypes.c_void_p),
         ("stream", ctypes.c_void_p),
         ("sde_a", ctypes.c_float), ("sde_step", ctypes.c_int32), ("sde_seed", ctypes.c_uint64),
+        ("sde_row0", ctypes.c_int32),
     ]
 
 
@@ -121,7 +122,7 @@ def load() -> ctypes.CDLL:
     L.flashbon_op_normals.argtypes = [i64, i32, i32, ctypes.c_uint64, vp, vp, vp]
     L.flashbon_op_normals.restype = i32
     L.flashbon_op_unpatch_sde.argtypes = [i32, i32, i32, i32, i32, vp, vp, f32, f32, f32, ctypes.c_uint64,
-                                          i32, vp]
+                                          i32, i32, vp]
     L.flashbon_op_unpatch_sde.restype = i32
     L.flashbon_select.argtypes = [i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_double, ctypes.c_double,
                                   ctypes.c_double, JUDGE_FN, vp, ctypes.POINTER(ctypes.c_int32),
@@ -227,13 +228,14 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
     a.stream = _stream(stream)
     if sde is not None:
         a.sde_a, a.sde_seed, a.sde_step = float(sde[0]), int(sde[1]), int(sde[2])
+        a.sde_row0 = int(sde[3]) if len(sde) > 3 else 0
     _check(fn(model, ctypes.byref(a)), where)
 
 
 def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
                         skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None, sde=None):
     """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays;
-    ``sde = (a, seed, step)`` selects the stochastic update (None or a = 0: Euler)."""
+    ``sde = (a, seed, step[, row0])`` selects the stochastic update (None or a = 0: Euler)."""
     _step(load().flashbon_draft_step, "flashbon_draft_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, skip, proxy, cache, meta, trace, hidden_dump, stream,
           num_blocks=len(meta), sde=sde)
@@ -328,6 +330,6 @@ def flashbon_op_normals(count, candidate, step, seed, words=None, normals=None, 
                                       _stream(stream)), "flashbon_op_normals")
 
 
-def flashbon_op_unpatch_sde(n, C, H, W, p, v, z, t_cur, t_next, a, seed, step, stream=None):
-    _check(load().flashbon_op_unpatch_sde(n, C, H, W, p, _ptr(v), _ptr(z), t_cur, t_next, a, seed, step,
+def flashbon_op_unpatch_sde(n, C, H, W, p, v, z, t_cur, t_next, a, seed, step, row0=0, stream=None):
+    _check(load().flashbon_op_unpatch_sde(n, C, H, W, p, _ptr(v), _ptr(z), t_cur, t_next, a, seed, step, row0,
                                           _stream(stream)), "flashbon_op_unpatch_sde")

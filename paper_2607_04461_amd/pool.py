@@ -67,11 +67,12 @@ class DraftPool:
 
     def refine_step(self, k: int, latents=None, cond_index=None, hidden_dump=None, stream=None,
                     sde=None) -> list:
+        """Step k with every knob off; ``sde = (a, seed[, row0])`` takes the stochastic update."""
         lat = self.latents if latents is None else latents
         cond = self.cond_index if cond_index is None else cond_index
         fb.flashbon_refine_step(self.model, lat, self.schedule[k], self.schedule[k + 1], self.text, cond,
                                 self.text_kv, self.text_kv_valid, self.trace, hidden_dump, stream,
-                                None if sde is None else (sde[0], sde[1], k))
+                                None if sde is None else (sde[0], sde[1], k, sde[2] if len(sde) > 2 else 0))
         return fb.trace_list(self.trace)
 
     def draft(self, steps: Optional[int] = None, on_step: Optional[Callable] = None) -> List[list]:
@@ -90,14 +91,16 @@ class DraftPool:
         self.last_selection = fb.flashbon_select(scores, judge, rho1, rho2, kappa)
         return self.last_selection[0]
 
-    def refine(self, j: int, out=None, stream=None):
+    def refine(self, j: int, out=None, stream=None, sde=None):
         """Stage 3 (Eq. 13): copy draft j's latent device-to-device (the pool stays intact for its
-        next use) and run the remaining steps S' .. S-1 with full computation.  Returns the latent."""
+        next use) and run the remaining steps S' .. S-1 with full computation.  ``sde = (a, seed)``
+        keeps the stochastic update with candidate j's own normals.  Returns the latent."""
         src = self.latents[j:j + 1]
         z = src.clone() if out is None else out.copy_(src)
         cond = self.cond_index[j:j + 1]
         for k in range(self.wl.steps_draft, self.wl.steps_total):
-            self.refine_step(k, latents=z, cond_index=cond, stream=stream)
+            self.refine_step(k, latents=z, cond_index=cond, stream=stream,
+                             sde=None if sde is None else (sde[0], sde[1], j))
         return z
 
     def close(self) -> None:

@@ -53,35 +53,37 @@ def test_normals_match_oracle(count, cand, step, seed):
     assert np.max(np.abs(got_z - ref_z)) <= 1e-6
 
 
-def _ref_unpatch_sde(v_tok, z, C, H, W, p, t_cur, t_next, a, seed, step):
+def _ref_unpatch_sde(v_tok, z, C, H, W, p, t_cur, t_next, a, seed, step, row0=0):
     n = z.shape[0]
     T = (H // p) * (W // p)
     out = np.empty_like(z, dtype=np.float64)
     for b in range(n):
         v = odit.unpatchify(v_tok[b * T:(b + 1) * T].astype(np.float64), C, H, W, p)
-        eps = osde.latent_normals((C, H, W), b, step, seed)
+        eps = osde.latent_normals((C, H, W), row0 + b, step, seed)
         out[b] = osde.sde_update(z[b], v, t_cur, t_next, a, eps)
     return out
 
 
-@pytest.mark.parametrize("n,C,H,W,p,t_cur,t_next,a", [
-    (2, 16, 8, 8, 2, 0.75, 0.5, 0.3),            # tiny latent
-    (3, 1, 9, 15, 3, 0.6, 0.5, 0.7),             # count 135 per candidate: ragged last counter
-    (1, 3, 2, 2, 1, 1.0, 0.98, 0.3),             # t = 1: sigma from 1 - t_next
-    (2, 16, 60, 104, 2, 0.02, 0.0, 0.3),         # 1.3B-shaped latent, last step (t_next = 0)
-    (16, 16, 60, 104, 2, 0.8, 0.78, 0.3),        # the 1.3B-shaped pool of 16
+@pytest.mark.parametrize("n,C,H,W,p,t_cur,t_next,a,row0", [
+    (2, 16, 8, 8, 2, 0.75, 0.5, 0.3, 0),            # tiny latent
+    (3, 1, 9, 15, 3, 0.6, 0.5, 0.7, 0),             # count 135 per candidate: ragged last counter
+    (1, 3, 2, 2, 1, 1.0, 0.98, 0.3, 0),             # t = 1: sigma from 1 - t_next
+    (2, 16, 60, 104, 2, 0.02, 0.0, 0.3, 0),         # 1.3B-shaped latent, last step (t_next = 0)
+    (16, 16, 60, 104, 2, 0.8, 0.78, 0.3, 0),        # the 1.3B-shaped pool of 16
+    (3, 16, 60, 104, 2, 0.5, 0.48, 0.3, 13),        # rows 13..15 of a pool, drawn on their own
 ])
-def test_unpatch_sde_matches_oracle(n, C, H, W, p, t_cur, t_next, a):
+def test_unpatch_sde_matches_oracle(n, C, H, W, p, t_cur, t_next, a, row0):
     fb = _fb()
     rng = np.random.default_rng(n * 1000 + C)
     T, P = (H // p) * (W // p), C * p * p
     v = rng.standard_normal((n * T, P)).astype(np.float32)
     z = rng.standard_normal((n, C, H, W)).astype(np.float32)
     zd = torch.from_numpy(z).cuda()
-    fb.flashbon_op_unpatch_sde(n, C, H, W, p, torch.from_numpy(v).cuda(), zd, t_cur, t_next, a, SEED, 11)
+    fb.flashbon_op_unpatch_sde(n, C, H, W, p, torch.from_numpy(v).cuda(), zd, t_cur, t_next, a, SEED, 11, row0)
     torch.cuda.synchronize()
     got = zd.cpu().numpy().astype(np.float64)
-    ref = _ref_unpatch_sde(v, z, C, H, W, p, float(np.float32(t_cur)), float(np.float32(t_next)), a, SEED, 11)
+    ref = _ref_unpatch_sde(v, z, C, H, W, p, float(np.float32(t_cur)), float(np.float32(t_next)), a, SEED, 11,
+                           row0)
     err = np.max(np.abs(got - ref) / (1.0 + np.abs(ref)))
     print(f"unpatch_sde n{n} C{C} {H}x{W} p{p}: {err:.2e}", flush=True)
     assert err <= 1e-5

@@ -50,4 +50,16 @@ def test_select_then_refine_matches_oracle(dtype, tol):
     err = rel_l2(out.cpu().numpy().astype(np.float64), ref)
     print(f"select+refine {dtype}: winner {j}, rel-L2 {err:.2e}", flush=True)
     assert err <= tol
+    # the stochastic variant keeps candidate j's own normals (counter row j) through refinement
+    a, seed = 0.3, 99
+    out_s = pool.refine(j, sde=(a, seed))
+    torch.cuda.synchronize()
+    kv = odit.prepare_text(W, wl.shape, text)
+    ref_s = z_draft[j:j + 1]
+    for k in range(wl.steps_draft, wl.steps_total):
+        ref_s = odit.refine_step(W, wl.shape, ref_s, sched[k], sched[k + 1], kv, wl.cond_index()[j:j + 1],
+                                 sde_args=(a, seed, k, j))
+    err_s = rel_l2(out_s.cpu().numpy().astype(np.float64), ref_s)
+    print(f"select+refine {dtype} stochastic: rel-L2 {err_s:.2e}", flush=True)
+    assert err_s <= tol
     pool.close()

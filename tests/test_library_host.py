@@ -123,7 +123,7 @@ def test_unpatch_sde_rejects_bad_noise_arguments_before_device_work(t_cur, t_nex
     """Host validation of the stochastic update (App. A.1, Eq. 20): no kernel is launched, so the
     (never dereferenced) placeholder pointers are safe without a device."""
     lib = fb.load()
-    st = lib.flashbon_op_unpatch_sde(1, 1, 8, 8, 2, 0x1000, 0x2000, t_cur, t_next, a, 1, 0, None)
+    st = lib.flashbon_op_unpatch_sde(1, 1, 8, 8, 2, 0x1000, 0x2000, t_cur, t_next, a, 1, 0, 0, None)
     assert st == fb.EINVAL
     assert b"t_cur" in lib.flashbon_last_error()
 
@@ -131,8 +131,14 @@ def test_unpatch_sde_rejects_bad_noise_arguments_before_device_work(t_cur, t_nex
 @pytest.mark.parametrize("args", [(0, 1, 8, 8, 2), (1, 1, 7, 8, 2), (1, 0, 8, 8, 2), (1, 1, 8, 8, 0)])
 def test_unpatch_sde_rejects_bad_shapes(args):
     lib = fb.load()
-    st = lib.flashbon_op_unpatch_sde(*args, 0x1000, 0x2000, 0.5, 0.4, 0.3, 1, 0, None)
+    st = lib.flashbon_op_unpatch_sde(*args, 0x1000, 0x2000, 0.5, 0.4, 0.3, 1, 0, 0, None)
     assert st == fb.ESHAPE
+
+
+def test_unpatch_sde_rejects_negative_counters():
+    lib = fb.load()
+    assert lib.flashbon_op_unpatch_sde(1, 1, 8, 8, 2, 0x1000, 0x2000, 0.5, 0.4, 0.3, 1, -1, 0, None) == fb.EINVAL
+    assert lib.flashbon_op_unpatch_sde(1, 1, 8, 8, 2, 0x1000, 0x2000, 0.5, 0.4, 0.3, 1, 0, -3, None) == fb.EINVAL
 
 
 def test_normals_rejects_bad_arguments():
