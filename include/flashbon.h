@@ -146,6 +146,11 @@ typedef struct {
   uint64_t sde_seed; /* Philox key */
   int32_t sde_row0;  /* candidate index of row 0 in the counter (>= 0): a slice of a larger pool, or a
                         single refined candidate, draws the normals of its place in the pool */
+
+  float *preview; /* optional device fp32 [n, C, H, W] output, NULL = off: the clean-latent estimate
+                     z - t_cur v of this step's state (rectified flow x_t = (1 - t) x_0 + t x_1, so
+                     x_0 = x_t - t v), i.e. one Euler jump of the step's output to t = 0 -- the
+                     draft preview a verifier scores (Sec. 4.2 Stage 1).  Must not alias latents. */
 } flashbon_step_args;
 
 /* Number of floats `host_weights` must hold for `cfg`. Returns 0 if cfg is invalid. */

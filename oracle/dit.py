@@ -245,6 +245,13 @@ def _noise(sde_args, n: int):
     return a, seed, step, row0 + n
 
 
+def clean_estimate(z: np.ndarray, v: np.ndarray, t: float) -> np.ndarray:
+    """Preview of the clean latent from state z at time t with velocity v: x_t = (1 - t) x_0 + t x_1
+    and v = x_1 - x_0 give x_0 = x_t - t v (rectified flow, App. A.1); the draft a verifier scores
+    (Sec. 4.2 Stage 1) is this estimate at the truncation point."""
+    return np.asarray(z, f64) - f64(t) * np.asarray(v, f64)
+
+
 def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
                kv_per_cond: List[List[Tuple[np.ndarray, np.ndarray]]], cond_index: np.ndarray,
                skip: np.ndarray, proxy: np.ndarray, cache: PoolCache,

@@ -60,8 +60,10 @@ __device__ __forceinline__ void epilogue4(const EpiArgs &e, int m, int n, float 
     for (int q = 0; q < 4; ++q) {
       int nn = n + q;
       int c = nn / pp, r = nn % pp, di = r / e.p, dj = r % e.p;
-      float *zp = e.z + (((int64_t)b * e.C + c) * e.H + (e.p * i + di)) * e.W + (e.p * j + dj);
-      *zp = *zp + e.dt * v[q];
+      const int64_t zi = (((int64_t)b * e.C + c) * e.H + (e.p * i + di)) * e.W + (e.p * j + dj);
+      const float z0 = e.z[zi];
+      if (e.preview) e.preview[zi] = z0 - e.t_cur * v[q];   // clean-latent estimate z - t v
+      e.z[zi] = z0 + e.dt * v[q];
     }
   }
 }

@@ -26,6 +26,8 @@ struct EpiArgs {
   // EULER: z [n][C][H][W] fp32, tokens per candidate T = (H/p)(W/p), N = C p p
   float *z = nullptr;
   float dt = 0.f;
+  float *preview = nullptr;    // EULER: optional [n][C][H][W] fp32 output z - t_cur v (before the update)
+  float t_cur = 0.f;
   int C = 0, H = 0, W = 0, p = 0, T = 0;
 };
 
@@ -76,9 +78,10 @@ struct SdeArgs {
 // sigma_t is not finite.  Row b of a launch draws counter row row0 + b.
 bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, int32_t row0,
                       SdeArgs *out);
-// z [n][C][H][W] fp32 updated in place from v = head output [n T][C p p] fp32 (unpatchified here)
+// z [n][C][H][W] fp32 updated in place from v = head output [n T][C p p] fp32 (unpatchified here);
+// preview (optional, same layout) receives z - t_cur v before the update
 hipError_t launch_unpatch_sde(int n, int C, int H, int W, int p, const float *v, float *z,
-                              const SdeArgs &a, hipStream_t s);
+                              const SdeArgs &a, float *preview, float t_cur, hipStream_t s);
 // the words (uint32 [ceil(count/4)][4], or null) and normals (fp32 [count], or null) of one candidate
 hipError_t launch_normals(int64_t count, uint32_t cand, uint32_t step, uint64_t seed, uint32_t *words,
                           float *normals, hipStream_t s);

@@ -259,6 +259,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   const int T = (int)T64;
   const int64_t M = (int64_t)a->n * T;
   if (!a->latents) return fail(FLASHBON_EINVAL, "latents is NULL");
+  if (a->preview && a->preview == a->latents) return fail(FLASHBON_EINVAL, "preview must not alias latents");
   if (!std::isfinite(a->t_cur) || !std::isfinite(a->t_next)) return fail(FLASHBON_EINVAL, "t_cur/t_next must be finite");
   if (!a->text || !a->cond_index || !a->text_kv || !a->text_kv_valid)
     return fail(FLASHBON_EINVAL, "text, cond_index, text_kv and text_kv_valid are required");
@@ -441,10 +442,11 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     EpiArgs e;
     e.out = m->vtok; e.ldo = P; e.bias = Bp(m->lay.head_b);
     HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head");
-    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_unpatch_sde(a->n, m->C, a->latent_h, a->latent_w, p, m->vtok, a->latents, sde, s); }), "unpatchify + stochastic update");
+    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_unpatch_sde(a->n, m->C, a->latent_h, a->latent_w, p, m->vtok, a->latents, sde, a->preview, a->t_cur, s); }), "unpatchify + stochastic update");
   } else {
     EpiArgs e;
     e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;
+    e.preview = a->preview; e.t_cur = a->t_cur;
     e.C = m->C; e.H = a->latent_h; e.W = a->latent_w; e.p = p; e.T = T;
     HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_EULER, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head + Euler");
   }

@@ -51,7 +51,7 @@ __device__ __forceinline__ void normals4(uint32_t quad, uint32_t cand, uint32_t 
 // grid (ceil(quads / 256), n); v: head output [n T][C p p] fp32 (bias included); z: [n][C][H][W].
 __global__ __launch_bounds__(256) void k_unpatch_sde(int C, int H, int W, int p,
                                                      const float *__restrict__ v, float *__restrict__ z,
-                                                     SdeArgs s) {
+                                                     SdeArgs s, float *__restrict__ preview, float t_cur) {
   const int64_t chw = (int64_t)C * H * W, quads = (chw + 3) >> 2;
   const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int b = blockIdx.y;
@@ -72,6 +72,7 @@ __global__ __launch_bounds__(256) void k_unpatch_sde(int C, int H, int W, int p,
     const int ti = y / p, di = y - ti * p, tj = x / p, dj = x - tj * p;
     const float vv = vb[(int64_t)(ti * wp + tj) * P + c * pp + di * p + dj];
     const float zz = zb[e];
+    if (preview) preview[(int64_t)b * chw + e] = zz - t_cur * vv;
     const float drift = fmaf(s.k, fmaf(s.omt, vv, zz), vv);
     zb[e] = fmaf(s.g, eps[i], fmaf(s.dt, drift, zz));
   }
@@ -115,10 +116,10 @@ bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t
 }
 
 hipError_t launch_unpatch_sde(int n, int C, int H, int W, int p, const float *v, float *z,
-                              const SdeArgs &a, hipStream_t s) {
+                              const SdeArgs &a, float *preview, float t_cur, hipStream_t s) {
   const int64_t quads = ((int64_t)C * H * W + 3) / 4;
   hipLaunchKernelGGL(k_unpatch_sde, dim3((unsigned)((quads + 255) / 256), (unsigned)n), dim3(256), 0, s,
-                     C, H, W, p, v, z, a);
+                     C, H, W, p, v, z, a, preview, t_cur);
   return hipGetLastError();
 }
 

@@ -59,7 +59,7 @@ class StepArgs(ctypes.Structure):
         ("trace", ctypes.POINTER(TraceEntry)), ("hidden_dump", ctypes.c_void_p),
         ("stream", ctypes.c_void_p),
         ("sde_a", ctypes.c_float), ("sde_step", ctypes.c_int32), ("sde_seed", ctypes.c_uint64),
-        ("sde_row0", ctypes.c_int32),
+        ("sde_row0", ctypes.c_int32), ("preview", ctypes.c_void_p),
     ]
 
 
@@ -202,7 +202,7 @@ def trace_list(trace) -> list:
 
 def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
           skip=None, proxy=None, cache=None, meta=None, trace=None, hidden_dump=None, stream=None,
-          num_blocks=None, sde=None):
+          num_blocks=None, sde=None, preview=None):
     n, C, H, W = (int(x) for x in latents.shape)
     n_cond, text_len = int(text.shape[0]), int(text.shape[1])
     cond = np.ascontiguousarray(np.asarray(cond_index, dtype=np.int32))
@@ -225,6 +225,7 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
     a.meta = meta
     a.trace = trace
     a.hidden_dump = _ptr(hidden_dump)
+    a.preview = _ptr(preview)
     a.stream = _stream(stream)
     if sde is not None:
         a.sde_a, a.sde_seed, a.sde_step = float(sde[0]), int(sde[1]), int(sde[2])
@@ -233,18 +234,21 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
 
 
 def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
-                        skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None, sde=None):
+                        skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None, sde=None,
+                        preview=None):
     """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays;
-    ``sde = (a, seed, step[, row0])`` selects the stochastic update (None or a = 0: Euler)."""
+    ``sde = (a, seed, step[, row0])`` selects the stochastic update (None or a = 0: Euler);
+    ``preview`` (device [n, C, H, W] fp32) receives z - t_cur v."""
     _step(load().flashbon_draft_step, "flashbon_draft_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, skip, proxy, cache, meta, trace, hidden_dump, stream,
-          num_blocks=len(meta), sde=sde)
+          num_blocks=len(meta), sde=sde, preview=preview)
 
 
 def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
-                         trace=None, hidden_dump=None, stream=None, sde=None):
+                         trace=None, hidden_dump=None, stream=None, sde=None, preview=None):
     _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
-          cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde)
+          cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde,
+          preview=preview)
 
 
 def flashbon_select(scores, judge, rho1=0.5, rho2=0.5, kappa=1.5):

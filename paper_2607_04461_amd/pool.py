@@ -53,8 +53,10 @@ class DraftPool:
         self.latents.copy_(self.torch.from_numpy(np.ascontiguousarray(z0, np.float32)))
         ctypes.memset(self.meta, 0, ctypes.sizeof(self.meta))
 
-    def draft_step(self, k: int, skip=None, proxy=None, hidden_dump=None, stream=None, sde=None) -> list:
-        """Step k of the schedule; ``sde = (a, seed)`` takes the stochastic update with counter k."""
+    def draft_step(self, k: int, skip=None, proxy=None, hidden_dump=None, stream=None, sde=None,
+                   preview=None) -> list:
+        """Step k of the schedule; ``sde = (a, seed)`` takes the stochastic update with counter k;
+        ``preview`` (device [n, C, H, W] fp32) receives the clean-latent estimate z - t v."""
         if skip is None or proxy is None:
             s, p = self.wl.masks(k)
             skip = s if skip is None else skip
@@ -62,7 +64,7 @@ class DraftPool:
         fb.flashbon_draft_step(self.model, self.latents, self.schedule[k], self.schedule[k + 1], self.text,
                                self.cond_index, self.text_kv, self.text_kv_valid, skip, proxy, self.cache,
                                self.meta, self.trace, hidden_dump, stream,
-                               None if sde is None else (sde[0], sde[1], k))
+                               None if sde is None else (sde[0], sde[1], k), preview)
         return fb.trace_list(self.trace)
 
     def refine_step(self, k: int, latents=None, cond_index=None, hidden_dump=None, stream=None,

@@ -122,3 +122,14 @@ def test_step_level_sde_option():
         drift = v[n] + sg * sg / 1.5 * (z[n] + 0.25 * v[n])
         np.testing.assert_allclose(noisy[n], z[n] + drift * (-0.25) + sg * 0.5 * eps, rtol=1e-12, atol=1e-12)
     assert not np.allclose(noisy[0] - base[0], noisy[1] - base[1])
+
+
+def test_clean_estimate_recovers_a_point_mass():
+    """For data concentrated at x0 the exact rectified-flow velocity at x_t = (1 - t) x0 + t x1 is
+    x1 - x0 = (x_t - x0) / t, and the preview z - t v returns x0 exactly."""
+    from oracle import dit as od_dit
+    rng = np.random.default_rng(9)
+    x0, x1 = rng.standard_normal((2, 4, 6, 6))
+    for t in (1.0, 0.73, 0.2):
+        xt = (1 - t) * x0 + t * x1
+        np.testing.assert_allclose(od_dit.clean_estimate(xt, (xt - x0) / t, t), x0, atol=1e-12)
