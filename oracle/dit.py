@@ -195,16 +195,12 @@ class PoolCache:
         self.data: Dict[Tuple[int, int, int], np.ndarray] = {}   # (candidate, block, slot) -> h
 
 
-def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
-                   kv: List[Tuple[np.ndarray, np.ndarray]], block_mod: np.ndarray,
-                   head_mod: np.ndarray, trace, meta_before: List[Dict], cache: Optional[PoolCache],
-                   cand: int, hidden: Optional[List[np.ndarray]] = None,
-                   noise: Optional[Tuple[float, int, int]] = None) -> np.ndarray:
-    """One denoising step of one candidate under an already-planned trace; returns z_next [C, H, W].
-
-    ``noise = (a, seed, step, row)`` replaces the Euler update by the stochastic one of App. A.1
-    (Eq. 20) with the normals of counter row ``row`` at counter ``step`` (oracle/sde.py).
-    """
+def candidate_velocity(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float,
+                       kv: List[Tuple[np.ndarray, np.ndarray]], block_mod: np.ndarray,
+                       head_mod: np.ndarray, trace, meta_before: List[Dict], cache: Optional[PoolCache],
+                       row: int, hidden: Optional[List[np.ndarray]] = None) -> np.ndarray:
+    """The network's velocity v [C, H, W] for one candidate under an already-planned trace; computed
+    block outputs are cached under key ``row``."""
     C, H, Wd = z.shape
     p = shape.patch
     tok = patchify(np.asarray(z, f64), p)
@@ -217,23 +213,49 @@ def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float,
         elif action == PROXY:                                 # Eq. 3-5
             m = meta_before[l]
             slots = recent_slots(m)
-            entries = [(cache.data[(cand, l, s)], m["t"][s]) for s in slots]
+            entries = [(cache.data[(row, l, s)], m["t"][s]) for s in slots]
             h = taylor_proxy(entries, t_cur, order)
         else:                                                 # Eq. 7
             h = block_forward(W, l, h, block_mod[l], kv[l], shape.heads, shape.ln_eps)
             if cache is not None:
-                cache.data[(cand, l, slot)] = h.copy()
+                cache.data[(row, l, slot)] = h.copy()
         if hidden is not None:
             hidden.append(h.copy())
     sh, sc = head_mod
     a = layer_norm(h, shape.ln_eps) * (1.0 + sc) + sh
     out = linear(a, W["head_w"], W["head_b"])
-    v = unpatchify(out, C, H, Wd, p)
+    return unpatchify(out, C, H, Wd, p)
+
+
+def update(z: np.ndarray, v: np.ndarray, t_cur: float, t_next: float,
+           noise: Optional[Tuple[float, int, int, int]] = None) -> np.ndarray:
+    """Euler update z + (t_next - t_cur) v (Eq. 20 with a = 0), or with ``noise = (a, seed, step, row)``
+    the stochastic update of App. A.1 (Eq. 20) with the normals of counter row ``row``."""
     if noise is not None:
         a, seed, step, row = noise
         eps = sde.latent_normals(z.shape, row, step, seed)
         return sde.sde_update(z, v, t_cur, t_next, a, eps)
     return np.asarray(z, f64) + (f64(t_next) - f64(t_cur)) * v
+
+
+def guided(v_cond: np.ndarray, v_uncond: np.ndarray, scale: float) -> np.ndarray:
+    """Classifier-free guidance: v = v_u + s (v_c - v_u)."""
+    return np.asarray(v_uncond, f64) + f64(scale) * (np.asarray(v_cond, f64) - np.asarray(v_uncond, f64))
+
+
+def candidate_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
+                   kv: List[Tuple[np.ndarray, np.ndarray]], block_mod: np.ndarray,
+                   head_mod: np.ndarray, trace, meta_before: List[Dict], cache: Optional[PoolCache],
+                   cand: int, hidden: Optional[List[np.ndarray]] = None,
+                   noise: Optional[Tuple[float, int, int, int]] = None) -> np.ndarray:
+    """One denoising step of one candidate under an already-planned trace; returns z_next [C, H, W].
+
+    ``noise = (a, seed, step, row)`` replaces the Euler update by the stochastic one of App. A.1
+    (Eq. 20) with the normals of counter row ``row`` at counter ``step`` (oracle/sde.py).
+    """
+    v = candidate_velocity(W, shape, z, t_cur, kv, block_mod, head_mod, trace, meta_before, cache, cand,
+                           hidden)
+    return update(z, v, t_cur, t_next, noise)
 
 
 def _noise(sde_args, n: int):
@@ -257,31 +279,41 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
                skip: np.ndarray, proxy: np.ndarray, cache: PoolCache,
                candidates: Optional[Sequence[int]] = None,
                hidden: Optional[Dict[int, List[np.ndarray]]] = None,
-               sde_args: Optional[Tuple[float, int, int]] = None):
+               sde_args: Optional[Tuple[float, int, int]] = None,
+               cfg: Optional[Tuple[float, np.ndarray]] = None):
     """One draft step over the pool (Eq. 2 with the knobs of Sec. 4.1).
 
     z [N, C, H, W]; returns (z_next [N, C, H, W] fp64 -- rows not in ``candidates`` are left as z --,
     trace).  The cache metadata advances once per step, as all candidates share the masks.
     ``sde_args = (a, seed, step[, row0])`` selects the stochastic update (Eq. 20), candidate n
     drawing the normals of counter row row0 + n (row0 = 0 by default) at ``step``.
+    ``cfg = (scale, uncond_index)``: classifier-free guidance; candidate n also runs with prompt
+    uncond_index[n] (cache key N + n) and steps with v_u + scale (v_c - v_u).
     """
     trace, new_meta = plan_step(skip, proxy, cache.meta, t_cur)
     block_mod, head_mod = modulations(W, shape.num_blocks, shape.freq_dim, t_cur)
     out = np.asarray(z, f64).copy()
-    for n in (range(z.shape[0]) if candidates is None else candidates):
+    N = z.shape[0]
+    for n in (range(N) if candidates is None else candidates):
         hid = None if hidden is None else hidden.setdefault(n, [])
-        out[n] = candidate_step(W, shape, z[n], t_cur, t_next, kv_per_cond[int(cond_index[n])],
-                                block_mod, head_mod, trace, cache.meta, cache, n, hid, _noise(sde_args, n))
+        v = candidate_velocity(W, shape, z[n], t_cur, kv_per_cond[int(cond_index[n])], block_mod, head_mod,
+                               trace, cache.meta, cache, n, hid)
+        if cfg is not None:
+            v_u = candidate_velocity(W, shape, z[n], t_cur, kv_per_cond[int(cfg[1][n])], block_mod, head_mod,
+                                     trace, cache.meta, cache, N + n)
+            v = guided(v, v_u, cfg[0])
+        out[n] = update(z[n], v, t_cur, t_next, _noise(sde_args, n))
     cache.meta = new_meta
     return out, trace
 
 
 def refine_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_next: float,
                 kv_per_cond, cond_index: np.ndarray, candidates: Optional[Sequence[int]] = None,
-                sde_args: Optional[Tuple[float, int, int]] = None):
+                sde_args: Optional[Tuple[float, int, int]] = None,
+                cfg: Optional[Tuple[float, np.ndarray]] = None):
     """Full-quality step (phi_full of Eq. 13): no skipping, no proxies, no cache.
 
-    ``sde_args`` as in ``draft_step``."""
+    ``sde_args`` and ``cfg`` as in ``draft_step``."""
     L = shape.num_blocks
     zeros = np.zeros(L, np.uint8)
     trace, _ = plan_step(zeros, zeros, [{"count": 0, "head": 0, "t": [0.0] * 3} for _ in range(L)],
@@ -289,8 +321,13 @@ def refine_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_
     block_mod, head_mod = modulations(W, L, shape.freq_dim, t_cur)
     out = np.asarray(z, f64).copy()
     for n in (range(z.shape[0]) if candidates is None else candidates):
-        out[n] = candidate_step(W, shape, z[n], t_cur, t_next, kv_per_cond[int(cond_index[n])],
-                                block_mod, head_mod, trace, None, None, n, None, _noise(sde_args, n))
+        v = candidate_velocity(W, shape, z[n], t_cur, kv_per_cond[int(cond_index[n])], block_mod, head_mod,
+                               trace, None, None, n)
+        if cfg is not None:
+            v_u = candidate_velocity(W, shape, z[n], t_cur, kv_per_cond[int(cfg[1][n])], block_mod, head_mod,
+                                     trace, None, None, n)
+            v = guided(v, v_u, cfg[0])
+        out[n] = update(z[n], v, t_cur, t_next, _noise(sde_args, n))
     return out
 
 

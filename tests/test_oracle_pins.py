@@ -411,3 +411,25 @@ def test_dispatch_fallback_and_liveness():
     tr, _ = od.plan_step(zeros, np.array([1, 0, 1, 1], np.uint8), meta2, 0.8)
     assert [e[3] for e in tr] == [1, 1, 0, 1]
     assert tr[2] == (od.PROXY, 1, 1, 0)          # block 2 was computed at 1.0 and 0.9
+
+
+def test_guidance_end_points_and_linearity():
+    """Classifier-free guidance v_u + s (v_c - v_u): s = 1 gives the conditional step and s = 0 the
+    unconditional one (to rounding); the step is affine in s, so the step at s = 2 is the reflection
+    of s = 0 through s = 1."""
+    wl, W, z, text = _tiny_setup()
+    text2 = np.concatenate([text, synth.make_text(1, wl.text_len, wl.shape.text_dim, first_seed=777)])
+    kv = od_dit.prepare_text(W, wl.shape, text2)
+    L = wl.shape.num_blocks
+    zeros = np.zeros(L, np.uint8)
+    cond = wl.cond_index()
+    unc = np.full(wl.n, 1, np.int32)
+
+    def step(cfg, c=cond):
+        return od_dit.draft_step(W, wl.shape, z, 0.75, 0.5, kv, c, zeros, zeros, od_dit.PoolCache(L), cfg=cfg)[0]
+
+    plain_c, plain_u = step(None), step(None, unc)
+    np.testing.assert_allclose(step((1.0, unc)), plain_c, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(step((0.0, unc)), plain_u, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(step((2.0, unc)) - plain_c, plain_c - plain_u, rtol=0, atol=1e-12)
+    assert not np.allclose(plain_c, plain_u)
