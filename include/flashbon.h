@@ -151,6 +151,15 @@ typedef struct {
                      z - t_cur v of this step's state (rectified flow x_t = (1 - t) x_0 + t x_1, so
                      x_0 = x_t - t v), i.e. one Euler jump of the step's output to t = 0 -- the
                      draft preview a verifier scores (Sec. 4.2 Stage 1).  Must not alias latents. */
+
+  /* Classifier-free guidance, off when cfg == 0.  On, the step runs 2n token rows through the
+   * network: rows [0, n) with prompts cond_index, rows [n, 2n) -- the unconditional twins of the same
+   * n latents -- with prompts uncond_index (host [n], values in [0, n_cond), typically a null
+   * prompt), and steps candidate b with v = v_u + cfg_scale (v_c - v_u).  2n <= max_n; cache and
+   * hidden_dump then hold 2n rows (flashbon_cache_bytes(model, 2n, T)). */
+  int32_t cfg;
+  float cfg_scale;
+  const int32_t *uncond_index;
 } flashbon_step_args;
 
 /* Number of floats `host_weights` must hold for `cfg`. Returns 0 if cfg is invalid. */

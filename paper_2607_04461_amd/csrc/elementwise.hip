@@ -150,7 +150,7 @@ hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const f
 
 // -------------------------------------------------------------------------------------- patchify
 template <typename T>
-__global__ __launch_bounds__(256) void k_patchify(int n, int C, int H, int W, int p,
+__global__ __launch_bounds__(256) void k_patchify(int n, int zrows, int C, int H, int W, int p,
                                                   const float *__restrict__ z, T *__restrict__ tok) {
   const int P = C * p * p, wp = W / p, T_ = (H / p) * wp;
   const int64_t total = (int64_t)n * T_ * P;
@@ -158,23 +158,23 @@ __global__ __launch_bounds__(256) void k_patchify(int n, int C, int H, int W, in
        idx += (int64_t)gridDim.x * blockDim.x) {
     int f = (int)(idx % P);
     int64_t m = idx / P;
-    int t = (int)(m % T_), b = (int)(m / T_);
+    int t = (int)(m % T_), b = (int)(m / T_) % zrows;
     int i = t / wp, j = t % wp;
     int c = f / (p * p), r = f % (p * p), di = r / p, dj = r % p;
     tok[idx] = from_f32<T>(z[(((int64_t)b * C + c) * H + (p * i + di)) * W + (p * j + dj)]);
   }
 }
 
-hipError_t launch_patchify(ActType t, int n, int C, int H, int W, int p, const float *z, void *tok,
+hipError_t launch_patchify(ActType t, int n, int zrows, int C, int H, int W, int p, const float *z, void *tok,
                            hipStream_t s) {
   int64_t total = (int64_t)n * C * H * W;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (t == ACT_BF16)
-    hipLaunchKernelGGL(k_patchify<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, n, C, H, W, p, z,
+    hipLaunchKernelGGL(k_patchify<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, n, zrows, C, H, W, p, z,
                        (bf16 *)tok);
   else
-    hipLaunchKernelGGL(k_patchify<float>, dim3((unsigned)blocks), dim3(256), 0, s, n, C, H, W, p, z,
+    hipLaunchKernelGGL(k_patchify<float>, dim3((unsigned)blocks), dim3(256), 0, s, n, zrows, C, H, W, p, z,
                        (float *)tok);
   return hipGetLastError();
 }

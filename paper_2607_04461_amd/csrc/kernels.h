@@ -51,8 +51,8 @@ hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, con
 hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const float *h3, int order,
                         float ca, float cb, float *out, hipStream_t s);
 
-// tokens [n*T][C p p] (act) from z [n][C][H][W] fp32
-hipError_t launch_patchify(ActType t, int n, int C, int H, int W, int p, const float *z, void *tok,
+// tokens [n*T][C p p] (act) from z [zrows][C][H][W] fp32; token row block b reads latent b % zrows
+hipError_t launch_patchify(ActType t, int n, int zrows, int C, int H, int W, int p, const float *z, void *tok,
                            hipStream_t s);
 
 // sinusoidal features of 1000 t, computed in double: f[j] = cos, f[half + j] = sin
@@ -78,10 +78,12 @@ struct SdeArgs {
 // sigma_t is not finite.  Row b of a launch draws counter row row0 + b.
 bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t step, int32_t row0,
                       SdeArgs *out);
-// z [n][C][H][W] fp32 updated in place from v = head output [n T][C p p] fp32 (unpatchified here);
-// preview (optional, same layout) receives z - t_cur v before the update
-hipError_t launch_unpatch_sde(int n, int C, int H, int W, int p, const float *v, float *z,
-                              const SdeArgs &a, float *preview, float t_cur, hipStream_t s);
+// z [n][C][H][W] fp32 updated in place from v = head output [n T][C p p] fp32 (unpatchified here).
+// guided: v holds 2n token rows, the unconditional twins after the n conditional ones, and the
+// velocity is v_u + scale (v_c - v_u).  a.g == 0 skips the normals (the Euler update when a.k == 0).
+// preview (optional, same layout as z) receives z - t_cur v before the update.
+hipError_t launch_head_update(int n, int C, int H, int W, int p, const float *v, bool guided, float scale,
+                              float *z, const SdeArgs &a, float *preview, float t_cur, hipStream_t s);
 // the words (uint32 [ceil(count/4)][4], or null) and normals (fp32 [count], or null) of one candidate
 hipError_t launch_normals(int64_t count, uint32_t cand, uint32_t step, uint64_t seed, uint32_t *words,
                           float *normals, hipStream_t s);

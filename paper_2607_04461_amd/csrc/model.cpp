@@ -251,13 +251,17 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   const flashbon_model_config &c = m->c;
   const int L = m->L, D = m->D, F = m->F, P = m->P, p = m->p;
   // ---------------------------------------------------------------- validation (no side effects)
-  if (a->n < 1 || a->n > c.max_n) return fail(FLASHBON_ESHAPE, "n outside [1, max_n]");
+  const bool guided = a->cfg != 0;
+  const int R = guided ? 2 * a->n : a->n;   // token rows through the network (twins when guided)
+  if (a->n < 1 || R > c.max_n) return fail(FLASHBON_ESHAPE, guided ? "2n outside [2, max_n]" : "n outside [1, max_n]");
+  if (guided && (!a->uncond_index || !std::isfinite(a->cfg_scale)))
+    return fail(FLASHBON_EINVAL, "guidance needs uncond_index and a finite cfg_scale");
   if (a->latent_h < p || a->latent_w < p || a->latent_h % p || a->latent_w % p)
     return fail(FLASHBON_ESHAPE, "latent_h/latent_w must be positive multiples of patch");
   const int64_t T64 = (int64_t)(a->latent_h / p) * (a->latent_w / p);
   if (T64 > c.max_tokens) return fail(FLASHBON_ESHAPE, "tokens exceed max_tokens");
   const int T = (int)T64;
-  const int64_t M = (int64_t)a->n * T;
+  const int64_t M = (int64_t)R * T;
   if (!a->latents) return fail(FLASHBON_EINVAL, "latents is NULL");
   if (a->preview && a->preview == a->latents) return fail(FLASHBON_EINVAL, "preview must not alias latents");
   if (!std::isfinite(a->t_cur) || !std::isfinite(a->t_next)) return fail(FLASHBON_EINVAL, "t_cur/t_next must be finite");
@@ -268,6 +272,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   for (int i = 0; i < a->n; ++i)
     if (a->cond_index[i] < 0 || a->cond_index[i] >= a->n_cond)
       return fail(FLASHBON_EINVAL, "cond_index[" + std::to_string(i) + "] outside [0, n_cond)");
+  if (guided)
+    for (int i = 0; i < a->n; ++i)
+      if (a->uncond_index[i] < 0 || a->uncond_index[i] >= a->n_cond)
+        return fail(FLASHBON_EINVAL, "uncond_index[" + std::to_string(i) + "] outside [0, n_cond)");
   if (draft) {
     if (!a->meta) return fail(FLASHBON_EINVAL, "draft step needs meta");
     if (!a->cache) return fail(FLASHBON_EINVAL, "draft step needs cache");
@@ -313,9 +321,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
 
   // cond_index -> device, only when it changed (the previous step may still read the old copy)
   std::vector<int32_t> cond(a->cond_index, a->cond_index + a->n);
+  if (guided) cond.insert(cond.end(), a->uncond_index, a->uncond_index + a->n);
   if (cond != m->last_cond) {
     HIPCHK(hipStreamSynchronize(s), "synchronise before cond_index upload");
-    HIPCHK(hipMemcpy(m->d_cond, cond.data(), sizeof(int32_t) * a->n, hipMemcpyHostToDevice), "cond_index upload");
+    HIPCHK(hipMemcpy(m->d_cond, cond.data(), sizeof(int32_t) * cond.size(), hipMemcpyHostToDevice), "cond_index upload");
     m->last_cond = cond;
   }
 
@@ -359,7 +368,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   for (int l = 0; l < L; ++l)
     if (trace[l].action != FLASHBON_SKIP) { embed_live = trace[l].action == FLASHBON_COMPUTE; break; }
   if (embed_live) {
-    HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s); }), "patchify");
+    HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, R, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s); }), "patchify");
     EpiArgs e;
     e.out = m->h; e.ldo = D; e.bias = Bp(m->lay.pe_b);
     HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, D, P, m->tok, Wp(m->lay.pe_w), e, s); }), "patch embed");
@@ -393,10 +402,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     {
       AttnArgs at;
-      at.batch = a->n; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = T;
+      at.batch = R; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = T;
       at.q = m->qkv; at.q_bs = (int64_t)T * 3 * D; at.q_rs = 3 * D;
       at.k = (const char *)m->qkv + (size_t)D * asz; at.v = (const char *)m->qkv + (size_t)2 * D * asz;
-      at.kv_bs = (int64_t)T * 3 * D; at.kv_rs = 3 * D; at.kv_index = nullptr; at.n_kv = a->n;
+      at.kv_bs = (int64_t)T * 3 * D; at.kv_rs = 3 * D; at.kv_index = nullptr; at.n_kv = R;
       at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
       HIPCHK(timed(m, FLASHBON_SITE_ATTN_SELF, s, [&] { return launch_attention(act, at, s); }), "self-attention");
     }
@@ -412,7 +421,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     {
       const char *kv = (const char *)a->text_kv + (size_t)l * kv_block * asz;
       AttnArgs at;
-      at.batch = a->n; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = Lt;
+      at.batch = R; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = Lt;
       at.q = m->qkv; at.q_bs = (int64_t)T * D; at.q_rs = D;
       at.k = kv; at.v = kv + (size_t)D * asz; at.kv_bs = (int64_t)Lt * 2 * D; at.kv_rs = 2 * D;
       at.kv_index = m->d_cond; at.n_kv = NC;
@@ -438,11 +447,16 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
 
   // head + unpatchify + Euler update of the latents (or the stochastic update of Eq. 20)
   HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, m->hmod, m->hmod + D, m->a, s); }), "head adaLN");
-  if (stochastic) {
+  if (stochastic || guided) {
+    if (!stochastic) {                      // Euler update through the same kernel: no drift term, no noise
+      sde = SdeArgs{};
+      sde.dt = a->t_next - a->t_cur;
+    }
     EpiArgs e;
     e.out = m->vtok; e.ldo = P; e.bias = Bp(m->lay.head_b);
     HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head");
-    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_unpatch_sde(a->n, m->C, a->latent_h, a->latent_w, p, m->vtok, a->latents, sde, a->preview, a->t_cur, s); }), "unpatchify + stochastic update");
+    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_head_update(a->n, m->C, a->latent_h, a->latent_w, p, m->vtok, guided, a->cfg_scale, a->latents, sde, a->preview, a->t_cur, s); }),
+           "unpatchify + guidance + update");
   } else {
     EpiArgs e;
     e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;

@@ -104,7 +104,8 @@ flashbon_status flashbon_op_unpatch_sde(int32_t n, int32_t C, int32_t H, int32_t
   SdeArgs s;
   if (!sde_coefficients(t_cur, t_next, a, seed, step, row0, &s))
     return fail(FLASHBON_EINVAL, "need a >= 0, finite, and 0 < t_cur <= 1 (t_next < 1 when t_cur = 1)");
-  return launched(launch_unpatch_sde(n, C, H, W, p, v, z, s, nullptr, 0.f, (hipStream_t)stream), "unpatch_sde");
+  return launched(launch_head_update(n, C, H, W, p, v, false, 0.f, z, s, nullptr, 0.f, (hipStream_t)stream),
+                  "unpatch_sde");
 }
 
 }  // extern "C"

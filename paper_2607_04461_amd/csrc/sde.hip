@@ -1,4 +1,6 @@
-// Stochastic flow update of App. A.1 (Eq. 20), fused with unpatchify, and its counter-based normals.
+// Head update of the latents outside the head GEMM's epilogue: unpatchify, optional classifier-free
+// guidance, and the stochastic flow update of App. A.1 (Eq. 20) with its counter-based normals (or
+// the Euler update, a = 0).
 //
 //   z <- z + dt [v + k (z + (1 - t) v)] + g eps,   k = sigma_t^2 / (2 t),  g = sigma_t sqrt(|dt|),
 //   sigma_t = a sqrt(t / (1 - t))  (1 - t_next in the denominator when t = 1).
@@ -48,21 +50,25 @@ __device__ __forceinline__ void normals4(uint32_t quad, uint32_t cand, uint32_t 
   box_muller(w[2], w[3], z[2], z[3]);
 }
 
-// grid (ceil(quads / 256), n); v: head output [n T][C p p] fp32 (bias included); z: [n][C][H][W].
-__global__ __launch_bounds__(256) void k_unpatch_sde(int C, int H, int W, int p,
-                                                     const float *__restrict__ v, float *__restrict__ z,
-                                                     SdeArgs s, float *__restrict__ preview, float t_cur) {
+// grid (ceil(quads / 256), n); v: head output [(n or 2n) T][C p p] fp32 (bias included); z: [n][C][H][W].
+// Guided (vu != null): the unconditional twin of candidate b is token row block n + b, and the
+// velocity is v_u + scale (v_c - v_u).  s.g == 0 (no noise) skips the normals.
+__global__ __launch_bounds__(256) void k_head_update(int C, int H, int W, int p,
+                                                     const float *__restrict__ v, int guided, float scale,
+                                                     float *__restrict__ z, SdeArgs s,
+                                                     float *__restrict__ preview, float t_cur) {
   const int64_t chw = (int64_t)C * H * W, quads = (chw + 3) >> 2;
   const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int b = blockIdx.y;
+  const int b = blockIdx.y, n = gridDim.y;
   if (q >= quads) return;
   uint32_t w[4];
-  float eps[4];
-  normals4((uint32_t)q, s.row0 + (uint32_t)b, s.step, s.key0, s.key1, w, eps);
+  float eps[4] = {0.f, 0.f, 0.f, 0.f};
+  if (s.g != 0.f) normals4((uint32_t)q, s.row0 + (uint32_t)b, s.step, s.key0, s.key1, w, eps);
   const int hw = H * W, wp = W / p, pp = p * p;
   const int64_t T = (int64_t)(H / p) * wp, P = (int64_t)C * pp;
   float *zb = z + (int64_t)b * chw;
   const float *vb = v + (int64_t)b * T * P;
+  const float *vu = guided ? v + (int64_t)(n + b) * T * P : nullptr;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int64_t e = 4 * q + i;
@@ -70,11 +76,14 @@ __global__ __launch_bounds__(256) void k_unpatch_sde(int C, int H, int W, int p,
     const int c = (int)(e / hw), yx = (int)(e - (int64_t)c * hw);
     const int y = yx / W, x = yx - y * W;
     const int ti = y / p, di = y - ti * p, tj = x / p, dj = x - tj * p;
-    const float vv = vb[(int64_t)(ti * wp + tj) * P + c * pp + di * p + dj];
+    const int64_t vi = (int64_t)(ti * wp + tj) * P + c * pp + di * p + dj;
+    float vv = vb[vi];
+    if (vu) vv = fmaf(scale, vv - vu[vi], vu[vi]);
     const float zz = zb[e];
     if (preview) preview[(int64_t)b * chw + e] = zz - t_cur * vv;
     const float drift = fmaf(s.k, fmaf(s.omt, vv, zz), vv);
-    zb[e] = fmaf(s.g, eps[i], fmaf(s.dt, drift, zz));
+    const float zn = fmaf(s.dt, drift, zz);
+    zb[e] = s.g != 0.f ? fmaf(s.g, eps[i], zn) : zn;
   }
 }
 
@@ -115,11 +124,11 @@ bool sde_coefficients(float t_cur, float t_next, float a, uint64_t seed, int32_t
   return std::isfinite(out->k) && std::isfinite(out->g);
 }
 
-hipError_t launch_unpatch_sde(int n, int C, int H, int W, int p, const float *v, float *z,
-                              const SdeArgs &a, float *preview, float t_cur, hipStream_t s) {
+hipError_t launch_head_update(int n, int C, int H, int W, int p, const float *v, bool guided, float scale,
+                              float *z, const SdeArgs &a, float *preview, float t_cur, hipStream_t s) {
   const int64_t quads = ((int64_t)C * H * W + 3) / 4;
-  hipLaunchKernelGGL(k_unpatch_sde, dim3((unsigned)((quads + 255) / 256), (unsigned)n), dim3(256), 0, s,
-                     C, H, W, p, v, z, a, preview, t_cur);
+  hipLaunchKernelGGL(k_head_update, dim3((unsigned)((quads + 255) / 256), (unsigned)n), dim3(256), 0, s,
+                     C, H, W, p, v, guided ? 1 : 0, scale, z, a, preview, t_cur);
   return hipGetLastError();
 }
 

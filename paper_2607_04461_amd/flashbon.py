@@ -60,6 +60,7 @@ class StepArgs(ctypes.Structure):
         ("stream", ctypes.c_void_p),
         ("sde_a", ctypes.c_float), ("sde_step", ctypes.c_int32), ("sde_seed", ctypes.c_uint64),
         ("sde_row0", ctypes.c_int32), ("preview", ctypes.c_void_p),
+        ("cfg", ctypes.c_int32), ("cfg_scale", ctypes.c_float), ("uncond_index", ctypes.POINTER(ctypes.c_int32)),
     ]
 
 
@@ -202,7 +203,7 @@ def trace_list(trace) -> list:
 
 def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
           skip=None, proxy=None, cache=None, meta=None, trace=None, hidden_dump=None, stream=None,
-          num_blocks=None, sde=None, preview=None):
+          num_blocks=None, sde=None, preview=None, cfg=None):
     n, C, H, W = (int(x) for x in latents.shape)
     n_cond, text_len = int(text.shape[0]), int(text.shape[1])
     cond = np.ascontiguousarray(np.asarray(cond_index, dtype=np.int32))
@@ -226,6 +227,12 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
     a.trace = trace
     a.hidden_dump = _ptr(hidden_dump)
     a.preview = _ptr(preview)
+    if cfg is not None:
+        unc = np.ascontiguousarray(np.asarray(cfg[1], dtype=np.int32))
+        if unc.shape != (n,):
+            raise ValueError(f"uncond_index must have shape ({n},)")
+        a.cfg, a.cfg_scale = 1, float(cfg[0])
+        a.uncond_index = unc.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
     a.stream = _stream(stream)
     if sde is not None:
         a.sde_a, a.sde_seed, a.sde_step = float(sde[0]), int(sde[1]), int(sde[2])
@@ -235,20 +242,21 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
 
 def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
                         skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None, sde=None,
-                        preview=None):
+                        preview=None, cfg=None):
     """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays;
     ``sde = (a, seed, step[, row0])`` selects the stochastic update (None or a = 0: Euler);
-    ``preview`` (device [n, C, H, W] fp32) receives z - t_cur v."""
+    ``preview`` (device [n, C, H, W] fp32) receives z - t_cur v; ``cfg = (scale, uncond_index)``
+    turns on classifier-free guidance (the cache then holds 2n rows)."""
     _step(load().flashbon_draft_step, "flashbon_draft_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, skip, proxy, cache, meta, trace, hidden_dump, stream,
-          num_blocks=len(meta), sde=sde, preview=preview)
+          num_blocks=len(meta), sde=sde, preview=preview, cfg=cfg)
 
 
 def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
-                         trace=None, hidden_dump=None, stream=None, sde=None, preview=None):
+                         trace=None, hidden_dump=None, stream=None, sde=None, preview=None, cfg=None):
     _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde,
-          preview=preview)
+          preview=preview, cfg=cfg)
 
 
 def flashbon_select(scores, judge, rho1=0.5, rho2=0.5, kappa=1.5):

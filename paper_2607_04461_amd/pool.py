@@ -17,7 +17,10 @@ from . import synth
 
 class DraftPool:
     def __init__(self, wl: synth.Workload, dtype: Optional[str] = None, weights: Optional[np.ndarray] = None,
-                 device: str = "cuda", max_n: Optional[int] = None, max_cond: Optional[int] = None):
+                 device: str = "cuda", max_n: Optional[int] = None, max_cond: Optional[int] = None,
+                 guidance: Optional[float] = None):
+        """``guidance``: classifier-free guidance scale; every candidate then also runs with a null prompt
+        (an all-zero text appended as prompt n_cond) and the cache holds 2n rows."""
         import torch
         self.torch = torch
         self.wl = wl
@@ -26,19 +29,26 @@ class DraftPool:
         self.device = device
         if weights is None:
             weights, _ = synth.make_weights(wl.shape, wl.seed_w)
+        self.guidance = guidance
+        rows = 2 * wl.n if guidance is not None else wl.n
+        n_text = wl.n_cond + (1 if guidance is not None else 0)
         cfg = fb.make_config(wl.shape, fb.BF16 if self.dtype == "bf16" else fb.FP32,
-                             max_n or wl.n, wl.tokens, wl.text_len, max_cond or wl.n_cond)
+                             max(max_n or rows, rows), wl.tokens, wl.text_len, max(max_cond or n_text, n_text))
         self.cfg = cfg
         self.model = fb.flashbon_init_model(cfg, weights)
         L = wl.shape.num_blocks
         self.L = L
         self.latents = torch.empty((wl.n, wl.shape.latent_channels, wl.latent_h, wl.latent_w),
                                    dtype=torch.float32, device=device)
-        self.text = torch.from_numpy(synth.make_text(wl.n_cond, wl.text_len, wl.shape.text_dim)).to(device)
+        text = synth.make_text(wl.n_cond, wl.text_len, wl.shape.text_dim)
+        if guidance is not None:
+            text = np.concatenate([text, np.zeros((1,) + text.shape[1:], np.float32)])
+        self.text = torch.from_numpy(text).to(device)
         self.cond_index = wl.cond_index()
-        self.text_kv = torch.empty(fb.flashbon_text_kv_bytes(self.model, wl.n_cond, wl.text_len),
+        self.uncond_index = np.full(wl.n, wl.n_cond, np.int32)
+        self.text_kv = torch.empty(fb.flashbon_text_kv_bytes(self.model, text.shape[0], wl.text_len),
                                    dtype=torch.uint8, device=device)
-        self.cache = torch.empty(fb.flashbon_cache_bytes(self.model, wl.n, wl.tokens) // 4,
+        self.cache = torch.empty(fb.flashbon_cache_bytes(self.model, rows, wl.tokens) // 4,
                                  dtype=torch.float32, device=device)
         self.text_kv_valid = ctypes.c_int32(0)
         self.meta = fb.new_meta(L)
@@ -64,8 +74,14 @@ class DraftPool:
         fb.flashbon_draft_step(self.model, self.latents, self.schedule[k], self.schedule[k + 1], self.text,
                                self.cond_index, self.text_kv, self.text_kv_valid, skip, proxy, self.cache,
                                self.meta, self.trace, hidden_dump, stream,
-                               None if sde is None else (sde[0], sde[1], k), preview)
+                               None if sde is None else (sde[0], sde[1], k), preview, self._cfg(None))
         return fb.trace_list(self.trace)
+
+    def _cfg(self, rows):
+        if self.guidance is None:
+            return None
+        unc = self.uncond_index if rows is None else self.uncond_index[:rows]
+        return (self.guidance, unc)
 
     def refine_step(self, k: int, latents=None, cond_index=None, hidden_dump=None, stream=None,
                     sde=None) -> list:
@@ -74,7 +90,8 @@ class DraftPool:
         cond = self.cond_index if cond_index is None else cond_index
         fb.flashbon_refine_step(self.model, lat, self.schedule[k], self.schedule[k + 1], self.text, cond,
                                 self.text_kv, self.text_kv_valid, self.trace, hidden_dump, stream,
-                                None if sde is None else (sde[0], sde[1], k, sde[2] if len(sde) > 2 else 0))
+                                None if sde is None else (sde[0], sde[1], k, sde[2] if len(sde) > 2 else 0),
+                                None, self._cfg(int(lat.shape[0])))
         return fb.trace_list(self.trace)
 
     def draft(self, steps: Optional[int] = None, on_step: Optional[Callable] = None) -> List[list]:
