@@ -41,7 +41,7 @@ def recent_slots(meta_l: Dict) -> List[int]:
     return [(h + 2) % 3, (h + 1) % 3, h][: min(meta_l["count"], 3)]
 
 
-def plan_step(skip: np.ndarray, proxy: np.ndarray, meta: List[Dict], t_cur: float
+def plan_step(skip: np.ndarray, proxy: np.ndarray, meta: List[Dict], t_cur: float, residual: bool = False
               ) -> Tuple[List[Tuple[int, int, int, int]], List[Dict]]:
     """Return (trace, new_meta) for one step.
 
@@ -50,6 +50,8 @@ def plan_step(skip: np.ndarray, proxy: np.ndarray, meta: List[Dict], t_cur: floa
       SKIP:    order -1, slot -1,      live 0
       PROXY:   order 0..2, slot of the most recent entry, live 0/1
     ``t_cur`` is stored as float32, the precision the cache metadata holds.
+    ``residual``: proxies forecast the block's residual delta and add it to their input, so every
+    proxy's output is read (live 1).
     """
     L = len(meta)
     actions = []
@@ -69,7 +71,7 @@ def plan_step(skip: np.ndarray, proxy: np.ndarray, meta: List[Dict], t_cur: floa
         elif a == PROXY:
             order = min(meta[l]["count"], 3) - 1
             nxt = [actions[j] for j in range(l + 1, L) if actions[j] != SKIP]
-            live = 1 if (not nxt or nxt[0] == COMPUTE) else 0
+            live = 1 if (residual or not nxt or nxt[0] == COMPUTE) else 0
             trace.append((PROXY, order, recent_slots(meta[l])[0], live))
         else:
             m = new_meta[l]

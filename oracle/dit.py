@@ -198,9 +198,14 @@ class PoolCache:
 def candidate_velocity(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float,
                        kv: List[Tuple[np.ndarray, np.ndarray]], block_mod: np.ndarray,
                        head_mod: np.ndarray, trace, meta_before: List[Dict], cache: Optional[PoolCache],
-                       row: int, hidden: Optional[List[np.ndarray]] = None) -> np.ndarray:
+                       row: int, hidden: Optional[List[np.ndarray]] = None,
+                       residual: bool = False) -> np.ndarray:
     """The network's velocity v [C, H, W] for one candidate under an already-planned trace; computed
-    block outputs are cached under key ``row``."""
+    block outputs are cached under key ``row``.
+
+    ``residual``: the alternative reading of the proxy in which h^(l) of Eq. 3-5 is the block's
+    residual delta B_l(h) - h (as in TaylorSeer-style feature forecasting): a computed block caches its
+    delta, a proxied block adds the forecast delta to its input."""
     C, H, Wd = z.shape
     p = shape.patch
     tok = patchify(np.asarray(z, f64), p)
@@ -214,11 +219,12 @@ def candidate_velocity(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: fl
             m = meta_before[l]
             slots = recent_slots(m)
             entries = [(cache.data[(row, l, s)], m["t"][s]) for s in slots]
-            h = taylor_proxy(entries, t_cur, order)
+            h = h + taylor_proxy(entries, t_cur, order) if residual else taylor_proxy(entries, t_cur, order)
         else:                                                 # Eq. 7
+            h_in = h
             h = block_forward(W, l, h, block_mod[l], kv[l], shape.heads, shape.ln_eps)
             if cache is not None:
-                cache.data[(row, l, slot)] = h.copy()
+                cache.data[(row, l, slot)] = (h - h_in) if residual else h.copy()
         if hidden is not None:
             hidden.append(h.copy())
     sh, sc = head_mod
@@ -280,7 +286,7 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
                candidates: Optional[Sequence[int]] = None,
                hidden: Optional[Dict[int, List[np.ndarray]]] = None,
                sde_args: Optional[Tuple[float, int, int]] = None,
-               cfg: Optional[Tuple[float, np.ndarray]] = None):
+               cfg: Optional[Tuple[float, np.ndarray]] = None, residual: bool = False):
     """One draft step over the pool (Eq. 2 with the knobs of Sec. 4.1).
 
     z [N, C, H, W]; returns (z_next [N, C, H, W] fp64 -- rows not in ``candidates`` are left as z --,
@@ -289,18 +295,19 @@ def draft_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_n
     drawing the normals of counter row row0 + n (row0 = 0 by default) at ``step``.
     ``cfg = (scale, uncond_index)``: classifier-free guidance; candidate n also runs with prompt
     uncond_index[n] (cache key N + n) and steps with v_u + scale (v_c - v_u).
+    ``residual``: proxies forecast residual deltas (see ``candidate_velocity``).
     """
-    trace, new_meta = plan_step(skip, proxy, cache.meta, t_cur)
+    trace, new_meta = plan_step(skip, proxy, cache.meta, t_cur, residual)
     block_mod, head_mod = modulations(W, shape.num_blocks, shape.freq_dim, t_cur)
     out = np.asarray(z, f64).copy()
     N = z.shape[0]
     for n in (range(N) if candidates is None else candidates):
         hid = None if hidden is None else hidden.setdefault(n, [])
         v = candidate_velocity(W, shape, z[n], t_cur, kv_per_cond[int(cond_index[n])], block_mod, head_mod,
-                               trace, cache.meta, cache, n, hid)
+                               trace, cache.meta, cache, n, hid, residual)
         if cfg is not None:
             v_u = candidate_velocity(W, shape, z[n], t_cur, kv_per_cond[int(cfg[1][n])], block_mod, head_mod,
-                                     trace, cache.meta, cache, N + n)
+                                     trace, cache.meta, cache, N + n, None, residual)
             v = guided(v, v_u, cfg[0])
         out[n] = update(z[n], v, t_cur, t_next, _noise(sde_args, n))
     cache.meta = new_meta
@@ -337,7 +344,7 @@ def prepare_text(W: Dict[str, np.ndarray], shape, text: np.ndarray):
 
 
 def run_draft(W, shape, z0, schedule, steps_draft: int, masks, text, cond_index,
-              candidates: Optional[Sequence[int]] = None, on_step=None):
+              candidates: Optional[Sequence[int]] = None, on_step=None, residual: bool = False):
     """Truncated trajectory (Eq. 2 truncated to S' steps).  ``masks(k)`` -> (skip, proxy).
 
     Returns (z after S' steps, cache, traces).  ``on_step(k, z)`` is called after each step.
@@ -349,7 +356,7 @@ def run_draft(W, shape, z0, schedule, steps_draft: int, masks, text, cond_index,
     for k in range(steps_draft):
         skip, proxy = masks(k)
         z, tr = draft_step(W, shape, z, schedule[k], schedule[k + 1], kv, cond_index, skip, proxy,
-                           cache, candidates)
+                           cache, candidates, residual=residual)
         traces.append(tr)
         if on_step is not None:
             on_step(k, z)

@@ -433,3 +433,44 @@ def test_guidance_end_points_and_linearity():
     np.testing.assert_allclose(step((0.0, unc)), plain_u, rtol=0, atol=1e-12)
     np.testing.assert_allclose(step((2.0, unc)) - plain_c, plain_c - plain_u, rtol=0, atol=1e-12)
     assert not np.allclose(plain_c, plain_u)
+
+
+def _constant_delta_weights(W, L):
+    """Zero every block matrix and modulation table, and the shared modulation matrix: each block then
+    adds a delta made of biases and constant gates only -- the same at every timestep and for every
+    input."""
+    W2 = dict(W)
+    W2["mod_w"] = np.zeros_like(W["mod_w"])
+    for l in range(L):
+        for name in ("wq", "wk", "wv", "wo", "wqc", "wkc", "wvc", "woc", "w1", "w2", "mod"):
+            W2[f"blk{l}.{name}"] = np.zeros_like(W[f"blk{l}.{name}"])
+    return W2
+
+
+def test_residual_proxy_is_exact_for_constant_deltas():
+    """The residual-delta reading of Eq. 3-5 forecasts B_l(h) - h and adds it to the proxied block's
+    input.  With constant block deltas every forecast is exact, so a proxied trajectory equals the fully
+    computed one; the output reading (which ignores the block's input) does not."""
+    wl, W, z, text = _tiny_setup()
+    L = wl.shape.num_blocks
+    W2 = _constant_delta_weights(W, L)
+    sched = wl.schedule()
+    cond = wl.cond_index()
+    full = od_dit.run_refine(W2, wl.shape, z, sched, 0, text, cond)
+    proxied = lambda k: (np.zeros(L, np.uint8), np.full(L, 1 if k % 2 else 0, np.uint8))
+    res, _, traces = od_dit.run_draft(W2, wl.shape, z, sched, 4, proxied, text, cond, residual=True)
+    out, _, _ = od_dit.run_draft(W2, wl.shape, z, sched, 4, proxied, text, cond)
+    assert any(e[0] == od.PROXY for tr in traces for e in tr)
+    np.testing.assert_allclose(res, full, rtol=0, atol=1e-12)
+    assert np.abs(out - full).max() > 1e-3
+
+
+def test_residual_mode_makes_every_proxy_live():
+    meta = [{"count": 2, "head": 2, "t": [0.9, 0.8, 0.0]} for _ in range(4)]
+    skip = np.array([0, 0, 1, 0], np.uint8)
+    proxy = np.ones(4, np.uint8)
+    tr_out, _ = od.plan_step(skip, proxy, meta, 0.7)
+    tr_res, _ = od.plan_step(skip, proxy, meta, 0.7, residual=True)
+    assert [e[3] for e in tr_out] == [0, 0, 0, 1]            # each proxy is overwritten by the next
+    assert [e[3] for e in tr_res] == [1, 1, 0, 1]            # the skipped block stays not live
+    assert [e[:3] for e in tr_out] == [e[:3] for e in tr_res]
