@@ -160,6 +160,14 @@ typedef struct {
   int32_t cfg;
   float cfg_scale;
   const int32_t *uncond_index;
+
+  /* Reading of the activation proxy (draft only): 0 (FLASHBON_PROXY_OUTPUT) -- h^(l) of Eq. 3-5 is
+   * the block's output, cached by computed blocks and forecast by proxies; 1
+   * (FLASHBON_PROXY_RESIDUAL) -- h^(l) is the block's residual delta B_l(h) - h: computed blocks cache
+   * their delta and a proxy adds the forecast delta to its input (every proxy is then live and the
+   * patch embedding always runs).  The cache holds one reading's entries: switching between calls
+   * needs a reset cache (meta count 0). */
+  int32_t proxy_mode;
 } flashbon_step_args;
 
 /* Number of floats `host_weights` must hold for `cfg`. Returns 0 if cfg is invalid. */
@@ -199,11 +207,14 @@ flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args
 /* Release the model.  NULL is a no-op.  Synchronises the device before freeing. */
 void flashbon_free(void *model);
 
+enum { FLASHBON_PROXY_OUTPUT = 0, FLASHBON_PROXY_RESIDUAL = 1 };
+
 /* Host-only dispatch of one step, as flashbon_draft_step performs it (Eq. 3-6 plus the cache
- * ring): fills trace[num_blocks] and advances meta[num_blocks] in place.  No device work. */
+ * ring): fills trace[num_blocks] and advances meta[num_blocks] in place.  proxy_mode as in
+ * flashbon_step_args.  No device work. */
 flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, const uint8_t *proxy,
                                    flashbon_cache_meta *meta, float t_cur,
-                                   flashbon_trace_entry *trace);
+                                   flashbon_trace_entry *trace, int32_t proxy_mode);
 
 /* Verifier callback of flashbon_select: judge candidate a (ranked above b) against candidate b.
  * Returns the winner (a or b) and writes the verifier's confidence to *confidence: 0 high, 1 medium,

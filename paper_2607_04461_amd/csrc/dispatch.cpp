@@ -11,7 +11,7 @@ bool meta_valid(const flashbon_cache_meta &m) {
 }
 
 void plan_step(int L, const uint8_t *skip, const uint8_t *proxy, flashbon_cache_meta *meta,
-               float t_cur, flashbon_trace_entry *trace) {
+               float t_cur, flashbon_trace_entry *trace, bool residual) {
   // 1) action per block: skip wins; a proxy needs at least one cached entry
   for (int l = 0; l < L; ++l) {
     int8_t a = FLASHBON_COMPUTE;
@@ -33,7 +33,7 @@ void plan_step(int L, const uint8_t *skip, const uint8_t *proxy, flashbon_cache_
       int next = -1;
       for (int j = l + 1; j < L; ++j)
         if (trace[j].action != FLASHBON_SKIP) { next = trace[j].action; break; }
-      e.live = (next == -1 || next == FLASHBON_COMPUTE) ? 1 : 0;
+      e.live = (residual || next == -1 || next == FLASHBON_COMPUTE) ? 1 : 0;
     } else {
       e.order = -1;
       e.slot = (int8_t)m.head;

@@ -7,9 +7,10 @@ namespace fb {
 
 bool meta_valid(const flashbon_cache_meta &m);
 
-// Fills trace[L] and advances meta[L] in place (see flashbon_plan_step).
+// Fills trace[L] and advances meta[L] in place (see flashbon_plan_step).  residual: proxies add a
+// forecast residual delta to their input, so every proxy is live.
 void plan_step(int L, const uint8_t *skip, const uint8_t *proxy, flashbon_cache_meta *meta,
-               float t_cur, flashbon_trace_entry *trace);
+               float t_cur, flashbon_trace_entry *trace, bool residual = false);
 
 // Coefficients (ca, cb) of the difference form h1 + ca (h1 - h2) + cb (h1 - 2 h2 + h3) for a proxy
 // of the given order, from the block's metadata before the step.

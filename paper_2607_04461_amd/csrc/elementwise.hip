@@ -92,7 +92,7 @@ hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, con
 // ------------------------------------------------------------------------------ activation proxy
 // Difference form h1 + ca (h1 - h2) + cb (h1 - 2 h2 + h3): a constant cache reproduces itself
 // exactly, whatever the coefficients.
-template <int ORDER>
+template <int ORDER, bool ACC>
 __global__ __launch_bounds__(256) void k_proxy(int64_t n4, const float4 *__restrict__ h1,
                                                const float4 *__restrict__ h2,
                                                const float4 *__restrict__ h3, float ca, float cb,
@@ -101,6 +101,10 @@ __global__ __launch_bounds__(256) void k_proxy(int64_t n4, const float4 *__restr
        i += (int64_t)gridDim.x * blockDim.x) {
     float4 a = h1[i];
     if constexpr (ORDER == 0) {
+      if constexpr (ACC) {
+        float4 o = out[i];
+        a = make_float4(o.x + a.x, o.y + a.y, o.z + a.z, o.w + a.w);
+      }
       out[i] = a;
     } else {
       float4 b = h2[i];
@@ -113,24 +117,36 @@ __global__ __launch_bounds__(256) void k_proxy(int64_t n4, const float4 *__restr
         r.z += cb * ((a.z - b.z) - (b.z - c.z));
         r.w += cb * ((a.w - b.w) - (b.w - c.w));
       }
+      if constexpr (ACC) {
+        float4 o = out[i];
+        r = make_float4(o.x + r.x, o.y + r.y, o.z + r.z, o.w + r.w);
+      }
       out[i] = r;
     }
   }
 }
 
 __global__ void k_proxy_tail(int64_t start, int64_t count, const float *h1, const float *h2,
-                             const float *h3, int order, float ca, float cb, float *out) {
+                             const float *h3, int order, float ca, float cb, float *out, int acc) {
   int64_t i = start + threadIdx.x;
   if (i >= count) return;
   float a = h1[i];
   float r = a;
   if (order >= 1) r = a + ca * (a - h2[i]);
   if (order >= 2) r += cb * ((a - h2[i]) - (h2[i] - h3[i]));
-  out[i] = r;
+  out[i] = acc ? out[i] + r : r;
+}
+
+template <bool ACC>
+static void proxy_body(int64_t n4, dim3 g, dim3 b, hipStream_t s, int order, const float4 *a, const float4 *bb,
+                       const float4 *c, float ca, float cb, float4 *o) {
+  if (order == 0) hipLaunchKernelGGL((k_proxy<0, ACC>), g, b, 0, s, n4, a, bb, c, ca, cb, o);
+  else if (order == 1) hipLaunchKernelGGL((k_proxy<1, ACC>), g, b, 0, s, n4, a, bb, c, ca, cb, o);
+  else hipLaunchKernelGGL((k_proxy<2, ACC>), g, b, 0, s, n4, a, bb, c, ca, cb, o);
 }
 
 hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const float *h3, int order,
-                        float ca, float cb, float *out, hipStream_t s) {
+                        float ca, float cb, float *out, hipStream_t s, bool accumulate) {
   int64_t n4 = count / 4;
   if (n4 > 0) {
     int64_t blocks = (n4 + 255) / 256;
@@ -138,13 +154,12 @@ hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const f
     dim3 g((unsigned)blocks), b(256);
     auto *o = (float4 *)out;
     auto *a = (const float4 *)h1, *bb = (const float4 *)h2, *c = (const float4 *)h3;
-    if (order == 0) hipLaunchKernelGGL(k_proxy<0>, g, b, 0, s, n4, a, bb, c, ca, cb, o);
-    else if (order == 1) hipLaunchKernelGGL(k_proxy<1>, g, b, 0, s, n4, a, bb, c, ca, cb, o);
-    else hipLaunchKernelGGL(k_proxy<2>, g, b, 0, s, n4, a, bb, c, ca, cb, o);
+    if (accumulate) proxy_body<true>(n4, g, b, s, order, a, bb, c, ca, cb, o);
+    else proxy_body<false>(n4, g, b, s, order, a, bb, c, ca, cb, o);
   }
   if (count % 4)
     hipLaunchKernelGGL(k_proxy_tail, dim3(1), dim3(64), 0, s, n4 * 4, count, h1, h2, h3, order, ca,
-                       cb, out);
+                       cb, out, accumulate ? 1 : 0);
   return hipGetLastError();
 }
 

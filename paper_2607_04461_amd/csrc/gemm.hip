@@ -51,7 +51,15 @@ __device__ __forceinline__ void epilogue4(const EpiArgs &e, int m, int n, float 
       h.x += v[0]; h.y += v[1]; h.z += v[2]; h.w += v[3];
     }
     *reinterpret_cast<float4 *>(o) = h;
-    if (e.cache) *reinterpret_cast<float4 *>(e.cache + (int64_t)m * e.ldo + n) = h;
+    if (e.cache) {
+      float4 *cp = reinterpret_cast<float4 *>(e.cache + (int64_t)m * e.ldo + n);
+      if (e.cache_delta) {
+        const float4 c0 = *cp;
+        *cp = make_float4(h.x - c0.x, h.y - c0.y, h.z - c0.z, h.w - c0.w);
+      } else {
+        *cp = h;
+      }
+    }
   } else if constexpr (EPI == EPI_EULER) {
     // m = candidate * T + token, token = i * (W/p) + j; n = c p^2 + p di + dj
     const int b = m / e.T, t = m % e.T, wp = e.W / e.p;
@@ -118,9 +126,15 @@ __device__ __forceinline__ void epilogue8(const EpiArgs &e, int m, int n, const 
       reinterpret_cast<float4 *>(o)[0] = h0;
       reinterpret_cast<float4 *>(o)[1] = h1;
       if (e.cache) {
-        float *c = e.cache + (int64_t)m * e.ldo + n;
-        reinterpret_cast<float4 *>(c)[0] = h0;
-        reinterpret_cast<float4 *>(c)[1] = h1;
+        float4 *c = reinterpret_cast<float4 *>(e.cache + (int64_t)m * e.ldo + n);
+        if (e.cache_delta) {
+          const float4 c0 = c[0], c1 = c[1];
+          c[0] = make_float4(h0.x - c0.x, h0.y - c0.y, h0.z - c0.z, h0.w - c0.w);
+          c[1] = make_float4(h1.x - c1.x, h1.y - c1.y, h1.z - c1.z, h1.w - c1.w);
+        } else {
+          c[0] = h0;
+          c[1] = h1;
+        }
       }
     }
   }

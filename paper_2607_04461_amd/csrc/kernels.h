@@ -23,6 +23,7 @@ struct EpiArgs {
   const float *bias = nullptr; // [N] or null
   const float *gate = nullptr; // [N] or null (RESIDUAL)
   float *cache = nullptr;      // [M][ldo] fp32 or null (RESIDUAL)
+  bool cache_delta = false;    // RESIDUAL: cache = updated out - cache (the cache held the block input)
   // EULER: z [n][C][H][W] fp32, tokens per candidate T = (H/p)(W/p), N = C p p
   float *z = nullptr;
   float dt = 0.f;
@@ -47,9 +48,10 @@ hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s);
 hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, const float *shift,
                          const float *scale, void *out, hipStream_t s);
 
-// out = h1 + ca (h1 - h2) + cb (h1 - 2 h2 + h3)   (order 2; order 1 drops cb, order 0 copies h1)
+// out = h1 + ca (h1 - h2) + cb (h1 - 2 h2 + h3)   (order 2; order 1 drops cb, order 0 copies h1);
+// accumulate: out += that forecast instead
 hipError_t launch_proxy(int64_t count, const float *h1, const float *h2, const float *h3, int order,
-                        float ca, float cb, float *out, hipStream_t s);
+                        float ca, float cb, float *out, hipStream_t s, bool accumulate = false);
 
 // tokens [n*T][C p p] (act) from z [zrows][C][H][W] fp32; token row block b reads latent b % zrows
 hipError_t launch_patchify(ActType t, int n, int zrows, int C, int H, int W, int p, const float *z, void *tok,

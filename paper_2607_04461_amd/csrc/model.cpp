@@ -98,13 +98,15 @@ size_t flashbon_weight_count(const flashbon_model_config *cfg) {
 
 flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, const uint8_t *proxy,
                                    flashbon_cache_meta *meta, float t_cur,
-                                   flashbon_trace_entry *trace) {
+                                   flashbon_trace_entry *trace, int32_t proxy_mode) {
   if (num_blocks < 1) return fail(FLASHBON_ESHAPE, "num_blocks must be >= 1");
   if (!meta || !trace) return fail(FLASHBON_EINVAL, "meta and trace are required");
   if (!std::isfinite(t_cur)) return fail(FLASHBON_EINVAL, "t_cur must be finite");
   for (int l = 0; l < num_blocks; ++l)
     if (!meta_valid(meta[l])) return fail(FLASHBON_ESTATE, "cache meta out of range at block " + std::to_string(l));
-  plan_step(num_blocks, skip, proxy, meta, t_cur, trace);
+  if (proxy_mode != FLASHBON_PROXY_OUTPUT && proxy_mode != FLASHBON_PROXY_RESIDUAL)
+    return fail(FLASHBON_EINVAL, "proxy_mode must be 0 or 1");
+  plan_step(num_blocks, skip, proxy, meta, t_cur, trace, proxy_mode == FLASHBON_PROXY_RESIDUAL);
   g_err.clear();
   return FLASHBON_OK;
 }
@@ -276,6 +278,9 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     for (int i = 0; i < a->n; ++i)
       if (a->uncond_index[i] < 0 || a->uncond_index[i] >= a->n_cond)
         return fail(FLASHBON_EINVAL, "uncond_index[" + std::to_string(i) + "] outside [0, n_cond)");
+  if (a->proxy_mode != FLASHBON_PROXY_OUTPUT && a->proxy_mode != FLASHBON_PROXY_RESIDUAL)
+    return fail(FLASHBON_EINVAL, "proxy_mode must be 0 or 1");
+  const bool residual = draft && a->proxy_mode == FLASHBON_PROXY_RESIDUAL;
   if (draft) {
     if (!a->meta) return fail(FLASHBON_EINVAL, "draft step needs meta");
     if (!a->cache) return fail(FLASHBON_EINVAL, "draft step needs cache");
@@ -286,7 +291,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   std::vector<flashbon_trace_entry> trace(L);
   if (draft) {
     std::memcpy(meta_new.data(), a->meta, sizeof(flashbon_cache_meta) * L);
-    plan_step(L, a->skip, a->proxy, meta_new.data(), a->t_cur, trace.data());
+    plan_step(L, a->skip, a->proxy, meta_new.data(), a->t_cur, trace.data(), residual);
   } else {
     std::vector<flashbon_cache_meta> z(L);
     std::memset(z.data(), 0, sizeof(flashbon_cache_meta) * L);
@@ -365,7 +370,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
 
   // patch embedding, unless the first non-skipped block is a proxy (its input is then never read)
   bool embed_live = true;
-  for (int l = 0; l < L; ++l)
+  for (int l = 0; l < L && !residual; ++l)
     if (trace[l].action != FLASHBON_SKIP) { embed_live = trace[l].action == FLASHBON_COMPUTE; break; }
   if (embed_live) {
     HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, R, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s); }), "patchify");
@@ -389,12 +394,16 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       const flashbon_cache_meta &mb = a->meta[l];
       const int s1 = (mb.head + 2) % 3, s2 = (mb.head + 1) % 3, s3 = mb.head;
       auto slot_ptr = [&](int sl) { return a->cache + ((int64_t)l * 3 + sl) * MD; };
-      HIPCHK(timed(m, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s); }),
+      HIPCHK(timed(m, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s, residual); }),
              "activation proxy");
       if ((st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
     }
-    // COMPUTE (Eq. 7)
+    // COMPUTE (Eq. 7); the residual reading first keeps the block input in its cache slot, which the
+    // down-projection epilogue turns into the block's delta
+    if (residual)
+      HIPCHK(hipMemcpyAsync(a->cache + ((int64_t)l * 3 + tr.slot) * MD, m->h, MD * 4, hipMemcpyDeviceToDevice, s),
+             "block input to cache");
     HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 0 * D, mod + 1 * D, m->a, s); }), "adaLN 1");
     {
       EpiArgs e; e.out = m->qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
@@ -440,6 +449,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     {
       EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
       if (draft) e.cache = a->cache + ((int64_t)l * 3 + tr.slot) * MD;
+      e.cache_delta = residual;
       HIPCHK(timed(m, FLASHBON_SITE_MLP_DOWN, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, F, m->u, Wp(b.w2), e, s); }), "mlp down");
     }
     if ((st = dump(l + 1)) != FLASHBON_OK) return st;

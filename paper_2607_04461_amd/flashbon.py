@@ -61,6 +61,7 @@ class StepArgs(ctypes.Structure):
         ("sde_a", ctypes.c_float), ("sde_step", ctypes.c_int32), ("sde_seed", ctypes.c_uint64),
         ("sde_row0", ctypes.c_int32), ("preview", ctypes.c_void_p),
         ("cfg", ctypes.c_int32), ("cfg_scale", ctypes.c_float), ("uncond_index", ctypes.POINTER(ctypes.c_int32)),
+        ("proxy_mode", ctypes.c_int32),
     ]
 
 
@@ -103,7 +104,7 @@ def load() -> ctypes.CDLL:
     L.flashbon_free.argtypes = [vp]
     L.flashbon_free.restype = None
     L.flashbon_plan_step.argtypes = [i32, ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_uint8),
-                                     ctypes.POINTER(CacheMeta), f32, ctypes.POINTER(TraceEntry)]
+                                     ctypes.POINTER(CacheMeta), f32, ctypes.POINTER(TraceEntry), i32]
     L.flashbon_plan_step.restype = i32
     L.flashbon_set_timing.argtypes = [vp, ctypes.c_uint32]
     L.flashbon_set_timing.restype = i32
@@ -203,7 +204,7 @@ def trace_list(trace) -> list:
 
 def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
           skip=None, proxy=None, cache=None, meta=None, trace=None, hidden_dump=None, stream=None,
-          num_blocks=None, sde=None, preview=None, cfg=None):
+          num_blocks=None, sde=None, preview=None, cfg=None, proxy_mode=0):
     n, C, H, W = (int(x) for x in latents.shape)
     n_cond, text_len = int(text.shape[0]), int(text.shape[1])
     cond = np.ascontiguousarray(np.asarray(cond_index, dtype=np.int32))
@@ -227,6 +228,7 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
     a.trace = trace
     a.hidden_dump = _ptr(hidden_dump)
     a.preview = _ptr(preview)
+    a.proxy_mode = int(proxy_mode)
     if cfg is not None:
         unc = np.ascontiguousarray(np.asarray(cfg[1], dtype=np.int32))
         if unc.shape != (n,):
@@ -242,14 +244,15 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
 
 def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
                         skip, proxy, cache, meta, trace=None, hidden_dump=None, stream=None, sde=None,
-                        preview=None, cfg=None):
+                        preview=None, cfg=None, proxy_mode=0):
     """One draft step; ``text_kv_valid`` is a ctypes.c_int32, ``meta``/``trace`` ctypes arrays;
     ``sde = (a, seed, step[, row0])`` selects the stochastic update (None or a = 0: Euler);
     ``preview`` (device [n, C, H, W] fp32) receives z - t_cur v; ``cfg = (scale, uncond_index)``
-    turns on classifier-free guidance (the cache then holds 2n rows)."""
+    turns on classifier-free guidance (the cache then holds 2n rows); ``proxy_mode`` 1 takes the
+    residual-delta reading of the proxy."""
     _step(load().flashbon_draft_step, "flashbon_draft_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, skip, proxy, cache, meta, trace, hidden_dump, stream,
-          num_blocks=len(meta), sde=sde, preview=preview, cfg=cfg)
+          num_blocks=len(meta), sde=sde, preview=preview, cfg=cfg, proxy_mode=proxy_mode)
 
 
 def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
@@ -287,13 +290,14 @@ def flashbon_select(scores, judge, rho1=0.5, rho2=0.5, kappa=1.5):
     return int(winner.value), ratings, int(calls.value)
 
 
-def flashbon_plan_step(skip, proxy, meta, t_cur: float, trace=None):
+def flashbon_plan_step(skip, proxy, meta, t_cur: float, trace=None, proxy_mode: int = 0):
     L = len(meta)
     sk, skp = _u8(skip, L)
     px, pxp = _u8(proxy, L)
     if trace is None:
         trace = new_trace(L)
-    _check(load().flashbon_plan_step(L, skp, pxp, meta, float(t_cur), trace), "flashbon_plan_step")
+    _check(load().flashbon_plan_step(L, skp, pxp, meta, float(t_cur), trace, int(proxy_mode)),
+           "flashbon_plan_step")
     return trace
 
 

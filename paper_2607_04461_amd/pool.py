@@ -18,7 +18,7 @@ from . import synth
 class DraftPool:
     def __init__(self, wl: synth.Workload, dtype: Optional[str] = None, weights: Optional[np.ndarray] = None,
                  device: str = "cuda", max_n: Optional[int] = None, max_cond: Optional[int] = None,
-                 guidance: Optional[float] = None):
+                 guidance: Optional[float] = None, proxy_mode: int = 0):
         """``guidance``: classifier-free guidance scale; every candidate then also runs with a null prompt
         (an all-zero text appended as prompt n_cond) and the cache holds 2n rows."""
         import torch
@@ -30,6 +30,7 @@ class DraftPool:
         if weights is None:
             weights, _ = synth.make_weights(wl.shape, wl.seed_w)
         self.guidance = guidance
+        self.proxy_mode = proxy_mode            # 1: residual-delta reading of the proxy
         rows = 2 * wl.n if guidance is not None else wl.n
         n_text = wl.n_cond + (1 if guidance is not None else 0)
         cfg = fb.make_config(wl.shape, fb.BF16 if self.dtype == "bf16" else fb.FP32,
@@ -74,7 +75,8 @@ class DraftPool:
         fb.flashbon_draft_step(self.model, self.latents, self.schedule[k], self.schedule[k + 1], self.text,
                                self.cond_index, self.text_kv, self.text_kv_valid, skip, proxy, self.cache,
                                self.meta, self.trace, hidden_dump, stream,
-                               None if sde is None else (sde[0], sde[1], k), preview, self._cfg(None))
+                               None if sde is None else (sde[0], sde[1], k), preview, self._cfg(None),
+                               self.proxy_mode)
         return fb.trace_list(self.trace)
 
     def _cfg(self, rows):

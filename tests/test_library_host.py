@@ -49,7 +49,8 @@ def test_plan_step_matches_oracle_on_workloads(name):
             assert list(meta_c[l].t) == meta_o[l]["t"]
 
 
-def test_plan_step_random_masks_bit_exact():
+@pytest.mark.parametrize("mode", [0, 1])
+def test_plan_step_random_masks_bit_exact(mode):
     rng = np.random.default_rng(42)
     for trial in range(200):
         L = int(rng.integers(1, 12))
@@ -59,10 +60,15 @@ def test_plan_step_random_masks_bit_exact():
         for k in range(int(rng.integers(1, 9))):
             skip = (rng.random(L) < rng.random()).astype(np.uint8)
             proxy = (rng.random(L) < rng.random()).astype(np.uint8)
-            tr_c = fb.trace_list(fb.flashbon_plan_step(skip, proxy, meta_c, t))
-            tr_o, meta_o = od.plan_step(skip, proxy, meta_o, t)
+            tr_c = fb.trace_list(fb.flashbon_plan_step(skip, proxy, meta_c, t, proxy_mode=mode))
+            tr_o, meta_o = od.plan_step(skip, proxy, meta_o, t, residual=bool(mode))
             assert tr_c == [tuple(e) for e in tr_o]
             t -= float(rng.random()) * 0.1
+
+
+def test_plan_step_rejects_unknown_proxy_mode():
+    with pytest.raises(fb.FlashbonError):
+        fb.flashbon_plan_step(np.zeros(3), np.zeros(3), fb.new_meta(3), 0.5, proxy_mode=2)
 
 
 def test_plan_step_rejects_bad_meta():
