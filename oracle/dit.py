@@ -129,27 +129,82 @@ def unpatchify(tok: np.ndarray, C: int, H: int, Wd: int, p: int) -> np.ndarray:
     return x.reshape(C, H, Wd)
 
 
-def text_kv(W: Dict[str, np.ndarray], num_blocks: int, text: np.ndarray
+def text_kv(W: Dict[str, np.ndarray], num_blocks: int, text: np.ndarray, eps: float = 1e-6
             ) -> List[Tuple[np.ndarray, np.ndarray]]:
-    """Per-block cross-attention keys/values of one prompt: ctx = text W_txt^T + b; K, V = ctx W^T + b."""
+    """Per-block cross-attention keys/values of one prompt: ctx = text W_txt^T + b; K, V = ctx W^T + b
+    (K RMS-normalised with its gain when the model has qk RMSNorm, reading R26)."""
     ctx = linear(np.asarray(text, f64), W["txt_w"], W["txt_b"])
-    return [(linear(ctx, W[f"blk{l}.wkc"], W[f"blk{l}.bkc"]),
-             linear(ctx, W[f"blk{l}.wvc"], W[f"blk{l}.bvc"])) for l in range(num_blocks)]
+    out = []
+    for l in range(num_blocks):
+        k = linear(ctx, W[f"blk{l}.wkc"], W[f"blk{l}.bkc"])
+        if f"blk{l}.nkc" in W:
+            k = rms_norm(k, W[f"blk{l}.nkc"], eps)
+        out.append((k, linear(ctx, W[f"blk{l}.wvc"], W[f"blk{l}.bvc"])))
+    return out
+
+
+def rms_norm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * g over the last axis (textbook RMSNorm)."""
+    x = np.asarray(x, f64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + f64(eps)) * np.asarray(g, f64)
+
+
+def rope_bands(dh: int) -> Tuple[int, int, int]:
+    """Head-dim split of the 3-D rotary embedding: (frame, height, width) bands; reading R26."""
+    q = dh // 6
+    return dh - 4 * q, 2 * q, 2 * q
+
+
+def rope_angles(hp: int, wp: int, dh: int, theta: float = 10000.0) -> np.ndarray:
+    """[T, dh/2] rotation angles of tokens t = i wp + j at position (frame 0, row i, column j): pair k of
+    a band of width d at position p turns by p theta^(-2k/d); bands in frame, height, width order."""
+    fb_, hb, wb = rope_bands(dh)
+    T = hp * wp
+    pos = np.stack([np.zeros(T), np.arange(T) // wp, np.arange(T) % wp], axis=1).astype(f64)
+    cols = []
+    for band, d in enumerate((fb_, hb, wb)):
+        freq = f64(theta) ** (-np.arange(0, d, 2, dtype=f64) / d)
+        cols.append(pos[:, band:band + 1] * freq[None, :])
+    return np.concatenate(cols, axis=1)
+
+
+def apply_rope(x: np.ndarray, angles: np.ndarray, heads: int) -> np.ndarray:
+    """Rotate consecutive pairs (2k, 2k + 1) of every head of x [T, D] by angles [T, dh/2]."""
+    x = np.asarray(x, f64)
+    T, D = x.shape
+    dh = D // heads
+    xr = x.reshape(T, heads, dh // 2, 2)
+    c, s = np.cos(angles)[:, None, :], np.sin(angles)[:, None, :]
+    out = np.empty_like(xr)
+    out[..., 0] = xr[..., 0] * c - xr[..., 1] * s
+    out[..., 1] = xr[..., 0] * s + xr[..., 1] * c
+    return out.reshape(T, D)
 
 
 def block_forward(W: Dict[str, np.ndarray], l: int, h: np.ndarray, mod: np.ndarray,
-                  kv: Tuple[np.ndarray, np.ndarray], heads: int, eps: float) -> np.ndarray:
-    """B_l(h, x, t) (Eq. 7) for one candidate; h [T, D], mod [6, D] -> new residual stream [T, D]."""
+                  kv: Tuple[np.ndarray, np.ndarray], heads: int, eps: float,
+                  angles: Optional[np.ndarray] = None) -> np.ndarray:
+    """B_l(h, x, t) (Eq. 7) for one candidate; h [T, D], mod [6, D] -> new residual stream [T, D].
+
+    With qk RMSNorm weights in W (reading R26): q and k of both attentions are RMS-normalised over D
+    with their gains, and self-attention's q and k are then rotated by ``angles`` (3-D RoPE); the text
+    keys in ``kv`` are normalised where they are made (``text_kv``)."""
     b = f"blk{l}."
+    qkn = (b + "nq") in W
     sh1, sc1, g1, sh2, sc2, g2 = mod
     a = layer_norm(h, eps) * (1.0 + sc1) + sh1
     q = linear(a, W[b + "wq"], W[b + "bq"])
     k = linear(a, W[b + "wk"], W[b + "bk"])
     v = linear(a, W[b + "wv"], W[b + "bv"])
+    if qkn:
+        q = apply_rope(rms_norm(q, W[b + "nq"], eps), angles, heads)
+        k = apply_rope(rms_norm(k, W[b + "nk"], eps), angles, heads)
     o = multi_head_attention(q, k, v, heads)
     h = h + g1 * linear(o, W[b + "wo"], W[b + "bo"])
     c = layer_norm(h, eps)
     qc = linear(c, W[b + "wqc"], W[b + "bqc"])
+    if qkn:
+        qc = rms_norm(qc, W[b + "nqc"], eps)
     oc = multi_head_attention(qc, kv[0], kv[1], heads)
     h = h + linear(oc, W[b + "woc"], W[b + "boc"])
     a = layer_norm(h, eps) * (1.0 + sc2) + sh2
@@ -208,6 +263,7 @@ def candidate_velocity(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: fl
     delta, a proxied block adds the forecast delta to its input."""
     C, H, Wd = z.shape
     p = shape.patch
+    angles = rope_angles(H // p, Wd // p, shape.head_dim) if getattr(shape, "qk_norm_rope", False) else None
     tok = patchify(np.asarray(z, f64), p)
     h = linear(tok, W["pe_w"], W["pe_b"])
     if hidden is not None:
@@ -222,7 +278,7 @@ def candidate_velocity(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: fl
             h = h + taylor_proxy(entries, t_cur, order) if residual else taylor_proxy(entries, t_cur, order)
         else:                                                 # Eq. 7
             h_in = h
-            h = block_forward(W, l, h, block_mod[l], kv[l], shape.heads, shape.ln_eps)
+            h = block_forward(W, l, h, block_mod[l], kv[l], shape.heads, shape.ln_eps, angles)
             if cache is not None:
                 cache.data[(row, l, slot)] = (h - h_in) if residual else h.copy()
         if hidden is not None:
@@ -340,7 +396,7 @@ def refine_step(W: Dict[str, np.ndarray], shape, z: np.ndarray, t_cur: float, t_
 
 def prepare_text(W: Dict[str, np.ndarray], shape, text: np.ndarray):
     """Per-prompt cross-attention keys/values for every block."""
-    return [text_kv(W, shape.num_blocks, text[c]) for c in range(text.shape[0])]
+    return [text_kv(W, shape.num_blocks, text[c], shape.ln_eps) for c in range(text.shape[0])]
 
 
 def run_draft(W, shape, z0, schedule, steps_draft: int, masks, text, cond_index,

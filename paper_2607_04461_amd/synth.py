@@ -23,6 +23,7 @@ from typing import Dict, List, Optional, Tuple
 import numpy as np
 
 WEIGHT_STD = 0.02
+NORM_GAINS = ("nq", "nk", "nqc", "nkc")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -36,6 +37,7 @@ class ModelShape:
     latent_channels: int = 16
     patch: int = 2
     ln_eps: float = 1e-6
+    qk_norm_rope: bool = False      # RMSNorm on q/k (self and cross) + 3-D RoPE on self-attention
 
     @property
     def head_dim(self) -> int:
@@ -106,6 +108,11 @@ WORKLOADS: Dict[str, Workload] = {
     # mid-size parity pool (head_dim 128, ragged token count 130, 2 prompts)
     "mid": Workload("mid", MID, n=3, latent_h=10, latent_w=52, text_len=40, n_cond=2,
                     steps_total=8, steps_draft=8, dtype="fp32"),
+    # the same two pools with qk RMSNorm + 3-D RoPE
+    "tiny_rope": Workload("tiny_rope", dataclasses.replace(TINY, qk_norm_rope=True), n=2, latent_h=8, latent_w=8,
+                          text_len=8, n_cond=1, steps_total=4, steps_draft=4, dtype="fp32"),
+    "mid_rope": Workload("mid_rope", dataclasses.replace(MID, qk_norm_rope=True), n=3, latent_h=10, latent_w=52,
+                         text_len=40, n_cond=2, steps_total=8, steps_draft=8, dtype="fp32"),
 }
 
 
@@ -113,7 +120,7 @@ def step_masks(name: str, num_blocks: int, k: int) -> Tuple[np.ndarray, np.ndarr
     """Per-step (skip, proxy) uint8 masks over 0-based blocks for the named workload, step k (0-based)."""
     skip = np.zeros(num_blocks, np.uint8)
     proxy = np.zeros(num_blocks, np.uint8)
-    if name == "tiny":
+    if name in ("tiny", "tiny_rope"):
         # skip block 1 on steps 2-3, proxies on step 3
         if k in (2, 3):
             skip[1] = 1
@@ -137,7 +144,7 @@ def step_masks(name: str, num_blocks: int, k: int) -> Tuple[np.ndarray, np.ndarr
         if k == 1:
             skip[1] = 1
             proxy[0] = 1
-    elif name == "mid":
+    elif name in ("mid", "mid_rope"):
         # exercises the empty-cache fallback, warm-up orders 0/1/2, dead and live proxies,
         # skip-over-proxy and proxies over unequally spaced cached steps
         if k >= 2:
@@ -174,6 +181,8 @@ def weight_specs(s: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
             (b + "w1", (F, D)), (b + "b1", (F,)),
             (b + "w2", (D, F)), (b + "b2", (D,)),
         ]
+        if s.qk_norm_rope:
+            specs += [(b + "nq", (D,)), (b + "nk", (D,)), (b + "nqc", (D,)), (b + "nkc", (D,))]
     specs += [("head_w", (P, D)), ("head_b", (P,))]
     return specs
 
@@ -184,7 +193,7 @@ def weight_count(s: ModelShape) -> int:
 
 def make_weights(s: ModelShape, seed_w: int = 1234, threads: int = 8,
                  out: Optional[np.ndarray] = None) -> Tuple[np.ndarray, Dict[str, np.ndarray]]:
-    """Draw every weight ~ N(0, 0.02^2) as float32.
+    """Draw every weight ~ N(0, 0.02^2) as float32 (RMSNorm gains ~ 1 + N(0, 0.02^2)).
 
     Returns (flat, views): ``flat`` is one contiguous float32 array in packing order, ``views`` maps
     each tensor name to a reshaped view into it.
@@ -201,6 +210,8 @@ def make_weights(s: ModelShape, seed_w: int = 1234, threads: int = 8,
         seg = flat[offs[i]:offs[i + 1]]
         rng.standard_normal(out=seg, dtype=np.float32)
         seg *= np.float32(WEIGHT_STD)
+        if specs[i][0].rsplit(".", 1)[-1] in NORM_GAINS:
+            seg += np.float32(1.0)
 
     with ThreadPoolExecutor(max(1, threads)) as ex:
         list(ex.map(fill, range(len(specs))))

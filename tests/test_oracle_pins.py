@@ -474,3 +474,47 @@ def test_residual_mode_makes_every_proxy_live():
     assert [e[3] for e in tr_out] == [0, 0, 0, 1]            # each proxy is overwritten by the next
     assert [e[3] for e in tr_res] == [1, 1, 0, 1]            # the skipped block stays not live
     assert [e[:3] for e in tr_out] == [e[:3] for e in tr_res]
+
+
+# ---------------------------------------------------------------- qk RMSNorm + 3-D RoPE (reading R26)
+
+def test_rms_norm_textbook():
+    x = np.array([[3.0, 4.0]])
+    np.testing.assert_allclose(od_dit.rms_norm(x, np.ones(2), 0.0), x / math.sqrt(12.5), atol=1e-15)
+    rng = np.random.default_rng(11)
+    y, g = rng.standard_normal((5, 16)), rng.standard_normal(16)
+    np.testing.assert_allclose(od_dit.rms_norm(7.5 * y, g, 0.0), od_dit.rms_norm(y, g, 0.0), atol=1e-13)
+    np.testing.assert_allclose(np.mean(od_dit.rms_norm(y, np.ones(16), 0.0) ** 2, axis=-1), 1.0, atol=1e-13)
+
+
+def test_rope_bands_and_hand_example():
+    assert od_dit.rope_bands(128) == (44, 42, 42)
+    assert od_dit.rope_bands(16) == (8, 4, 4)
+    assert od_dit.rope_bands(6) == (2, 2, 2)
+    # dh = 6: one pair per band, frequency 1; token (row 1, column 2) of a 2 x 3 grid is t = 5
+    ang = od_dit.rope_angles(2, 3, 6)
+    np.testing.assert_allclose(ang[5], [0.0, 1.0, 2.0], atol=1e-15)
+    x = np.tile(np.array([[1.0, 0.0, 1.0, 0.0, 1.0, 0.0]]), (6, 1))
+    r = od_dit.apply_rope(x, ang, 1)[5]
+    np.testing.assert_allclose(r, [1, 0, math.cos(1), math.sin(1), math.cos(2), math.sin(2)], atol=1e-15)
+    np.testing.assert_array_equal(od_dit.apply_rope(x, ang, 1)[0], x[0])      # position (0, 0): identity
+
+
+def test_rope_is_a_relative_position_encoding():
+    """Rotations keep pair norms, and the score of a rotated query and key depends only on the offset
+    between their positions: moving both by the same grid shift leaves it unchanged."""
+    rng = np.random.default_rng(12)
+    heads, dh, hp, wp = 2, 16, 6, 7
+    ang = od_dit.rope_angles(hp, wp, dh)
+    q, k = rng.standard_normal((2, heads * dh))
+    rq = od_dit.apply_rope(np.tile(q, (hp * wp, 1)), ang, heads)
+    rk = od_dit.apply_rope(np.tile(k, (hp * wp, 1)), ang, heads)
+    np.testing.assert_allclose(np.linalg.norm(rq.reshape(-1, 2), axis=1),
+                               np.linalg.norm(np.tile(q, hp * wp).reshape(-1, 2), axis=1), atol=1e-12)
+    t = lambda i, j: i * wp + j
+    for (i1, j1), (i2, j2), (di, dj) in [((0, 0), (2, 3), (1, 2)), ((4, 1), (1, 5), (1, 1)), ((2, 2), (2, 2), (3, 4))]:
+        for hd in range(heads):
+            sl = slice(hd * dh, (hd + 1) * dh)
+            a = rq[t(i1, j1), sl] @ rk[t(i2, j2), sl]
+            b = rq[t(i1 + di, j1 + dj), sl] @ rk[t(i2 + di, j2 + dj), sl]
+            assert a == pytest.approx(b, abs=1e-12)
