@@ -73,6 +73,12 @@ typedef struct {
   int32_t max_tokens;      /* largest T = (latent_h/p)(latent_w/p) */
   int32_t max_text_len;    /* largest text_len */
   int32_t max_cond;        /* largest n_cond */
+  int32_t qk_norm_rope;    /* 0 or 1: RMSNorm (eps = ln_eps, per-block gains) on q and k of both attentions
+                              -- the text keys once, when text_kv is made -- and 3-D rotary position
+                              embedding on self-attention: head_dim splits into frame, height and width
+                              bands of dh - 4 (dh/6), 2 (dh/6), 2 (dh/6) dims; a token at (frame 0, row i,
+                              column j) turns pair k of a band of width d by p 10000^(-2k/d), p its
+                              position along the band's axis, pairs (2k, 2k+1) of each head */
 } flashbon_model_config;
 
 /* Per-block activation-cache metadata, host side (one per block).  The cache of a block is a ring of
@@ -181,6 +187,7 @@ size_t flashbon_weight_count(const flashbon_model_config *cfg);
  *   pe_w[D][C p p] pe_b[D] txt_w[D][text_dim] txt_b[D]
  *   per block l: mod[6][D] wq wk wv[D][D each] bq bk bv[D each] wo[D][D] bo[D] wqc[D][D] bqc[D]
  *                wkc wvc[D][D each] bkc bvc[D each] woc[D][D] boc[D] w1[F][D] b1[F] w2[D][F] b2[D]
+ *                and, with qk_norm_rope, the RMSNorm gains nq nk nqc nkc[D each]
  *   head_w[C p p][D] head_b[C p p]
  * Timestep conditioning: f = [cos(1000 t w_j) | sin(1000 t w_j)], w_j = 10000^(-j/(freq/2));
  * e = t_w2 SiLU(t_w1 f + t_b1) + t_b2; m = mod_w SiLU(e) + mod_b; block l uses m + mod_l split as

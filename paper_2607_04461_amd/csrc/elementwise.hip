@@ -194,6 +194,107 @@ hipError_t launch_patchify(ActType t, int n, int zrows, int C, int H, int W, int
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ qk RMSNorm + 3-D rotary table
+// (cos, sin) per (token, pair): token t = i wp + j sits at (frame 0, row i, column j); pair k of the
+// head dim falls in the frame, height or width band (widths dh - 4 (dh/6), 2 (dh/6), 2 (dh/6)) and
+// turns by position * 10000^(-2 k' / width), k' its index inside the band.  Computed in double.
+__global__ void k_rope_table(int T, int wp, int dh, float2 *__restrict__ tab) {
+  const int half = dh / 2;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)T * half) return;
+  const int t = (int)(idx / half), k = (int)(idx % half);
+  const int q6 = dh / 6, fw = dh - 4 * q6, bw = 2 * q6;
+  int pos, kb, width;
+  if (2 * k < fw) { pos = 0; kb = k; width = fw; }
+  else if (2 * k < fw + bw) { pos = t / wp; kb = k - fw / 2; width = bw; }
+  else { pos = t % wp; kb = k - (fw + bw) / 2; width = bw; }
+  const double ang = (double)pos * pow(10000.0, -2.0 * (double)kb / (double)width);
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  tab[idx] = make_float2((float)cs, (float)sn);
+}
+
+hipError_t launch_rope_table(int T, int wp, int dh, float2 *tab, hipStream_t s) {
+  const int64_t n = (int64_t)T * (dh / 2);
+  hipLaunchKernelGGL(k_rope_table, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, T, wp, dh, tab);
+  return hipGetLastError();
+}
+
+template <typename T> __device__ __forceinline__ void load8(const T *p, float v[8]);
+template <> __device__ __forceinline__ void load8<float>(const float *p, float v[8]) {
+  const float4 a = reinterpret_cast<const float4 *>(p)[0], b = reinterpret_cast<const float4 *>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+template <> __device__ __forceinline__ void load8<bf16>(const bf16 *p, float v[8]) {
+  const bf16x8 a = *reinterpret_cast<const bf16x8 *>(p);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (float)a[i];
+}
+template <typename T> __device__ __forceinline__ void store8(T *p, const float v[8]);
+template <> __device__ __forceinline__ void store8<float>(float *p, const float v[8]) {
+  reinterpret_cast<float4 *>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4 *>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <> __device__ __forceinline__ void store8<bf16>(bf16 *p, const float v[8]) {
+  bf16x8 a;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = (bf16)v[i];
+  *reinterpret_cast<bf16x8 *>(p) = a;
+}
+
+// In place on rows of x (stride rs): x <- RMSNorm(x) * gain over D, then, with a table, every pair
+// (2k, 2k+1) of each head rotated by the table entry of (row % T, k).  One wave per row, two passes
+// over the row (statistics, then normalise + rotate), 8 elements per lane per load.
+template <typename T>
+__global__ __launch_bounds__(256) void k_qk_norm(int M, int D, int dh, T *__restrict__ x, int64_t rs,
+                                                 const float *__restrict__ gain, float eps,
+                                                 const float2 *__restrict__ tab, int tokens) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  T *xr = x + row * rs;
+  const int chunks = D >> 3;
+  float ss = 0.f;
+  for (int c = lane; c < chunks; c += 64) {
+    float v[8];
+    load8<T>(xr + 8 * c, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)D + eps);
+  const float2 *tr = tab ? tab + (row % tokens) * (dh >> 1) : nullptr;
+  for (int c = lane; c < chunks; c += 64) {
+    float v[8];
+    load8<T>(xr + 8 * c, v);
+    const float4 g0 = reinterpret_cast<const float4 *>(gain + 8 * c)[0];
+    const float4 g1 = reinterpret_cast<const float4 *>(gain + 8 * c)[1];
+    const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = v[i] * rstd * g[i];
+    if (tr) {
+#pragma unroll
+      for (int pr = 0; pr < 4; ++pr) {
+        const int d = (8 * c + 2 * pr) % dh;
+        const float2 cs = tr[d >> 1];
+        const float a = v[2 * pr], b = v[2 * pr + 1];
+        v[2 * pr] = a * cs.x - b * cs.y;
+        v[2 * pr + 1] = a * cs.y + b * cs.x;
+      }
+    }
+    store8<T>(xr + 8 * c, v);
+  }
+}
+
+hipError_t launch_qk_norm(ActType t, int M, int D, int dh, void *x, int64_t rs, const float *gain, float eps,
+                          const float2 *tab, int tokens, hipStream_t s) {
+  dim3 g((unsigned)((M + 3) / 4)), b(256);
+  if (t == ACT_BF16)
+    hipLaunchKernelGGL(k_qk_norm<bf16>, g, b, 0, s, M, D, dh, (bf16 *)x, rs, gain, eps, tab, tokens);
+  else
+    hipLaunchKernelGGL(k_qk_norm<float>, g, b, 0, s, M, D, dh, (float *)x, rs, gain, eps, tab, tokens);
+  return hipGetLastError();
+}
+
 // --------------------------------------------------------------------------------- timestep path
 __global__ void k_time_features(double t, int half, float *f) {
   int j = blockIdx.x * blockDim.x + threadIdx.x;

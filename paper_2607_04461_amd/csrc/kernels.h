@@ -70,6 +70,13 @@ hipError_t launch_block_mods(int L, int width, const float *m, const float *tabl
 
 hipError_t launch_f32_to_bf16(int64_t count, const float *x, void *y, hipStream_t s);
 
+// qk RMSNorm + 3-D rotary embedding: (cos, sin) table [T][dh/2] for a token grid of width wp; and the
+// in-place normalisation (gain over D, eps) of M rows of x (act, row stride rs), rotated by the table
+// (row % tokens) when tab is not null.  D % 8 == 0.
+hipError_t launch_rope_table(int T, int wp, int dh, float2 *tab, hipStream_t s);
+hipError_t launch_qk_norm(ActType t, int M, int D, int dh, void *x, int64_t rs, const float *gain, float eps,
+                          const float2 *tab, int tokens, hipStream_t s);
+
 // Stochastic update (App. A.1, Eq. 20): z <- z + dt [v + k (z + omt v)] + g eps, eps from Philox4x32-10
 // with key (key0, key1) and counter (element / 4, candidate, step, 0) through Box-Muller.
 struct SdeArgs {

@@ -40,6 +40,7 @@ bool config_ok(const flashbon_model_config *c, std::string *why) {
     return bad("text_dim must be a positive multiple of 8, <= 65536");
   if (c->dtype != FLASHBON_FP32 && c->dtype != FLASHBON_BF16) return bad("dtype must be FP32 or BF16");
   if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return bad("ln_eps must be positive");
+  if (c->qk_norm_rope != 0 && c->qk_norm_rope != 1) return bad("qk_norm_rope must be 0 or 1");
   if (c->max_n < 1 || c->max_tokens < 1 || c->max_text_len < 1 || c->max_cond < 1)
     return bad("max_n, max_tokens, max_text_len, max_cond must be >= 1");
   if ((int64_t)c->max_n * c->max_tokens > (int64_t)1 << 30) return bad("max_n * max_tokens too large");
@@ -68,6 +69,7 @@ Layout make_layout(const flashbon_model_config &c) {
     b.woc = take(D * D); b.boc = take(D);
     b.w1 = take(F * D); b.b1 = take(F);
     b.w2 = take(D * F); b.b2 = take(D);
+    if (c.qk_norm_rope) { b.nq = take(D); b.nk = take(D); b.nqc = take(D); b.nkc = take(D); }
   }
   L.block_stride = c.num_blocks > 1 ? L.blk[1].mod - L.blk[0].mod : 0;
   L.head_w = take(P * D); L.head_b = take(P);
@@ -153,7 +155,8 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
          o_txt = carve(m->act == ACT_BF16 ? txt_rows * m->Dt * a : 0), o_ctx = carve(txt_rows * D * a),
          o_tf = carve(m->fd * 4), o_e1 = carve(D * 4), o_e = carve(D * 4), o_m6 = carve(6 * D * 4),
          o_bm = carve((size_t)m->L * 6 * D * 4), o_hm = carve(2 * D * 4), o_cond = carve(cfg->max_n * 4),
-         o_v = carve(M * P * 4);
+         o_v = carve(M * P * 4),
+         o_rope = carve(cfg->qk_norm_rope ? (size_t)cfg->max_tokens * (D / cfg->heads / 2) * 8 : 0);
   if (hipMalloc(&m->ws, off) != hipSuccess) return cleanup(FLASHBON_ENOMEM, "workspace of " + std::to_string(off) + " bytes");
   m->ws_bytes = off;
   char *w = (char *)m->ws;
@@ -162,6 +165,7 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
   m->tf = (float *)(w + o_tf); m->e1 = (float *)(w + o_e1); m->e = (float *)(w + o_e);
   m->m6 = (float *)(w + o_m6); m->bmods = (float *)(w + o_bm); m->hmod = (float *)(w + o_hm);
   m->d_cond = (int32_t *)(w + o_cond); m->vtok = (float *)(w + o_v);
+  if (cfg->qk_norm_rope) m->rope = (float2 *)(w + o_rope);
 
   if (hipMemcpy(m->w32, host_weights, total * 4, hipMemcpyHostToDevice) != hipSuccess)
     return cleanup(FLASHBON_EHIP, "weight upload");
@@ -348,6 +352,9 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       EpiArgs k;
       k.out = (char *)a->text_kv + (size_t)l * kv_block * asz; k.ldo = 2 * D; k.bias = Bp(m->lay.blk[l].bkvc);
       HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, m->ctx, Wp(m->lay.blk[l].wkvc), k, s); }), "text K/V");
+      if (c.qk_norm_rope)
+        HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_qk_norm(act, NC * Lt, D, m->dh, k.out, 2 * D, Bp(m->lay.blk[l].nkc), c.ln_eps, nullptr, 1, s); }),
+               "text key RMSNorm");
     }
   }
 
@@ -359,6 +366,13 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(2 * D, D, m->w32 + m->lay.hmod_w, Bp(m->lay.hmod_b), m->e, m->hmod, 1, 0, s); }), "head modulation");
   HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_block_mods(L, 6 * D, m->m6, m->w32 + m->lay.blk[0].mod, (int64_t)m->lay.block_stride, m->bmods, s); }),
          "block modulation");
+
+  // rotary table of this latent size (kept while the size does not change)
+  if (c.qk_norm_rope && (m->rope_h != a->latent_h || m->rope_w != a->latent_w)) {
+    HIPCHK(launch_rope_table(T, a->latent_w / p, m->dh, m->rope, s), "rotary table");
+    m->rope_h = a->latent_h;
+    m->rope_w = a->latent_w;
+  }
 
   const int64_t MD = M * D;
   auto dump = [&](int idx) -> flashbon_status {
@@ -409,6 +423,11 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       EpiArgs e; e.out = m->qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
       HIPCHK(timed(m, FLASHBON_SITE_QKV, s, [&] { return launch_linear(act, EPI_STORE, (int)M, 3 * D, D, m->a, Wp(b.wqkv), e, s); }), "qkv projection");
     }
+    if (c.qk_norm_rope) {
+      void *kp = (char *)m->qkv + (size_t)D * asz;
+      HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, m->qkv, 3 * D, Bp(b.nq), c.ln_eps, m->rope, T, s); }), "q RMSNorm + rotary");
+      HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, kp, 3 * D, Bp(b.nk), c.ln_eps, m->rope, T, s); }), "k RMSNorm + rotary");
+    }
     {
       AttnArgs at;
       at.batch = R; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = T;
@@ -427,6 +446,8 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       EpiArgs e; e.out = m->qkv; e.ldo = D; e.bias = Bp(b.bqc);
       HIPCHK(timed(m, FLASHBON_SITE_CROSS_Q, s, [&] { return launch_linear(act, EPI_STORE, (int)M, D, D, m->a, Wp(b.wqc), e, s); }), "cross q projection");
     }
+    if (c.qk_norm_rope)
+      HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, m->qkv, D, Bp(b.nqc), c.ln_eps, nullptr, T, s); }), "cross q RMSNorm");
     {
       const char *kv = (const char *)a->text_kv + (size_t)l * kv_block * asz;
       AttnArgs at;

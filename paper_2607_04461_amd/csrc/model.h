@@ -14,6 +14,7 @@ namespace fb {
 // Element offsets of every tensor in the packed weight blob (same offsets in the fp32 and bf16 copies).
 struct BlockOff {
   size_t mod, wqkv, bqkv, wo, bo, wqc, bqc, wkvc, bkvc, woc, boc, w1, b1, w2, b2;
+  size_t nq = 0, nk = 0, nqc = 0, nkc = 0;   // RMSNorm gains (qk_norm_rope)
 };
 struct Layout {
   size_t t_w1, t_b1, t_w2, t_b2, mod_w, mod_b, hmod_w, hmod_b, pe_w, pe_b, txt_w, txt_b;
@@ -36,6 +37,8 @@ struct Model {
   float *h;              // residual stream [maxM][D] fp32
   void *a, *qkv, *o, *u, *tok, *txt, *ctx;  // act buffers
   float *vtok;           // head output [maxM][C p p] fp32 (stochastic update only)
+  float2 *rope = nullptr;  // (cos, sin) per token and pair [max_tokens][head_dim/2] (qk_norm_rope)
+  int rope_h = -1, rope_w = -1;   // latent size the table was made for
   float *tf, *e1, *e, *m6, *bmods, *hmod;   // timestep path (fp32)
   int32_t *d_cond;
   std::vector<int32_t> last_cond;

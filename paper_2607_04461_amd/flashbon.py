@@ -35,7 +35,7 @@ class ModelConfig(ctypes.Structure):
                                                "latent_channels", "patch", "freq_dim", "text_dim",
                                                "dtype")] + \
                [("ln_eps", ctypes.c_float)] + \
-               [(n, ctypes.c_int32) for n in ("max_n", "max_tokens", "max_text_len", "max_cond")]
+               [(n, ctypes.c_int32) for n in ("max_n", "max_tokens", "max_text_len", "max_cond", "qk_norm_rope")]
 
 
 class CacheMeta(ctypes.Structure):
@@ -162,7 +162,8 @@ def _u8(mask: Optional[Sequence[int]], n: int):
 def make_config(shape, dtype: int, max_n: int, max_tokens: int, max_text_len: int, max_cond: int) -> ModelConfig:
     return ModelConfig(shape.num_blocks, shape.hidden, shape.heads, shape.mlp_hidden,
                        shape.latent_channels, shape.patch, shape.freq_dim, shape.text_dim, dtype,
-                       shape.ln_eps, max_n, max_tokens, max_text_len, max_cond)
+                       shape.ln_eps, max_n, max_tokens, max_text_len, max_cond,
+                       1 if getattr(shape, "qk_norm_rope", False) else 0)
 
 
 def flashbon_weight_count(cfg: ModelConfig) -> int:

@@ -83,7 +83,9 @@ def test_plan_step_rejects_bad_meta():
         fb.flashbon_plan_step(np.zeros(3), np.zeros(3), meta, 0.5)
 
 
-@pytest.mark.parametrize("shape", [synth.TINY, synth.MID, synth.WAN_1_3B, synth.WAN_14B])
+@pytest.mark.parametrize("shape", [synth.TINY, synth.MID, synth.WAN_1_3B, synth.WAN_14B,
+                                   synth.WORKLOADS["mid_rope"].shape,
+                                   synth.dataclasses.replace(synth.WAN_1_3B, qk_norm_rope=True)])
 def test_weight_count_matches_packing(shape):
     cfg = fb.make_config(shape, fb.BF16, 1, 16, 8, 1)
     assert fb.flashbon_weight_count(cfg) == synth.weight_count(shape)
@@ -100,7 +102,8 @@ def test_weight_count_of_published_shapes():
 
 @pytest.mark.parametrize("field,value", [("hidden", 60), ("heads", 5), ("mlp_hidden", 12), ("dtype", 7),
                                          ("mlp_hidden", 65544), ("text_dim", 65544), ("hidden", 6152),
-                                         ("max_n", 0), ("ln_eps", 0.0), ("freq_dim", 6), ("num_blocks", 0)])
+                                         ("max_n", 0), ("ln_eps", 0.0), ("freq_dim", 6), ("num_blocks", 0),
+                                         ("qk_norm_rope", 2)])
 def test_invalid_config_rejected(field, value):
     cfg = fb.make_config(synth.TINY, fb.FP32, 2, 16, 8, 1)
     setattr(cfg, field, value)
