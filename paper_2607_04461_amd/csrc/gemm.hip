@@ -152,8 +152,8 @@ constexpr int BK = 64;
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) & 5) | (((r >> 1) ^ (r >> 3)) & 2); }
 __device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ swz(r)) << 3); }
 
-// Raw buffer resource over `rows` rows of K bf16; loads past the range return zero.  The entry points
-// bound K by 65536, so 256 rows span at most 32 MiB, well inside the 32-bit range.
+// Raw buffer resource over `rows` rows of K bf16; loads whose VGPR offset lies past the range return
+// zero.  The entry points bound K by 65536, so 256 rows span at most 32 MiB, well inside 32 bits.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const bf16 *base, int rows, int K) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16 *>(base), (short)0, rows * K * 2, 0x00020000);
 }
@@ -346,17 +346,21 @@ __global__ __launch_bounds__(512, 1) void k_linear_ilv(int M, int N, int K, cons
   tile_of(blockIdx.x, MT, NT, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
   const int ld_r = tid >> 3, ld_c = tid & 7;
-  // Buffer loads over the workgroup's rows: rows past M (N) fall outside the buffer's range and
-  // read as zero, so one VGPR offset per thread serves every load (row step and K step are scalar).
+  // Buffer loads over the workgroup's rows: rows past M (N) fall outside the buffer's range and read
+  // as zero.  The range check covers the VGPR offset only (not the scalar one), so each row's offset
+  // is a VGPR and only the K position (inside every row) rides in the scalar offset.
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
   const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
-  const int voff = (ld_r * K + ld_c * 8) * 2;
+  static_assert(LA == LW, "A and W share the row offsets");
+  int voff[LA];
+#pragma unroll
+  for (int i = 0; i < LA; ++i) voff[i] = ((ld_r + ROWS * i) * K + ld_c * 8) * 2;
   u32x4 ra[LA], rw[LW];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < LA; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rsA, voff, (ROWS * i * K + k0) * 2, 0);
+    for (int i = 0; i < LA; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rsA, voff[i], k0 * 2, 0);
 #pragma unroll
-    for (int i = 0; i < LW; ++i) rw[i] = __builtin_amdgcn_raw_buffer_load_b128(rsW, voff, (ROWS * i * K + k0) * 2, 0);
+    for (int i = 0; i < LW; ++i) rw[i] = __builtin_amdgcn_raw_buffer_load_b128(rsW, voff[i], k0 * 2, 0);
   };
   auto lstore = [&](bf16 *sA) {
     bf16 *sW = sA + BM * BK;
