@@ -1,16 +1,19 @@
 // Linear layers of the DiT step: C[m][n] = sum_k A[m][k] Wt[n][k] with fused epilogues.
-//   * k_linear_ilv / k_linear_mfma: bf16 operands on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16),
-//     fp32 accumulation.  Workgroup tiles of 256x256 (8 waves of 128x64; explicitly interleaved
-//     schedule when K % 64 == 0) or 128x128 (4 waves of 64x64, loads two K tiles ahead), chosen per
-//     shape; K tiles of 64 staged through double-buffered, XOR-swizzled LDS (one barrier per K
-//     tile); XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) so that every lane ends
-//     up owning four consecutive output columns of one row, which the epilogues store as one vector.
+//   * k_linear_dma / k_linear_mfma: bf16 operands on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16),
+//     fp32 accumulation.  Workgroup tiles of 256x256 (k_linear_dma: 4 waves of 128x128, LDS filled
+//     by buffer loads that write LDS themselves, K % 64 == 0; k_linear_mfma<8,4,2,4>: 8 waves of
+//     128x64 for other K) or 128x128 (4 waves of 64x64, two workgroups per CU), chosen per shape by
+//     a round-count model; K tiles of 64 in double-buffered, XOR-swizzled LDS; XCD-aware grouped tile
+//     order.  Operands are swapped (the weight tile feeds the MFMA "A" side) and the weight rows
+//     permuted so that every lane owns 8 consecutive output columns of one row.  Every kernel
+//     accumulates K in the same order, so an output element does not depend on the tiling.
 //   * k_linear_valu: fp32 (or bf16) operands on the vector ALUs, 64x64 tiles; used by the fp32 mode
 //     and for shapes the MFMA tiling does not take.
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -140,6 +143,197 @@ __device__ __forceinline__ void epilogue8(const EpiArgs &e, int m, int n, const 
   }
 }
 
+// ------------------------------------------------------------- whole-tile epilogue of the MFMA kernels
+// A wave's accumulators acc[i][j] (i over 16-column W fragments, permuted so that fragments 2a and
+// 2a+1 give a lane 8 consecutive columns; j over 16-row A fragments) hold rows mbase + 16 j + fr and
+// columns nbase + 32 a + 8 fq .. + 7.  On gfx9 one counter tracks vector loads and stores in issue
+// order, so a load issued after stores cannot be waited for without waiting for those stores too.
+// The epilogue therefore loads the per-column bias and gate once, before any store, and fetches the
+// residual rows one column group ahead of the stores that use them.  Rows past M and columns past N
+// go through buffer instructions whose offset is pushed out of the resource's range (loads read
+// zero, stores are dropped), so the memory instructions are issued unconditionally.
+namespace epi {
+constexpr uint32_t OUT_OF_RANGE = 0x80000000u;   // past every resource below (each < 2^31 bytes)
+
+// The arguments are wave-uniform (kernel arguments and workgroup/wave indices); readfirstlane states
+// it, so the resource lives in scalar registers rather than behind a per-lane waterfall loop.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
+  const uint64_t p = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+__device__ __forceinline__ f32x4 ld4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
+}
+}  // namespace epi
+
+// Residual update h += gate (acc + bias) of one wave's tile, optional cache write (CM 1: copy of the
+// new row, CM 2: new row minus what the cache held).  The tile is walked in batches of JB 16-row
+// blocks of one column group; PIPE 2: the rows of batch x + 1 are requested before the stores of x.
+template <int WTN, int WTM, int CM, int PIPE, int JB>
+__device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
+                                              int mbase, int nbase, int fr, int fq) {
+  using namespace epi;
+  constexpr int NP = WTN / 2, NJ = WTM / JB, NB = NP * NJ;
+  static_assert(WTM % JB == 0, "row blocks per batch");
+  const int rows = max(0, min(M - mbase, 16 * WTM));
+  const uint32_t bytes = (uint32_t)rows * (uint32_t)e.ldo * 4u;
+  const __amdgpu_buffer_rsrc_t rsO = rsrc((float *)e.out + (int64_t)mbase * e.ldo, bytes);
+  const __amdgpu_buffer_rsrc_t rsC = rsrc(CM ? e.cache + (int64_t)mbase * e.ldo : nullptr, CM ? bytes : 0u);
+  const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
+  const __amdgpu_buffer_rsrc_t rsG = rsrc(e.gate, e.gate ? (uint32_t)N * 4u : 0u);
+  uint32_t c0[NP], c1[NP];   // byte offsets of the two 4-column halves, or out of range
+  f32x4 b[NP][2], g[NP][2];
+#pragma unroll
+  for (int pa = 0; pa < NP; ++pa) {
+    const int n = nbase + 32 * pa + 8 * fq;
+    c0[pa] = n < N ? (uint32_t)n * 4u : OUT_OF_RANGE;
+    c1[pa] = n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE;
+    b[pa][0] = ld4(rsB, c0[pa]);
+    b[pa][1] = ld4(rsB, c1[pa]);
+    if (e.gate) {
+      g[pa][0] = ld4(rsG, c0[pa]);
+      g[pa][1] = ld4(rsG, c1[pa]);
+    } else {
+      g[pa][0] = g[pa][1] = f32x4{1.f, 1.f, 1.f, 1.f};
+    }
+  }
+  const uint32_t ro = (uint32_t)fr * (uint32_t)e.ldo * 4u, rstep = 16u * (uint32_t)e.ldo * 4u;
+  f32x4 h[PIPE][JB][2], c[CM == 2 ? PIPE : 1][JB][2];
+  auto fetch = [&](int x, int buf) {   // batch x: column group x / NJ, row blocks JB (x % NJ) ..
+    const int pa = x / NJ, j0 = JB * (x % NJ);
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj) {
+      const uint32_t r = ro + (uint32_t)(j0 + jj) * rstep;
+      h[buf][jj][0] = ld4(rsO, r + c0[pa]);
+      h[buf][jj][1] = ld4(rsO, r + c1[pa]);
+      if constexpr (CM == 2) {
+        c[buf][jj][0] = ld4(rsC, r + c0[pa]);
+        c[buf][jj][1] = ld4(rsC, r + c1[pa]);
+      }
+    }
+  };
+  if constexpr (PIPE == 2) fetch(0, 0);
+#pragma unroll
+  for (int x = 0; x < NB; ++x) {
+    const int pa = x / NJ, j0 = JB * (x % NJ);
+    const int buf = PIPE == 2 ? (x & 1) : 0;
+    if constexpr (PIPE == 2) {
+      if (x + 1 < NB) fetch(x + 1, (x + 1) & 1);
+    } else {
+      fetch(x, 0);
+    }
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj) {
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const f32x4 a = acc[2 * pa + hf][j0 + jj];
+        f32x4 o = h[buf][jj][hf];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] += g[pa][hf][q] * (a[q] + b[pa][hf][q]);
+        const uint32_t off = ro + (uint32_t)(j0 + jj) * rstep + (hf ? c1[pa] : c0[pa]);
+        st4(rsO, off, o);
+        if constexpr (CM == 1) st4(rsC, off, o);
+        if constexpr (CM == 2) st4(rsC, off, o - c[buf][jj][hf]);
+      }
+    }
+  }
+}
+
+// Store (bf16 or fp32), GELU-and-store, or fp32 store of one wave's tile; bias loaded first, no load
+// between the stores.
+template <int EPI, typename TO, int WTN, int WTM>
+__device__ __forceinline__ void store_tile(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
+                                           int mbase, int nbase, int fr, int fq) {
+  using namespace epi;
+  constexpr int NP = WTN / 2;
+  constexpr bool F32 = EPI == EPI_STORE_F32 || sizeof(TO) == 4;
+  constexpr uint32_t ES = F32 ? 4u : 2u;
+  const int rows = max(0, min(M - mbase, 16 * WTM));
+  const __amdgpu_buffer_rsrc_t rsO = rsrc((char *)e.out + (int64_t)mbase * e.ldo * ES, (uint32_t)rows * (uint32_t)e.ldo * ES);
+  const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
+  uint32_t c0[NP], c1[NP];
+  f32x4 b[NP][2];
+#pragma unroll
+  for (int pa = 0; pa < NP; ++pa) {
+    const int n = nbase + 32 * pa + 8 * fq;
+    c0[pa] = n < N ? (uint32_t)n : OUT_OF_RANGE;
+    c1[pa] = n + 4 < N ? (uint32_t)(n + 4) : OUT_OF_RANGE;
+    b[pa][0] = ld4(rsB, n < N ? (uint32_t)n * 4u : OUT_OF_RANGE);
+    b[pa][1] = ld4(rsB, n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE);
+  }
+#pragma unroll
+  for (int pa = 0; pa < NP; ++pa) {
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+      const uint32_t ro = (uint32_t)(16 * j + fr) * (uint32_t)e.ldo;
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[q] = acc[2 * pa][j][q] + b[pa][0][q];
+        v[4 + q] = acc[2 * pa + 1][j][q] + b[pa][1][q];
+      }
+      if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = gelu_tanh(v[q]);
+      }
+      // an out-of-range column offset stays out of range after the row offset and scaling are added
+      const uint32_t o0 = c0[pa] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c0[pa]) * ES;
+      const uint32_t o1 = c1[pa] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c1[pa]) * ES;
+      if constexpr (F32) {
+        st4(rsO, o0, f32x4{v[0], v[1], v[2], v[3]});
+        st4(rsO, o1, f32x4{v[4], v[5], v[6], v[7]});
+      } else {
+        const bf16x4 w0 = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+        const bf16x4 w1 = {(bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+        if (N % 8 == 0) {   // whole 8-column groups: one 16-byte store
+          const bf16x8 w = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w), rsO, o0, 0, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w0), rsO, o0, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w1), rsO, o1, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// The epilogue of a wave's tile for every epilogue kind.  PIPE: residual rows fetched one column
+// group ahead (2) or per group (1), by the kernel's register budget.
+template <int EPI, typename TO, int WTN, int WTM, int PIPE>
+__device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
+                                              int mbase, int nbase, int fr, int fq) {
+  if constexpr (EPI == EPI_RESIDUAL) {
+    constexpr int JB = PIPE == 2 ? (WTM >= 2 ? 2 : WTM) : (WTM >= 4 ? 4 : WTM);
+    if (!e.cache) residual_tile<WTN, WTM, 0, PIPE, JB>(e, acc, M, N, mbase, nbase, fr, fq);
+    else if (!e.cache_delta) residual_tile<WTN, WTM, 1, PIPE, JB>(e, acc, M, N, mbase, nbase, fr, fq);
+    else residual_tile<WTN, WTM, 2, 1, JB>(e, acc, M, N, mbase, nbase, fr, fq);
+  } else if constexpr (EPI == EPI_EULER) {
+#pragma unroll
+    for (int pa = 0; pa < WTN / 2; ++pa) {
+      const int n = nbase + 32 * pa + 8 * fq;
+#pragma unroll
+      for (int j = 0; j < WTM; ++j) {
+        const int m = mbase + 16 * j + fr;
+        const float v[8] = {acc[2 * pa][j][0], acc[2 * pa][j][1], acc[2 * pa][j][2], acc[2 * pa][j][3],
+                            acc[2 * pa + 1][j][0], acc[2 * pa + 1][j][1], acc[2 * pa + 1][j][2],
+                            acc[2 * pa + 1][j][3]};
+        if (m < M && n < N) {
+          if (n + 8 <= N) epilogue8<EPI, TO>(e, m, n, v);
+          else epilogue4<EPI, TO>(e, m, n, v[0], v[1], v[2], v[3]);   // N % 8 == 4 edge
+        }
+      }
+    }
+  } else {
+    store_tile<EPI, TO, WTN, WTM>(e, acc, M, N, mbase, nbase, fr, fq);
+  }
+}
+
 // ---------------------------------------------------------------------------------- MFMA path
 namespace mf {
 constexpr int BK = 64;
@@ -263,21 +457,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, WGM * WGN <= 4 ? 2 : 1) void k_line
   };
   // acc[i][j] (C^T tile 16x16): lane column = m index (lane & 15), rows = 4 consecutive n.
   auto epilogue = [&](int em0, int en0) {
-#pragma unroll
-    for (int pa = 0; pa < WTN / 2; ++pa) {
-      const int n = en0 + 16 * WTN * wn + 32 * pa + 8 * fq;
-#pragma unroll
-      for (int j = 0; j < WTM; ++j) {
-        const int m = em0 + 16 * WTM * wm + 16 * j + fr;
-        const float v[8] = {acc[2 * pa][j][0], acc[2 * pa][j][1], acc[2 * pa][j][2], acc[2 * pa][j][3],
-                            acc[2 * pa + 1][j][0], acc[2 * pa + 1][j][1], acc[2 * pa + 1][j][2],
-                            acc[2 * pa + 1][j][3]};
-        if (m < M && n < N) {
-          if (n + 8 <= N) epilogue8<EPI, TO>(e, m, n, v);
-          else epilogue4<EPI, TO>(e, m, n, v[0], v[1], v[2], v[3]);   // N % 8 == 4 edge
-        }
-      }
-    }
+    tile_epilogue<EPI, TO, WTN, WTM, 1>(e, acc, M, N, em0 + 16 * WTM * wm, en0 + 16 * WTN * wn, fr, fq);
   };
   auto zero_acc = [&]() {
 #pragma unroll
@@ -325,133 +505,122 @@ __global__ __launch_bounds__(64 * WGM * WGN, WGM * WGN <= 4 ? 2 : 1) void k_line
   }
 }
 
-// ------------------------------------------------------- MFMA path, explicitly interleaved 256x256
-// 8 waves of 128 (m) x 64 (n), K tiles of 64 (K % 64 == 0), register-staged double-buffered LDS.
-// The instruction order inside a K tile is pinned: the next tile's global loads first; substep-1 W
-// fragments; substep 0's MFMAs with substep-1 A fragments read in place between MFMA groups (so
-// each fragment register is refilled right after its last use); half of substep 1; the staged
-// stores and the barrier; the next tile's substep-0 fragments, again refilled in place, overlapping
-// the second half of substep 1.  LDS latency is then hidden behind MFMA groups instead of exposed
-// at each substep, and the barrier drain overlaps 16 MFMAs.
+// ------------------------------------------------- MFMA path, 4 waves of 128x128, LDS filled directly
+// 256x256 workgroup tile, 4 waves in a 2x2 grid, each 128 (m) x 128 (n) with 256 accumulators (one
+// wave per SIMD; the compiler holds them in AGPRs); K tiles of 64 (K % 64 == 0, K >= 128).  Global -> LDS by buffer loads that write
+// LDS themselves (no staging registers, no ds_write): one load instruction fills 1 KB = 8 rows of the
+// swizzled layout, lane l writing 16-byte slot l, so each lane fetches the chunk that belongs in its
+// slot.  Two LDS stages.  Per K tile: substep 0's MFMAs while substep 1's fragments are read; wait
+// for the next tile's loads and barrier; the loads of the tile after next go into the stage just
+// finished; substep 1's MFMAs while the next tile's substep-0 fragments are read.
 template <int EPI, typename TO>
-__global__ __launch_bounds__(512, 1) void k_linear_ilv(int M, int N, int K, const bf16 *__restrict__ A,
+__global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, const bf16 *__restrict__ A,
                                                 const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT) {
   using namespace mf;
-  constexpr int BM = 256, BN = 256, WTM = 8, WTN = 4, ROWS = 64, LA = 4, LW = 4;
+  constexpr int BM = 256, BN = 256, WT = 8;
   constexpr int STAGE = (BM + BN) * BK;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
   int mt, nt;
   tile_of(blockIdx.x, MT, NT, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
-  const int ld_r = tid >> 3, ld_c = tid & 7;
-  // Buffer loads over the workgroup's rows: rows past M (N) fall outside the buffer's range and read
-  // as zero.  The range check covers the VGPR offset only (not the scalar one), so each row's offset
-  // is a VGPR and only the K position (inside every row) rides in the scalar offset.
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
   const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
-  static_assert(LA == LW, "A and W share the row offsets");
-  int voff[LA];
+  // load instruction i of this wave fills rows 64 wave + 8 i .. + 7; lane l -> row + (l >> 3), slot l & 7
+  int voff[8];
 #pragma unroll
-  for (int i = 0; i < LA; ++i) voff[i] = ((ld_r + ROWS * i) * K + ld_c * 8) * 2;
-  u32x4 ra[LA], rw[LW];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rsA, voff[i], k0 * 2, 0);
-#pragma unroll
-    for (int i = 0; i < LW; ++i) rw[i] = __builtin_amdgcn_raw_buffer_load_b128(rsW, voff[i], k0 * 2, 0);
-  };
-  auto lstore = [&](bf16 *sA) {
-    bf16 *sW = sA + BM * BK;
-#pragma unroll
-    for (int i = 0; i < LA; ++i) *reinterpret_cast<u32x4 *>(&sA[lds_off(ld_r + ROWS * i, ld_c)]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < LW; ++i) *reinterpret_cast<u32x4 *>(&sW[lds_off(ld_r + ROWS * i, ld_c)]) = rw[i];
-  };
-  f32x4 acc[WTN][WTM];
-#pragma unroll
-  for (int i = 0; i < WTN; ++i)
-#pragma unroll
-    for (int j = 0; j < WTM; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
-  const int fr = lane & 15, fq = lane >> 4;
-  // MFMA tile i of this wave takes W rows 32 (i/2) + 8 (fr/4) + 4 (i%2) + fr%4 (fr = lane & 15), so
-  // the C^T rows a lane ends up with for tiles 2a and 2a+1 are 8 consecutive output columns
-  const int rowA = 16 * WTM * wm + fr;
-  auto w_row = [&](int i) { return 16 * WTN * wn + 32 * (i >> 1) + 8 * (fr >> 2) + 4 * (i & 1) + (fr & 3); };
-  bf16x8 fw0[WTN], fw1[WTN], fa[WTM];
-  auto rd_w = [&](const bf16 *st, int ks, bf16x8 *fw) {
-    const bf16 *sW = st + BM * BK;
-#pragma unroll
-    for (int i = 0; i < WTN; ++i) fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[lds_off(w_row(i), fq + 4 * ks)]);
-  };
-  auto rd_a = [&](const bf16 *st, int ks, int j) {
-    fa[j] = *reinterpret_cast<const bf16x8 *>(&st[lds_off(rowA + 16 * j, fq + 4 * ks)]);
-  };
-  auto mm = [&](const bf16x8 *fw, int j) {
-#pragma unroll
-    for (int i = 0; i < WTN; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
-  };
-  const int KT = K / BK;
-  gload(0);
-  lstore(smem);
-  __syncthreads();
-  rd_w(smem, 0, fw0);
-#pragma unroll
-  for (int j = 0; j < WTM; ++j) rd_a(smem, 0, j);
-  for (int kt = 0; kt < KT; ++kt) {
-    const bool more = kt + 1 < KT;
-    const bf16 *cur = smem + (kt & 1) * STAGE;
-    bf16 *nxt = smem + ((kt + 1) & 1) * STAGE;
-    if (more) gload((kt + 1) * BK);
-    rd_w(cur, 1, fw1);
-    __builtin_amdgcn_sched_barrier(0);
-    // substep 0; substep-1 A fragments replace substep-0 ones in place
-#pragma unroll
-    for (int j = 0; j < WTM; ++j) {
-      mm(fw0, j);
-      rd_a(cur, 1, j);
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    // substep 1, first half
-#pragma unroll
-    for (int j = 0; j < WTM / 2; ++j) mm(fw1, j);
-    __builtin_amdgcn_sched_barrier(0);
-    if (more) lstore(nxt);
-    __syncthreads();
-    if (more) {
-      rd_w(nxt, 0, fw0);
-#pragma unroll
-      for (int j = 0; j < WTM / 2; ++j) rd_a(nxt, 0, j);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    // substep 1, second half; next tile's A fragments replace these in place
-#pragma unroll
-    for (int j = WTM / 2; j < WTM; ++j) {
-      mm(fw1, j);
-      if (more) rd_a(nxt, 0, j);
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+  for (int i = 0; i < 8; ++i) {
+    const int r = 64 * wave + 8 * i + (lane >> 3);
+    voff[i] = (r * K + (((lane & 7) ^ swz(r)) << 3)) * 2;
   }
+  // load x (0..15) of K tile kt into stage st: x < 8 -> A rows 64 wave + 8 x, else W rows 64 wave + 8 (x - 8)
+  auto dma_one = [&](int kt, int st, int x) {
+    const int soff = kt * BK * 2;
+    bf16 *sA = smem + st * STAGE;
+    if (x < 8)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (__attribute__((address_space(3))) void *)(sA + (64 * wave + 8 * x) * BK),
+                                               16, voff[x], soff, 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (__attribute__((address_space(3))) void *)(sA + BM * BK + (64 * wave + 8 * (x - 8)) * BK),
+                                               16, voff[x - 8], soff, 0, 0);
+  };
+  auto dma_all = [&](int kt, int st) {
 #pragma unroll
-  for (int pa = 0; pa < WTN / 2; ++pa) {
-    const int n = n0 + 16 * WTN * wn + 32 * pa + 8 * fq;
+    for (int x = 0; x < 16; ++x) dma_one(kt, st, x);
+  };
+  f32x4 acc[WT][WT];
 #pragma unroll
-    for (int j = 0; j < WTM; ++j) {
-      const int m = m0 + 16 * WTM * wm + 16 * j + fr;
-      const float v[8] = {acc[2 * pa][j][0], acc[2 * pa][j][1], acc[2 * pa][j][2], acc[2 * pa][j][3],
-                          acc[2 * pa + 1][j][0], acc[2 * pa + 1][j][1], acc[2 * pa + 1][j][2],
-                          acc[2 * pa + 1][j][3]};
-      if (m < M && n < N) {
-        if (n + 8 <= N) epilogue8<EPI, TO>(e, m, n, v);
-        else epilogue4<EPI, TO>(e, m, n, v[0], v[1], v[2], v[3]);   // N % 8 == 4 edge
+  for (int i = 0; i < WT; ++i)
+#pragma unroll
+    for (int j = 0; j < WT; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+  const int fr = lane & 15, fq = lane >> 4;
+  // Fragment x of substep ks: x < 8 -> W fragment i = x, rows 128 wn + 32 (i/2) + 8 (fr/4) + 4 (i%2) +
+  // fr%4 (a lane's outputs of tiles 2a, 2a+1 are then 8 consecutive columns); x >= 8 -> A fragment
+  // j = x - 8, rows 128 wm + 16 j + fr.  Rows 32 apart share the swizzle, so each fragment is one of
+  // four per-lane byte offsets ([ks][parity], W and A) plus an immediate.
+  uint32_t offW[2][2], offA[2][2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      offW[ks][q] = 2 * (BM * BK + lds_off(128 * wn + 8 * (fr >> 2) + 4 * q + (fr & 3), fq + 4 * ks));
+      offA[ks][q] = 2 * lds_off(128 * wm + 16 * q + fr, fq + 4 * ks);
+    }
+  const char *lds = reinterpret_cast<const char *>(smem);
+  bf16x8 fw0[WT], fa0[WT], fw1[WT], fa1[WT];
+  auto rd = [&](int st, int ks, bf16x8 *fw, bf16x8 *fa, int x) {
+    const char *base = lds + st * (STAGE * 2);
+    if (x < WT) fw[x] = *reinterpret_cast<const bf16x8 *>(base + offW[ks][x & 1] + 4096 * (x >> 1));
+    else fa[x - WT] = *reinterpret_cast<const bf16x8 *>(base + offA[ks][x & 1] + 4096 * ((x - WT) >> 1));
+  };
+  // 64 MFMAs of one substep, the 16 fragment reads of the next substep (READ) and the 16 loads of a
+  // later tile (LOAD) spread over them; fences pin the interleaving.  The MFMAs are builtins so the
+  // compiler sees their latency and covers it wherever it copies an accumulator.
+  auto substep = [&](auto READ, auto LOAD, const bf16x8 *fw, const bf16x8 *fa, int nst, int nks, bf16x8 *nfw,
+                     bf16x8 *nfa, int dma_kt, int dma_st) {
+#pragma unroll
+    for (int j = 0; j < WT; ++j) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int i = 4 * h; i < 4 * h + 4; ++i)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
+        if constexpr (decltype(READ)::value) rd(nst, nks, nfw, nfa, 2 * j + h);
+        if constexpr (decltype(LOAD)::value) dma_one(dma_kt, dma_st, 2 * j + h);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  const int KT = K / BK;   // >= 2
+  dma_all(0, 0);
+  dma_all(1, 1);
+  // s_waitcnt encodings (gfx9): vmcnt low bits 3:0, high bits 15:14; expcnt 6:4 and lgkmcnt 11:8 left open
+  __builtin_amdgcn_s_waitcnt(0x4F70);   // vmcnt(16): tile 0 has landed
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < 2 * WT; ++x) rd(0, 0, fw0, fa0, x);
+  // tile kt sits in stage kt & 1; tile kt+1 is in flight into the other stage
+  int kt = 0;
+  for (; kt + 2 < KT; ++kt) {
+    substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+    // tile kt+1 has landed (the LDS-writing loads count in vmcnt, which the barrier alone does not
+    // wait for); after the barrier nobody reads stage kt & 1 any more
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __syncthreads();
+    substep(T_{}, T_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, kt + 2, kt & 1);
   }
+  substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the last tile has landed
+  __syncthreads();
+  substep(T_{}, F_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, 0, 0);
+  ++kt;
+  substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+  substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
+  tile_epilogue<EPI, TO, WT, WT, 2>(e, acc, M, N, m0 + 128 * wm, n0 + 128 * wn, fr, fq);
 }
 // ---------------------------------------------------------------------------------- VALU path
 template <typename TI, int EPI, typename TO>
@@ -506,8 +675,20 @@ enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT };
 static int cu_count();
 
 static TilePlan pick_tiles(int M, int N, int K, int *split_rows) {
-  const char *force = getenv("FLASHBON_LINEAR_TILE");  // "256x256" or "128x128": tests and tuning
-  if (force) return strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL;
+  // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", or "split:<rows>" (rows a multiple
+  // of 256 with 0 < rows < M: the first rows on 256x256 tiles, the rest on 128x128 tiles)
+  const char *force = getenv("FLASHBON_LINEAR_TILE");
+  if (force) {
+    if (!strncmp(force, "split:", 6)) {
+      const int rows = atoi(force + 6);
+      if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) {
+        *split_rows = rows;
+        return PLAN_SPLIT;
+      }
+      return PLAN_BIG;
+    }
+    return strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL;
+  }
   constexpr double kSmallRound = 0.64;
   const int cus = cu_count();
   const int64_t NT = (N + 255) / 256, T = (int64_t)((M + 255) / 256) * NT, NT2 = (N + 127) / 128;
@@ -545,10 +726,10 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
 }
 
 template <int EPI>
-static hipError_t launch_ilv(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
+static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
                              hipStream_t s) {
   const size_t lds = (size_t)2 * (256 + 256) * mf::BK * sizeof(bf16);
-  auto kern = k_linear_ilv<EPI, bf16>;
+  auto kern = k_linear_dma<EPI, bf16>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -556,7 +737,7 @@ static hipError_t launch_ilv(int M, int N, int K, const void *A, const void *Wt,
     attr_set = true;
   }
   const int MT = (M + 255) / 256, NT = (N + 255) / 256;
-  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(512), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
+  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(256), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
                      MT, NT);
   return hipGetLastError();
 }
@@ -584,6 +765,16 @@ static EpiArgs rows_from(const EpiArgs &e, int m) {
   return r;
 }
 
+// 256x256 tiles: the 4-wave kernel with LDS-writing loads when it takes the shape, else the generic
+// 8-wave kernel (K % 64 != 0 or K < 128, and the latent scatter, which stays on 2 waves per SIMD).
+template <int EPI>
+static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s) {
+  if constexpr (EPI != EPI_EULER) {
+    if (K % mf::BK == 0 && K >= 2 * mf::BK) return launch_dma<EPI>(M, N, K, A, Wt, e, s);
+  }
+  return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
+}
+
 template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
@@ -592,9 +783,8 @@ static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, cons
     TilePlan plan = pick_tiles(M, N, K, &rows);
     if (plan == PLAN_SPLIT && EPI == EPI_EULER) plan = PLAN_BIG;   // the latent scatter needs whole rows
     if (plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
-    if (K % mf::BK) return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
-    if (plan == PLAN_BIG) return launch_ilv<EPI>(M, N, K, A, Wt, e, s);
-    hipError_t err = launch_ilv<EPI>(rows, N, K, A, Wt, e, s);
+    if (plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s);
+    hipError_t err = launch_big<EPI>(rows, N, K, A, Wt, e, s);
     if (err != hipSuccess) return err;
     return launch_mfma<4, 4, 2, 2, EPI, 2>(M - rows, N, K, (const bf16 *)A + (size_t)rows * K, Wt,
                                            rows_from<EPI>(e, rows), s);

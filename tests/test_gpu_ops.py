@@ -83,12 +83,15 @@ def test_linear_small(dtype, M, N, K, epi):
     assert rel_l2(got, ref) <= tol
 
 
-@pytest.mark.parametrize("tile", ["256x256", "128x128"])
-@pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192)])
+@pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256"])
+@pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
+                                   (520, 776, 1024)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
 def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
-    """Every MFMA kernel (forced tiling; the 256x256 one is the interleaved kernel when K % 64 == 0)
-    on ragged M, N and K tails, against the oracle."""
+    """Every MFMA tiling (forced: "256x256" is the 4-wave kernel with LDS-writing loads when K % 64 == 0
+    and K >= 128, else the 8-wave kernel; "split:256" puts rows 0..255 on 256x256 tiles and the rest
+    on 128x128 tiles, when M > 256 and K % 64 == 0) on ragged M, N and K tails, against the oracle.
+    The residual case also writes the cache copy."""
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
     F = fb()
     A = _operand((M, K), 71, "bf16")
@@ -103,9 +106,12 @@ def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
         h0 = synth.random_matrix((M, N), 74)
         gate = synth.random_matrix((N,), 75)
         out = _dev(h0, "fp32")
+        cache = torch.full((M, N), 7.0, device="cuda", dtype=torch.float32)
         F.flashbon_op_linear(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"),
-                             F.EPI_RESIDUAL, out, _dev(gate, "fp32"))
+                             F.EPI_RESIDUAL, out, _dev(gate, "fp32"), cache)
         ref, tol = h0 + gate * ref, 2e-6
+        torch.cuda.synchronize()
+        assert torch.equal(cache, out)
     torch.cuda.synchronize()
     assert rel_l2(out.float().cpu().numpy(), ref) <= tol
 
