@@ -264,9 +264,10 @@ def main():
         "mfma_frac_end_to_end": round(tflops / PEAK_BF16_TFLOPS, 4),
         "algorithmic_tflop_per_step": round(flops / 1e12, 3),
         "roofline": {
-            "kernel": ("MLP up-projection + GELU (M=%d N=%d K=%d): k_linear_ilv<EPI_GELU> on the rows that fill "
-                       "whole rounds of 256x256 tiles + k_linear_mfma<128x128, EPI_GELU> on the remaining rows, "
-                       "timed together per call" % (M, wl.shape.mlp_hidden, wl.shape.hidden)),
+            "kernel": ("MLP up-projection + GELU (M=%d N=%d K=%d): k_linear_dma<EPI_GELU> (256x256 tiles, "
+                       "LDS-writing loads) on the rows that fill whole rounds of tiles + k_linear_mfma<128x128, "
+                       "EPI_GELU> on the remaining rows, timed together per call"
+                       % (M, wl.shape.mlp_hidden, wl.shape.hidden)),
             "bound": "mfma", "achieved": round(up_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",

@@ -309,7 +309,7 @@ template <int EPI, typename TO, int WTN, int WTM, int PIPE>
 __device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
                                               int mbase, int nbase, int fr, int fq) {
   if constexpr (EPI == EPI_RESIDUAL) {
-    constexpr int JB = PIPE == 2 ? (WTM >= 2 ? 2 : WTM) : (WTM >= 4 ? 4 : WTM);
+    constexpr int JB = PIPE == 2 ? (WTM % 2 == 0 ? 2 : 1) : (WTM % 4 == 0 ? 4 : (WTM % 2 == 0 ? 2 : 1));
     if (!e.cache) residual_tile<WTN, WTM, 0, PIPE, JB>(e, acc, M, N, mbase, nbase, fr, fq);
     else if (!e.cache_delta) residual_tile<WTN, WTM, 1, PIPE, JB>(e, acc, M, N, mbase, nbase, fr, fq);
     else residual_tile<WTN, WTM, 2, 1, JB>(e, acc, M, N, mbase, nbase, fr, fq);
@@ -505,20 +505,31 @@ __global__ __launch_bounds__(64 * WGM * WGN, WGM * WGN <= 4 ? 2 : 1) void k_line
   }
 }
 
-// ------------------------------------------------- MFMA path, 4 waves of 128x128, LDS filled directly
-// 256x256 workgroup tile, 4 waves in a 2x2 grid, each 128 (m) x 128 (n) with 256 accumulators (one
-// wave per SIMD; the compiler holds them in AGPRs); K tiles of 64 (K % 64 == 0, K >= 128).  Global -> LDS by buffer loads that write
-// LDS themselves (no staging registers, no ds_write): one load instruction fills 1 KB = 8 rows of the
-// swizzled layout, lane l writing 16-byte slot l, so each lane fetches the chunk that belongs in its
-// slot.  Two LDS stages.  Per K tile: substep 0's MFMAs while substep 1's fragments are read; wait
-// for the next tile's loads and barrier; the loads of the tile after next go into the stage just
-// finished; substep 1's MFMAs while the next tile's substep-0 fragments are read.
-template <int EPI, typename TO>
+// ------------------------------------------------- MFMA path, 4 waves, LDS filled directly
+// (32 WTA)x256 workgroup tile (WTA = 4..8; the plan uses 8 and 7), 4 waves in a 2x2 grid, each (16 WTA) (m) x 128 (n) with up
+// to 256 accumulators (one wave per SIMD; the compiler holds them in AGPRs); K tiles of 64 (K % 64 ==
+// 0, K >= 128).  The tile height lets a launch fill whole rounds of the chip (at M = 24960, N = 1536:
+// 672 tiles of 224 rows fill three rounds, where 588 tiles of 256 rows leave the third 30% full).
+// Global -> LDS by buffer loads that write LDS themselves (no staging registers, no ds_write): one
+// load instruction fills 1 KB = 8 rows of the swizzled layout, lane l writing 16-byte slot l, so each
+// lane fetches the chunk that belongs in its slot.  Two LDS stages.  Per K tile: substep 0's MFMAs
+// while substep 1's fragments are read; wait for the next tile's loads and barrier; the loads of the
+// tile after next go into the stage just finished; substep 1's MFMAs while the next tile's substep-0
+// fragments are read.
+__host__ __device__ constexpr int vmcnt_imm(int n) {   // s_waitcnt vmcnt(n), expcnt and lgkmcnt open
+  return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00;
+}
+
+template <int EPI, typename TO, int WTA>
 __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, const bf16 *__restrict__ A,
                                                 const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT) {
   using namespace mf;
-  constexpr int BM = 256, BN = 256, WT = 8;
+  static_assert(WTA >= 4 && WTA <= 8, "tile height 128..256");
+  constexpr int BM = 32 * WTA, BN = 256, WT = 8;
   constexpr int STAGE = (BM + BN) * BK;
+  constexpr int NL = WTA + 8;      // load instructions per wave per K tile (A rows, then W rows)
+  constexpr int NR = WTA + 8;      // fragment reads per wave per substep (W, then A)
+  constexpr int NS = 2 * WTA;      // MFMA groups of 4 per substep, the slots the reads and loads ride in
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -528,37 +539,42 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
   const int m0 = mt * BM, n0 = nt * BN;
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
   const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
-  // load instruction i of this wave fills rows 64 wave + 8 i .. + 7; lane l -> row + (l >> 3), slot l & 7
-  int voff[8];
+  // load x of this wave: x < WTA -> A rows 8 WTA wave + 8 x .. + 7, else W rows 64 wave + 8 (x - WTA)
+  // .. + 7; lane l -> row + (l >> 3), slot l & 7
+  int voffA[8], voffW[8];   // voffA: first WTA used
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = 64 * wave + 8 * i + (lane >> 3);
-    voff[i] = (r * K + (((lane & 7) ^ swz(r)) << 3)) * 2;
+  for (int x = 0; x < WTA; ++x) {
+    const int r = 8 * WTA * wave + 8 * x + (lane >> 3);
+    voffA[x] = (r * K + (((lane & 7) ^ swz(r)) << 3)) * 2;
   }
-  // load x (0..15) of K tile kt into stage st: x < 8 -> A rows 64 wave + 8 x, else W rows 64 wave + 8 (x - 8)
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const int r = 64 * wave + 8 * x + (lane >> 3);
+    voffW[x] = (r * K + (((lane & 7) ^ swz(r)) << 3)) * 2;
+  }
   auto dma_one = [&](int kt, int st, int x) {
     const int soff = kt * BK * 2;
     bf16 *sA = smem + st * STAGE;
-    if (x < 8)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (__attribute__((address_space(3))) void *)(sA + (64 * wave + 8 * x) * BK),
-                                               16, voff[x], soff, 0, 0);
+    if (x < WTA)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (__attribute__((address_space(3))) void *)(sA + (8 * WTA * wave + 8 * x) * BK),
+                                               16, voffA[x], soff, 0, 0);
     else
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (__attribute__((address_space(3))) void *)(sA + BM * BK + (64 * wave + 8 * (x - 8)) * BK),
-                                               16, voff[x - 8], soff, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (__attribute__((address_space(3))) void *)(sA + BM * BK + (64 * wave + 8 * (x - WTA)) * BK),
+                                               16, voffW[x - WTA], soff, 0, 0);
   };
   auto dma_all = [&](int kt, int st) {
 #pragma unroll
-    for (int x = 0; x < 16; ++x) dma_one(kt, st, x);
+    for (int x = 0; x < NL; ++x) dma_one(kt, st, x);
   };
-  f32x4 acc[WT][WT];
+  f32x4 acc[WT][WTA];
 #pragma unroll
   for (int i = 0; i < WT; ++i)
 #pragma unroll
-    for (int j = 0; j < WT; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+    for (int j = 0; j < WTA; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
   const int fr = lane & 15, fq = lane >> 4;
   // Fragment x of substep ks: x < 8 -> W fragment i = x, rows 128 wn + 32 (i/2) + 8 (fr/4) + 4 (i%2) +
   // fr%4 (a lane's outputs of tiles 2a, 2a+1 are then 8 consecutive columns); x >= 8 -> A fragment
-  // j = x - 8, rows 128 wm + 16 j + fr.  Rows 32 apart share the swizzle, so each fragment is one of
+  // j = x - 8, rows 16 WTA wm + 16 j + fr.  Rows 32 apart share the swizzle, so each fragment is one of
   // four per-lane byte offsets ([ks][parity], W and A) plus an immediate.
   uint32_t offW[2][2], offA[2][2];
 #pragma unroll
@@ -566,29 +582,37 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       offW[ks][q] = 2 * (BM * BK + lds_off(128 * wn + 8 * (fr >> 2) + 4 * q + (fr & 3), fq + 4 * ks));
-      offA[ks][q] = 2 * lds_off(128 * wm + 16 * q + fr, fq + 4 * ks);
+      offA[ks][q] = 2 * lds_off(16 * WTA * wm + 16 * q + fr, fq + 4 * ks);
     }
   const char *lds = reinterpret_cast<const char *>(smem);
-  bf16x8 fw0[WT], fa0[WT], fw1[WT], fa1[WT];
+  bf16x8 fw0[WT], fa0[WTA], fw1[WT], fa1[WTA];
   auto rd = [&](int st, int ks, bf16x8 *fw, bf16x8 *fa, int x) {
     const char *base = lds + st * (STAGE * 2);
     if (x < WT) fw[x] = *reinterpret_cast<const bf16x8 *>(base + offW[ks][x & 1] + 4096 * (x >> 1));
     else fa[x - WT] = *reinterpret_cast<const bf16x8 *>(base + offA[ks][x & 1] + 4096 * ((x - WT) >> 1));
   };
-  // 64 MFMAs of one substep, the 16 fragment reads of the next substep (READ) and the 16 loads of a
-  // later tile (LOAD) spread over them; fences pin the interleaving.  The MFMAs are builtins so the
-  // compiler sees their latency and covers it wherever it copies an accumulator.
+  // The 8 WTA MFMAs of one substep in NS groups of 4, the NR fragment reads of the next substep (READ)
+  // and the NL loads of a later tile (LOAD) spread over the groups; fences pin the interleaving.  The
+  // MFMAs are builtins so the compiler sees their latency and covers it wherever it copies an
+  // accumulator.
   auto substep = [&](auto READ, auto LOAD, const bf16x8 *fw, const bf16x8 *fa, int nst, int nks, bf16x8 *nfw,
                      bf16x8 *nfa, int dma_kt, int dma_st) {
 #pragma unroll
-    for (int j = 0; j < WT; ++j) {
+    for (int j = 0; j < WTA; ++j) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
+        const int slot = 2 * j + h;
 #pragma unroll
         for (int i = 4 * h; i < 4 * h + 4; ++i)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
-        if constexpr (decltype(READ)::value) rd(nst, nks, nfw, nfa, 2 * j + h);
-        if constexpr (decltype(LOAD)::value) dma_one(dma_kt, dma_st, 2 * j + h);
+        if constexpr (decltype(READ)::value) {
+#pragma unroll
+          for (int x = slot * NR / NS; x < (slot + 1) * NR / NS; ++x) rd(nst, nks, nfw, nfa, x);
+        }
+        if constexpr (decltype(LOAD)::value) {
+#pragma unroll
+          for (int x = slot * NL / NS; x < (slot + 1) * NL / NS; ++x) dma_one(dma_kt, dma_st, x);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -598,29 +622,28 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
   const int KT = K / BK;   // >= 2
   dma_all(0, 0);
   dma_all(1, 1);
-  // s_waitcnt encodings (gfx9): vmcnt low bits 3:0, high bits 15:14; expcnt 6:4 and lgkmcnt 11:8 left open
-  __builtin_amdgcn_s_waitcnt(0x4F70);   // vmcnt(16): tile 0 has landed
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(NL));   // tile 0 has landed (tile 1's NL loads may be in flight)
   __syncthreads();
 #pragma unroll
-  for (int x = 0; x < 2 * WT; ++x) rd(0, 0, fw0, fa0, x);
+  for (int x = 0; x < NR; ++x) rd(0, 0, fw0, fa0, x);
   // tile kt sits in stage kt & 1; tile kt+1 is in flight into the other stage
   int kt = 0;
   for (; kt + 2 < KT; ++kt) {
     substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
     // tile kt+1 has landed (the LDS-writing loads count in vmcnt, which the barrier alone does not
     // wait for); after the barrier nobody reads stage kt & 1 any more
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __syncthreads();
     substep(T_{}, T_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, kt + 2, kt & 1);
   }
   substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the last tile has landed
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the last tile has landed
   __syncthreads();
   substep(T_{}, F_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, 0, 0);
   ++kt;
   substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
   substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
-  tile_epilogue<EPI, TO, WT, WT, 2>(e, acc, M, N, m0 + 128 * wm, n0 + 128 * wn, fr, fq);
+  tile_epilogue<EPI, TO, WT, WTA, 2>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 128 * wn, fr, fq);
 }
 // ---------------------------------------------------------------------------------- VALU path
 template <typename TI, int EPI, typename TO>
@@ -672,38 +695,53 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
 // that fill complete rounds plus the remaining rows as 128x128 tiles (a second launch), which
 // trims a last round that would leave most CUs idle.
 enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT };
+struct TileChoice {
+  TilePlan plan;
+  int wta;    // PLAN_BIG with the 4-wave kernel: tile height 32 wta
+  int rows;   // PLAN_SPLIT: rows on 256x256 tiles
+};
 static int cu_count();
 
-static TilePlan pick_tiles(int M, int N, int K, int *split_rows) {
-  // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", or "split:<rows>" (rows a multiple
-  // of 256 with 0 < rows < M: the first rows on 256x256 tiles, the rest on 128x128 tiles)
+// Round-count model, in units of one K step of a 256x256 round: a launch takes ceil(tiles / CUs)
+// rounds; a round of 256x256 tiles costs K + kFix (kFix: per-tile prologue and epilogue), of 224x256
+// tiles k224 K + kFix, of 128x128 tiles (two per CU) kSmallA K + kSmallFix.  Fitted to the 1.3B-shaped
+// projections at M = 24960 (K = 1536 and 8960).  Picks the cheapest of: one launch of 256- or 224-row
+// tiles, one launch of 128x128 tiles, or 256x256 tiles on the rows that fill whole rounds plus 128x128
+// tiles on the rest.
+static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
+  // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", "bm:224" (4-wave kernel with
+  // 224-row tiles), or "split:<rows>" (rows a multiple of 256 with 0 < rows < M: the first rows on
+  // 256x256 tiles, the rest on 128x128 tiles)
   const char *force = getenv("FLASHBON_LINEAR_TILE");
   if (force) {
     if (!strncmp(force, "split:", 6)) {
       const int rows = atoi(force + 6);
-      if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) {
-        *split_rows = rows;
-        return PLAN_SPLIT;
-      }
-      return PLAN_BIG;
+      if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) return {PLAN_SPLIT, 8, rows};
+      return {PLAN_BIG, 8, 0};
     }
-    return strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL;
+    if (!strcmp(force, "bm:224")) return {PLAN_BIG, dma_ok ? 7 : 8, 0};
+    return {strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL, 8, 0};
   }
-  constexpr double kSmallRound = 0.64;
+  constexpr double kFix = 358.0, k224 = 0.92, kSmallA = 0.704, kSmallFix = 604.0;
   const int cus = cu_count();
+  auto rounds = [&](int64_t tiles, int per_cu) { return (double)((tiles + per_cu * cus - 1) / (per_cu * cus)); };
   const int64_t NT = (N + 255) / 256, T = (int64_t)((M + 255) / 256) * NT, NT2 = (N + 127) / 128;
-  const double t_big = (double)((T + cus - 1) / cus);
-  const double t_small = (double)((((M + 127) / 128) * NT2 + 2 * cus - 1) / (2 * cus)) * kSmallRound;
-  double t_split = 1e30;
+  const double big = K + kFix, small = kSmallA * K + kSmallFix;
+  TileChoice best = {PLAN_BIG, 8, 0};
+  double t_best = rounds(T, 1) * big;
+  if (dma_ok) {
+    const double t = rounds((int64_t)((M + 223) / 224) * NT, 1) * (k224 * K + kFix);
+    if (t < t_best) { t_best = t; best = {PLAN_BIG, 7, 0}; }
+  }
+  const double t_small = rounds((int64_t)((M + 127) / 128) * NT2, 2) * small;
+  if (t_small < t_best) { t_best = t_small; best = {PLAN_SMALL, 8, 0}; }
   const int64_t mt_big = (T - T % cus) / NT;
   const int rows = (int)(mt_big * 256);
   if (K % mf::BK == 0 && rows > 0 && rows < M) {
-    const int64_t T2 = ((M - rows + 127) / 128) * NT2;
-    t_split = (double)((mt_big * NT + cus - 1) / cus) + (double)((T2 + 2 * cus - 1) / (2 * cus)) * kSmallRound;
+    const double t_split = rounds(mt_big * NT, 1) * big + rounds(((M - rows + 127) / 128) * NT2, 2) * small;
+    if (t_split < t_best) { t_best = t_split; best = {PLAN_SPLIT, 8, rows}; }
   }
-  *split_rows = rows;
-  if (t_split < t_big && t_split < t_small) return PLAN_SPLIT;
-  return t_big <= t_small ? PLAN_BIG : PLAN_SMALL;
+  return best;
 }
 
 template <int WTM, int WTN, int WGM, int WGN, int EPI, int DEPTH>
@@ -725,18 +763,19 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
   return hipGetLastError();
 }
 
-template <int EPI>
+template <int EPI, int WTA>
 static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
                              hipStream_t s) {
-  const size_t lds = (size_t)2 * (256 + 256) * mf::BK * sizeof(bf16);
-  auto kern = k_linear_dma<EPI, bf16>;
+  constexpr int BM = 32 * WTA;
+  const size_t lds = (size_t)2 * (BM + 256) * mf::BK * sizeof(bf16);
+  auto kern = k_linear_dma<EPI, bf16, WTA>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (err != hipSuccess) return err;
     attr_set = true;
   }
-  const int MT = (M + 255) / 256, NT = (N + 255) / 256;
+  const int MT = (M + BM - 1) / BM, NT = (N + 255) / 256;
   hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(256), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
                      MT, NT);
   return hipGetLastError();
@@ -768,9 +807,12 @@ static EpiArgs rows_from(const EpiArgs &e, int m) {
 // 256x256 tiles: the 4-wave kernel with LDS-writing loads when it takes the shape, else the generic
 // 8-wave kernel (K % 64 != 0 or K < 128, and the latent scatter, which stays on 2 waves per SIMD).
 template <int EPI>
-static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s) {
+static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s,
+                             int wta) {
   if constexpr (EPI != EPI_EULER) {
-    if (K % mf::BK == 0 && K >= 2 * mf::BK) return launch_dma<EPI>(M, N, K, A, Wt, e, s);
+    if (K % mf::BK == 0 && K >= 2 * mf::BK) {
+      return wta == 7 ? launch_dma<EPI, 7>(M, N, K, A, Wt, e, s) : launch_dma<EPI, 8>(M, N, K, A, Wt, e, s);
+    }
   }
   return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
 }
@@ -779,15 +821,15 @@ template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
-    int rows = 0;
-    TilePlan plan = pick_tiles(M, N, K, &rows);
-    if (plan == PLAN_SPLIT && EPI == EPI_EULER) plan = PLAN_BIG;   // the latent scatter needs whole rows
-    if (plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
-    if (plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s);
-    hipError_t err = launch_big<EPI>(rows, N, K, A, Wt, e, s);
+    const bool dma_ok = EPI != EPI_EULER && K % mf::BK == 0 && K >= 2 * mf::BK;
+    TileChoice c = pick_tiles(M, N, K, dma_ok);
+    if (c.plan == PLAN_SPLIT && EPI == EPI_EULER) c = {PLAN_BIG, 8, 0};   // the latent scatter needs whole rows
+    if (c.plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
+    if (c.plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s, c.wta);
+    hipError_t err = launch_big<EPI>(c.rows, N, K, A, Wt, e, s, 8);
     if (err != hipSuccess) return err;
-    return launch_mfma<4, 4, 2, 2, EPI, 2>(M - rows, N, K, (const bf16 *)A + (size_t)rows * K, Wt,
-                                           rows_from<EPI>(e, rows), s);
+    return launch_mfma<4, 4, 2, 2, EPI, 2>(M - c.rows, N, K, (const bf16 *)A + (size_t)c.rows * K, Wt,
+                                           rows_from<EPI>(e, c.rows), s);
   }
   dim3 grid((M + 63) / 64, (N + 63) / 64);
   hipLaunchKernelGGL((k_linear_valu<float, EPI, float>), grid, dim3(256), 0, s, M, N, K,

@@ -83,14 +83,15 @@ def test_linear_small(dtype, M, N, K, epi):
     assert rel_l2(got, ref) <= tol
 
 
-@pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256"])
+@pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256", "bm:224"])
 @pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
                                    (520, 776, 1024)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
 def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
     """Every MFMA tiling (forced: "256x256" is the 4-wave kernel with LDS-writing loads when K % 64 == 0
     and K >= 128, else the 8-wave kernel; "split:256" puts rows 0..255 on 256x256 tiles and the rest
-    on 128x128 tiles, when M > 256 and K % 64 == 0) on ragged M, N and K tails, against the oracle.
+    on 128x128 tiles, when M > 256 and K % 64 == 0; "bm:224" the 4-wave kernel with 224-row tiles)
+    on ragged M, N and K tails, against the oracle.
     The residual case also writes the cache copy."""
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
     F = fb()
