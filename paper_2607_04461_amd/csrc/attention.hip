@@ -14,6 +14,10 @@
 //     LDS transpose read (ds_read_b64_tr_b16): in each group of 16 lanes, lane j addresses 4
 //     consecutive head dims of one key and lane 4a + b receives element b of the pieces addressed by
 //     lanes a, a + 4, a + 8, a + 12 -- i.e. one head dim across four keys.
+#include <cstdlib>
+#include <cstring>
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -101,9 +105,10 @@ constexpr int QW = 32;          // queries per wave
 constexpr int WAVES = 4;
 constexpr int QB = QW * WAVES;  // queries per workgroup
 __device__ __forceinline__ int k_off(int r, int c) { return r * DH + ((c ^ (r & 15)) << 3); }
-// V rows: 16-byte chunk c of key r at c ^ (2 r mod 16); keeps the four keys of a transpose-read group
-// on distinct banks
-__device__ __forceinline__ int v_off(int r, int c) { return r * DH + ((c ^ ((r << 1) & 14)) << 3); }
+// V rows: 16-byte chunk c of key r at c ^ 4 (r mod 4).  A transpose read serves 32 lanes a cycle:
+// four keys r..r+3 (r a multiple of 4) times chunks 4 dt .. 4 dt + 3, whose positions then differ in
+// bits 2-3 per key, so the 32 eight-byte pieces fill the 256-byte bank window once.
+__device__ __forceinline__ int v_off(int r, int c) { return r * DH + ((c ^ ((r & 3) << 2)) << 3); }
 }  // namespace fa
 
 __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
@@ -253,6 +258,201 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(AttnP p) {
     }
 }
 
+// ---------------------------------------------------------------- pipelined MFMA attention (dh 128)
+// Same fragment layouts as k_attn_mfma (S^T = K Q^T per 32-key slab, O^T += V^T P^T per 16-key chunk,
+// one lane per query), reorganised so that matrix cores and vector ALUs of a wave work at the same
+// time: while the VALUs turn the scores of key tile j into probabilities, the MFMAs already form the
+// scores of tile j + 1; the V^T P^T products of tile j follow.  K and V tiles reach LDS through
+// buffer loads that write LDS themselves (no staging registers): K tiles in a ring of two one tile
+// ahead, V tiles in their own ring of two; one barrier per tile.  Keys past tk read as zero (the
+// buffer range ends at the last key) and are masked on the ragged last tile.  LDS offsets are
+// per-lane bases plus immediates (stage, slab, chunk).
+namespace fa2 {
+constexpr int DH = 128, KT = 64, QW = 32, WAVES = 4, QB = QW * WAVES;
+constexpr int TILE_B = KT * DH * 2;   // bytes of one K or V tile
+// LDS: K stage 0, K stage 1, V stage 0, V stage 1
+constexpr int K_OFF = 0, V_OFF = 2 * TILE_B;
+}  // namespace fa2
+
+__global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
+  using namespace fa2;
+  __shared__ __attribute__((aligned(16))) bf16 sm[4 * KT * DH];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, li = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int q0 = blockIdx.x * QB + w * QW;
+  const int kb = kv_batch(p, b);
+  const bf16 *Q = (const bf16 *)p.q + (int64_t)b * p.q_bs + h * DH;
+  const bf16 *Kb = (const bf16 *)p.k + (int64_t)kb * p.kv_bs + h * DH;
+  const bf16 *Vb = (const bf16 *)p.v + (int64_t)kb * p.kv_bs + h * DH;
+  const int nt = (p.tk + KT - 1) / KT;
+  char *lds = reinterpret_cast<char *>(sm);
+
+  // this lane's query row, as the B operand of S^T = K Q^T: 8 k-steps of 16 head dims
+  const int qi = min(q0 + li, p.tq - 1);
+  bf16x8 qf[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks)
+    qf[ks] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qi * p.q_rs + 16 * ks + 8 * g);
+
+  // ---- tile loads: wave w fills rows 16 w + 4 x + (lane >> 4), x = 0..3, one 1 KiB load each; lane
+  // l writes 16-byte slot l & 15 of its row, so it fetches the chunk the swizzle puts there
+  auto tile_rsrc = [&](const bf16 *base, int j) {
+    const int valid = min(KT, p.tk - j * KT);
+    const uint64_t a = (uint64_t)(base + (int64_t)j * KT * p.kv_rs);
+    const uint32_t bytes = (uint32_t)((valid - 1) * p.kv_rs + DH) * 2u;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a), hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0,
+                                             (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+  };
+  auto load_k = [&](int j, int st) {
+    const __amdgpu_buffer_rsrc_t r = tile_rsrc(Kb, j);
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          r, (__attribute__((address_space(3))) void *)(lds + K_OFF + st * TILE_B + (16 * w + 4 * x) * DH * 2), 16,
+          (uint32_t)((16 * w + 4 * x + (lane >> 4)) * p.kv_rs + 8 * ((lane & 15) ^ ((4 * x + (lane >> 4)) & 15))) * 2u, 0, 0, 0);
+  };
+  auto load_v = [&](int j, int st) {
+    const __amdgpu_buffer_rsrc_t r = tile_rsrc(Vb, j);
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          r, (__attribute__((address_space(3))) void *)(lds + V_OFF + st * TILE_B + (16 * w + 4 * x) * DH * 2), 16,
+          (uint32_t)((16 * w + 4 * x + (lane >> 4)) * p.kv_rs + 8 * ((lane & 15) ^ (((lane >> 4) & 3) << 2))) * 2u, 0, 0, 0);
+  };
+
+  // ---- fragment offsets.  K fragment (slab sl, k-step ks): key 32 sl + li, chunk 2 ks + g at
+  // chunk ^ (key & 15).  V^T fragment (chunk c, dims 32 dt ..): transpose read of key 16 c + tkey
+  // (+ 8), head dims 32 dt + tdim .. + 3, chunk (d >> 3) ^ 4 (key & 3).
+  uint32_t ko[8], vo[4];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) ko[ks] = (uint32_t)(li * DH * 2 + (((2 * ks + g) ^ (li & 15)) << 4));
+  const int tq = lane & 15, th = (lane >> 4) & 1;
+  const int tkey = 4 * g + (tq >> 2), tdim = 16 * th + 4 * (tq & 3);
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    const int d = 32 * dt + tdim;
+    vo[dt] = (uint32_t)(tkey * DH * 2 + (((d >> 3) ^ ((tkey & 3) << 2)) << 4) + (d & 7) * 2);
+  }
+
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) o[dt][j] = 0.f;
+  float mrun = -INFINITY, lsum = 0.f;
+
+  // S^T of the tile in K stage st: lane holds query li, keys 32 sl + (j/4)*8 + 4 g + (j%4)
+  auto scores = [&](int st, f32x16 (&sc)[2]) {
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sc[sl][j] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(lds + K_OFF + st * TILE_B + sl * 32 * DH * 2 + ko[ks]);
+        sc[sl] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[sl], 0, 0, 0);
+      }
+    }
+  };
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  auto vread = [&](int st, int c, int dt, int hh) {
+    return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4 *)(lds + V_OFF + st * TILE_B + (16 * c + 8 * hh) * DH * 2 + vo[dt])));
+  };
+
+  // One key tile j (K of j in stage j & 1, V of j in stage j & 1): probabilities from sc, interleaved
+  // with the scores of tile j + 1 into sn when there is one, then O^T += V^T P^T.
+  auto tile = [&](auto STAGE, int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
+    constexpr int st = decltype(STAGE)::value;
+    // K of j + 1 and V of j have landed; every wave is done with K of j (read one tile ago) and V of
+    // j - 1, so those stages take K of j + 2 and V of j + 1
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __syncthreads();
+    if (j + 2 < nt) load_k(j + 2, st);
+    if (j + 1 < nt) load_v(j + 1, st ^ 1);
+    if ((j + 1) * KT > p.tk) {   // ragged last tile: keys at or past tk get -inf
+      const int lim = p.tk - j * KT - 4 * g;
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) sc[sl][q] = 32 * sl + (q >> 2) * 8 + (q & 3) < lim ? sc[sl][q] : -INFINITY;
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) tmax = fmaxf(tmax, sc[sl][q]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mnew = fmaxf(mrun, tmax);
+    if (__any(mnew > mrun)) {
+      const float corr = __builtin_amdgcn_exp2f((mrun - mnew) * p.qscale);
+      lsum *= corr;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) o[dt][q] *= corr;
+      mrun = mnew;
+    }
+    const float mb = mrun * p.qscale;
+    bf16x8 pf[4];
+    auto probs = [&]() {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+#pragma unroll
+        for (int i = 0; i < 8; i += 2) {
+          const float e0 = __builtin_amdgcn_exp2f(fmaf(sc[c >> 1][8 * (c & 1) + i], p.qscale, -mb));
+          const float e1 = __builtin_amdgcn_exp2f(fmaf(sc[c >> 1][8 * (c & 1) + i + 1], p.qscale, -mb));
+          lsum += e0 + e1;
+          const bf16x2 pr = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){e0, e1}, bf16x2);
+          pf[c][i] = pr[0];
+          pf[c][i + 1] = pr[1];
+        }
+      }
+    };
+    // the next tile's scores (after the last tile: from a stale stage, unused) with the
+    // probabilities of this one, in one block so the two can interleave
+    scores(st ^ 1, sn);
+    probs();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        const bf16x4 w0 = vread(st, c, dt, 0), w1 = vread(st, c, dt, 1);
+        const bf16x8 vf = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c], o[dt], 0, 0, 0);
+      }
+    }
+  };
+
+  load_k(0, 0);
+  if (nt > 1) load_k(1, 1);
+  load_v(0, 0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  __syncthreads();
+  f32x16 s0[2], s1[2];
+  scores(0, s0);
+  for (int j = 0; j < nt; j += 2) {
+    tile(std::integral_constant<int, 0>{}, j, s0, s1);
+    if (j + 1 >= nt) break;
+    tile(std::integral_constant<int, 1>{}, j + 1, s1, s0);
+  }
+  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  const float inv = 1.0f / ltot;
+  if (q0 + li >= p.tq) return;
+  bf16 *O = (bf16 *)p.out + (int64_t)b * p.o_bs + (int64_t)(q0 + li) * p.o_rs + h * DH;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      bf16x4 w4 = {(bf16)(o[dt][4 * jq] * inv), (bf16)(o[dt][4 * jq + 1] * inv),
+                   (bf16)(o[dt][4 * jq + 2] * inv), (bf16)(o[dt][4 * jq + 3] * inv)};
+      *reinterpret_cast<bf16x4 *>(O + 32 * dt + 8 * jq + 4 * g) = w4;
+    }
+}
+
 template <typename T>
 static hipError_t launch_valu(const AttnP &p, int dh, hipStream_t s) {
   dim3 grid((p.tq + 63) / 64, p.heads, p.batch), block(64);
@@ -277,7 +477,9 @@ hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s) {
   p.qscale = (float)(1.4426950408889634 / sqrt((double)a.head_dim));
   if (t == ACT_BF16 && a.head_dim == fa::DH) {
     dim3 grid((p.tq + fa::QB - 1) / fa::QB, p.heads, p.batch);
-    hipLaunchKernelGGL(k_attn_mfma, grid, dim3(256), 0, s, p);
+    const char *sel = getenv("FLASHBON_ATTN");   // "mfma": the unpipelined kernel (tuning)
+    if (sel && !strcmp(sel, "mfma")) hipLaunchKernelGGL(k_attn_mfma, grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL(k_attn_fa, grid, dim3(256), 0, s, p);
     return hipGetLastError();
   }
   if (t == ACT_BF16) return launch_valu<bf16>(p, a.head_dim, s);

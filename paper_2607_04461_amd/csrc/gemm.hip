@@ -174,7 +174,8 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
 
 // Residual update h += gate (acc + bias) of one wave's tile, optional cache write (CM 1: copy of the
 // new row, CM 2: new row minus what the cache held).  The tile is walked in batches of JB 16-row
-// blocks of one column group; PIPE 2: the rows of batch x + 1 are requested before the stores of x.
+// blocks of one column group; a column group's bias and gate come with its first batch.  PIPE 2: the
+// loads of batch x + 1 are issued before the stores of batch x.
 template <int WTN, int WTM, int CM, int PIPE, int JB>
 __device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
                                               int mbase, int nbase, int fr, int fq) {
@@ -187,26 +188,28 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&ac
   const __amdgpu_buffer_rsrc_t rsC = rsrc(CM ? e.cache + (int64_t)mbase * e.ldo : nullptr, CM ? bytes : 0u);
   const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
   const __amdgpu_buffer_rsrc_t rsG = rsrc(e.gate, e.gate ? (uint32_t)N * 4u : 0u);
+  const bool has_gate = e.gate != nullptr;
   uint32_t c0[NP], c1[NP];   // byte offsets of the two 4-column halves, or out of range
-  f32x4 b[NP][2], g[NP][2];
 #pragma unroll
   for (int pa = 0; pa < NP; ++pa) {
     const int n = nbase + 32 * pa + 8 * fq;
     c0[pa] = n < N ? (uint32_t)n * 4u : OUT_OF_RANGE;
     c1[pa] = n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE;
-    b[pa][0] = ld4(rsB, c0[pa]);
-    b[pa][1] = ld4(rsB, c1[pa]);
-    if (e.gate) {
-      g[pa][0] = ld4(rsG, c0[pa]);
-      g[pa][1] = ld4(rsG, c1[pa]);
-    } else {
-      g[pa][0] = g[pa][1] = f32x4{1.f, 1.f, 1.f, 1.f};
-    }
   }
   const uint32_t ro = (uint32_t)fr * (uint32_t)e.ldo * 4u, rstep = 16u * (uint32_t)e.ldo * 4u;
-  f32x4 h[PIPE][JB][2], c[CM == 2 ? PIPE : 1][JB][2];
+  f32x4 h[PIPE][JB][2], c[CM == 2 ? PIPE : 1][JB][2], b[NP][2], g[NP][2];
   auto fetch = [&](int x, int buf) {   // batch x: column group x / NJ, row blocks JB (x % NJ) ..
     const int pa = x / NJ, j0 = JB * (x % NJ);
+    if (x % NJ == 0) {
+      b[pa][0] = ld4(rsB, c0[pa]);
+      b[pa][1] = ld4(rsB, c1[pa]);
+      if (has_gate) {
+        g[pa][0] = ld4(rsG, c0[pa]);
+        g[pa][1] = ld4(rsG, c1[pa]);
+      } else {
+        g[pa][0] = g[pa][1] = f32x4{1.f, 1.f, 1.f, 1.f};
+      }
+    }
 #pragma unroll
     for (int jj = 0; jj < JB; ++jj) {
       const uint32_t r = ro + (uint32_t)(j0 + jj) * rstep;
@@ -247,7 +250,8 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&ac
 
 // Store (bf16 or fp32), GELU-and-store, or fp32 store of one wave's tile; bias loaded first, no load
 // between the stores.
-template <int EPI, typename TO, int WTN, int WTM>
+// WHOLE8: N % 8 == 0, one 16-byte store per 8 bf16 values; else two 8-byte stores.
+template <int EPI, typename TO, int WTN, int WTM, bool WHOLE8>
 __device__ __forceinline__ void store_tile(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
                                            int mbase, int nbase, int fr, int fq) {
   using namespace epi;
@@ -291,7 +295,7 @@ __device__ __forceinline__ void store_tile(const EpiArgs &e, const f32x4 (&acc)[
       } else {
         const bf16x4 w0 = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
         const bf16x4 w1 = {(bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
-        if (N % 8 == 0) {   // whole 8-column groups: one 16-byte store
+        if constexpr (WHOLE8) {
           const bf16x8 w = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w), rsO, o0, 0, 0);
         } else {
@@ -305,7 +309,7 @@ __device__ __forceinline__ void store_tile(const EpiArgs &e, const f32x4 (&acc)[
 
 // The epilogue of a wave's tile for every epilogue kind.  PIPE: residual rows fetched one column
 // group ahead (2) or per group (1), by the kernel's register budget.
-template <int EPI, typename TO, int WTN, int WTM, int PIPE>
+template <int EPI, typename TO, int WTN, int WTM, int PIPE, bool WHOLE8>
 __device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
                                               int mbase, int nbase, int fr, int fq) {
   if constexpr (EPI == EPI_RESIDUAL) {
@@ -330,7 +334,7 @@ __device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&ac
       }
     }
   } else {
-    store_tile<EPI, TO, WTN, WTM>(e, acc, M, N, mbase, nbase, fr, fq);
+    store_tile<EPI, TO, WTN, WTM, WHOLE8>(e, acc, M, N, mbase, nbase, fr, fq);
   }
 }
 
@@ -457,7 +461,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, WGM * WGN <= 4 ? 2 : 1) void k_line
   };
   // acc[i][j] (C^T tile 16x16): lane column = m index (lane & 15), rows = 4 consecutive n.
   auto epilogue = [&](int em0, int en0) {
-    tile_epilogue<EPI, TO, WTN, WTM, 1>(e, acc, M, N, em0 + 16 * WTM * wm, en0 + 16 * WTN * wn, fr, fq);
+    tile_epilogue<EPI, TO, WTN, WTM, 1, false>(e, acc, M, N, em0 + 16 * WTM * wm, en0 + 16 * WTN * wn, fr, fq);
   };
   auto zero_acc = [&]() {
 #pragma unroll
@@ -567,10 +571,6 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
     for (int x = 0; x < NL; ++x) dma_one(kt, st, x);
   };
   f32x4 acc[WT][WTA];
-#pragma unroll
-  for (int i = 0; i < WT; ++i)
-#pragma unroll
-    for (int j = 0; j < WTA; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
   const int fr = lane & 15, fq = lane >> 4;
   // Fragment x of substep ks: x < 8 -> W fragment i = x, rows 128 wn + 32 (i/2) + 8 (fr/4) + 4 (i%2) +
   // fr%4 (a lane's outputs of tiles 2a, 2a+1 are then 8 consecutive columns); x >= 8 -> A fragment
@@ -626,7 +626,11 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
   __syncthreads();
 #pragma unroll
   for (int x = 0; x < NR; ++x) rd(0, 0, fw0, fa0, x);
-  // tile kt sits in stage kt & 1; tile kt+1 is in flight into the other stage
+#pragma unroll
+  for (int i = 0; i < WT; ++i)
+#pragma unroll
+    for (int j = 0; j < WTA; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+  // K tile kt sits in stage kt & 1; tile kt+1 is in flight into the other stage
   int kt = 0;
   for (; kt + 2 < KT; ++kt) {
     substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
@@ -637,13 +641,13 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
     substep(T_{}, T_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, kt + 2, kt & 1);
   }
   substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the last tile has landed
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the last K tile has landed
   __syncthreads();
   substep(T_{}, F_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, 0, 0);
   ++kt;
   substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
   substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
-  tile_epilogue<EPI, TO, WT, WTA, 2>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 128 * wn, fr, fq);
+  tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 128 * wn, fr, fq);
 }
 // ---------------------------------------------------------------------------------- VALU path
 template <typename TI, int EPI, typename TO>
@@ -805,12 +809,13 @@ static EpiArgs rows_from(const EpiArgs &e, int m) {
 }
 
 // 256x256 tiles: the 4-wave kernel with LDS-writing loads when it takes the shape, else the generic
-// 8-wave kernel (K % 64 != 0 or K < 128, and the latent scatter, which stays on 2 waves per SIMD).
+// 8-wave kernel (K % 64 != 0, K < 128 or N % 8 != 0, and the latent scatter, which stays on 2 waves
+// per SIMD).
 template <int EPI>
 static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s,
                              int wta) {
   if constexpr (EPI != EPI_EULER) {
-    if (K % mf::BK == 0 && K >= 2 * mf::BK) {
+    if (K % mf::BK == 0 && K >= 2 * mf::BK && N % 8 == 0) {
       return wta == 7 ? launch_dma<EPI, 7>(M, N, K, A, Wt, e, s) : launch_dma<EPI, 8>(M, N, K, A, Wt, e, s);
     }
   }
@@ -821,7 +826,7 @@ template <int EPI>
 static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, const void *Wt,
                              const EpiArgs &e, hipStream_t s) {
   if (t == ACT_BF16) {
-    const bool dma_ok = EPI != EPI_EULER && K % mf::BK == 0 && K >= 2 * mf::BK;
+    const bool dma_ok = EPI != EPI_EULER && K % mf::BK == 0 && K >= 2 * mf::BK && N % 8 == 0;
     TileChoice c = pick_tiles(M, N, K, dma_ok);
     if (c.plan == PLAN_SPLIT && EPI == EPI_EULER) c = {PLAN_BIG, 8, 0};   // the latent scatter needs whole rows
     if (c.plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);

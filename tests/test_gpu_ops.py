@@ -177,6 +177,30 @@ def test_cross_attention_kv_index(dtype):
     assert rel_l2(got, ref) <= (1e-2 if dtype == "bf16" else 2e-6)
 
 
+@pytest.mark.parametrize("kernel", ["fa", "mfma"])
+@pytest.mark.parametrize("tq,tk", [(1, 1), (130, 64), (129, 128), (200, 65), (67, 192), (160, 321)])
+def test_attention_mfma_kernels_tile_edges(kernel, tq, tk, monkeypatch):
+    """Both head_dim-128 bf16 kernels (FLASHBON_ATTN: "fa" the pipelined one, the default; "mfma" the
+    unpipelined one) over key counts that give one key, exactly one or two full 64-key tiles, a
+    one-key ragged tail, and odd and even tile counts, with query blocks that end mid-wave; one of
+    the batches reads its keys through the kv index."""
+    monkeypatch.setenv("FLASHBON_ATTN", kernel)
+    F = fb()
+    B, NC, heads, dh = 3, 2, 2, 128
+    D = heads * dh
+    q = _operand((B, tq, D), 51, "bf16")
+    kv = _operand((NC, tk, 2 * D), 52, "bf16")
+    idx = np.array([1, 0, 1], np.int32)
+    dkv = _dev(kv, "bf16")
+    out = torch.empty((B, tq, D), device="cuda", dtype=torch.bfloat16)
+    F.flashbon_op_attention(F.BF16, B, heads, dh, tq, tk, _dev(q, "bf16"), tq * D, D, dkv, dkv[..., D:],
+                            tk * 2 * D, 2 * D, torch.from_numpy(idx).cuda(), NC, out, tq * D, D)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    ref = np.stack([_attn_ref(q[b], kv[idx[b], :, :D], kv[idx[b], :, D:], heads) for b in range(B)])
+    assert rel_l2(got, ref) <= 1e-2
+
+
 @pytest.mark.parametrize("B,heads,T,tk", [(16, 12, 1560, 1560), (16, 12, 1560, 512), (4, 40, 4096, 4096)])
 def test_attention_full_shapes_bf16_sampled_queries(B, heads, T, tk):
     F = fb()
