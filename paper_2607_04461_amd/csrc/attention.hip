@@ -25,6 +25,7 @@ namespace fb {
 
 struct AttnP {
   int batch, heads, tq, tk;
+  int nqb;       // query blocks per (candidate, head) (k_attn_fa's 1-D grid)
   const void *q; int64_t q_bs, q_rs;
   const void *k; const void *v; int64_t kv_bs, kv_rs;
   const int32_t *kv_index; int n_kv;
@@ -279,8 +280,14 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
   __shared__ __attribute__((aligned(16))) bf16 sm[4 * KT * DH];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, li = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int b = blockIdx.z, h = blockIdx.y;
-  const int q0 = blockIdx.x * QB + w * QW;
+  // 1-D grid, XCD-aware: workgroups go to the 8 XCDs round-robin by id, so id -> (unit u = head *
+  // batch + candidate, query block) keeps every query block of a unit on XCD u % 8, where its K and V
+  // stay in that XCD's L2 (and the text K/V of one head is shared by the candidates on that XCD)
+  const int id = blockIdx.x, rest = id >> 3;
+  const int u = (rest / p.nqb) * 8 + (id & 7), qblk = rest % p.nqb;
+  if (u >= p.batch * p.heads) return;
+  const int h = u / p.batch, b = u % p.batch;
+  const int q0 = qblk * QB + w * QW;
   const int kb = kv_batch(p, b);
   const bf16 *Q = (const bf16 *)p.q + (int64_t)b * p.q_bs + h * DH;
   const bf16 *Kb = (const bf16 *)p.k + (int64_t)kb * p.kv_bs + h * DH;
@@ -396,34 +403,34 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
       mrun = mnew;
     }
     const float mb = mrun * p.qscale;
-    bf16x8 pf[4];
-    auto probs = [&]() {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-#pragma unroll
-        for (int i = 0; i < 8; i += 2) {
-          const float e0 = __builtin_amdgcn_exp2f(fmaf(sc[c >> 1][8 * (c & 1) + i], p.qscale, -mb));
-          const float e1 = __builtin_amdgcn_exp2f(fmaf(sc[c >> 1][8 * (c & 1) + i + 1], p.qscale, -mb));
-          lsum += e0 + e1;
-          const bf16x2 pr = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){e0, e1}, bf16x2);
-          pf[c][i] = pr[0];
-          pf[c][i + 1] = pr[1];
-        }
-      }
-    };
-    // the next tile's scores (after the last tile: from a stale stage, unused) with the
-    // probabilities of this one, in one block so the two can interleave
+    // the next tile's scores (after the last tile: from a stale stage, unused), this tile's
+    // probabilities and its V^T P^T products in one block, chunk by chunk (16 keys), with the V
+    // fragments of chunk c + 1 read while chunk c is in flight
     scores(st ^ 1, sn);
-    probs();
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    bf16x8 vf[2][4];
+    auto vload = [&](int c, bf16x8 (&v)[4]) {
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         const bf16x4 w0 = vread(st, c, dt, 0), w1 = vread(st, c, dt, 1);
-        const bf16x8 vf = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c], o[dt], 0, 0, 0);
+        v[dt] = bf16x8{w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
       }
+    };
+    vload(0, vf[0]);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      bf16x8 pc;
+#pragma unroll
+      for (int i = 0; i < 8; i += 2) {
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(sc[c >> 1][8 * (c & 1) + i], p.qscale, -mb));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(sc[c >> 1][8 * (c & 1) + i + 1], p.qscale, -mb));
+        lsum += e0 + e1;
+        const bf16x2 pr = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){e0, e1}, bf16x2);
+        pc[i] = pr[0];
+        pc[i + 1] = pr[1];
+      }
+      if (c + 1 < 4) vload(c + 1, vf[(c + 1) & 1]);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1][dt], pc, o[dt], 0, 0, 0);
     }
   };
 
@@ -469,6 +476,7 @@ static hipError_t launch_valu(const AttnP &p, int dh, hipStream_t s) {
 
 hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s) {
   AttnP p;
+  p.nqb = 0;
   p.batch = a.batch; p.heads = a.heads; p.tq = a.tq; p.tk = a.tk;
   p.q = a.q; p.q_bs = a.q_bs; p.q_rs = a.q_rs;
   p.k = a.k; p.v = a.v; p.kv_bs = a.kv_bs; p.kv_rs = a.kv_rs;
@@ -478,8 +486,13 @@ hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s) {
   if (t == ACT_BF16 && a.head_dim == fa::DH) {
     dim3 grid((p.tq + fa::QB - 1) / fa::QB, p.heads, p.batch);
     const char *sel = getenv("FLASHBON_ATTN");   // "mfma": the unpipelined kernel (tuning)
-    if (sel && !strcmp(sel, "mfma")) hipLaunchKernelGGL(k_attn_mfma, grid, dim3(256), 0, s, p);
-    else hipLaunchKernelGGL(k_attn_fa, grid, dim3(256), 0, s, p);
+    if (sel && !strcmp(sel, "mfma")) {
+      hipLaunchKernelGGL(k_attn_mfma, grid, dim3(256), 0, s, p);
+    } else {
+      p.nqb = (p.tq + fa2::QB - 1) / fa2::QB;
+      const int64_t units8 = ((int64_t)p.batch * p.heads + 7) / 8 * 8;
+      hipLaunchKernelGGL(k_attn_fa, dim3((unsigned)(units8 * p.nqb)), dim3(256), 0, s, p);
+    }
     return hipGetLastError();
   }
   if (t == ACT_BF16) return launch_valu<bf16>(p, a.head_dim, s);
