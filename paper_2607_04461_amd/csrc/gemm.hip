@@ -172,59 +172,63 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
 }
 }  // namespace epi
 
-// Residual update h += gate (acc + bias) of one wave's tile, optional cache write (CM 1: copy of the
-// new row, CM 2: new row minus what the cache held).  The tile is walked in batches of JB 16-row
-// blocks of one column group; a column group's bias and gate come with its first batch.  PIPE 2: the
-// loads of batch x + 1 are issued before the stores of batch x.
-template <int WTN, int WTM, int CM, int PIPE, int JB>
-__device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
-                                              int mbase, int nbase, int fr, int fq) {
+// A wave's output, whatever the MFMA shape, is walked as NCG column groups x NRB row blocks: in row
+// block rb the lane owns row mbase + RS rb + r0 and, in column group cg, the 8 consecutive columns
+// nbase + col(cg) .. + 7 with values val(cg, rb, q), q = 0..7 (two 4-column halves).
+
+// Residual update h += gate (acc + bias), optional cache write (CM 1: copy of the new row, CM 2: new
+// row minus what the cache held).  Batches of JB row blocks of one column group; a column group's
+// bias and gate come with its first batch.  PIPE 2: the loads of batch x + 1 are issued before the
+// stores of batch x.
+template <int NCG, int NRB, int RS, int CM, int PIPE, int JB, typename Col, typename Val>
+__device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, int mbase, int nbase, int r0,
+                                              Col col, Val val) {
   using namespace epi;
-  constexpr int NP = WTN / 2, NJ = WTM / JB, NB = NP * NJ;
-  static_assert(WTM % JB == 0, "row blocks per batch");
-  const int rows = max(0, min(M - mbase, 16 * WTM));
+  constexpr int NJ = NRB / JB, NB = NCG * NJ;
+  static_assert(NRB % JB == 0, "row blocks per batch");
+  const int rows = max(0, min(M - mbase, RS * NRB));
   const uint32_t bytes = (uint32_t)rows * (uint32_t)e.ldo * 4u;
   const __amdgpu_buffer_rsrc_t rsO = rsrc((float *)e.out + (int64_t)mbase * e.ldo, bytes);
   const __amdgpu_buffer_rsrc_t rsC = rsrc(CM ? e.cache + (int64_t)mbase * e.ldo : nullptr, CM ? bytes : 0u);
   const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
   const __amdgpu_buffer_rsrc_t rsG = rsrc(e.gate, e.gate ? (uint32_t)N * 4u : 0u);
   const bool has_gate = e.gate != nullptr;
-  uint32_t c0[NP], c1[NP];   // byte offsets of the two 4-column halves, or out of range
+  uint32_t c0[NCG], c1[NCG];   // byte offsets of the two 4-column halves, or out of range
 #pragma unroll
-  for (int pa = 0; pa < NP; ++pa) {
-    const int n = nbase + 32 * pa + 8 * fq;
-    c0[pa] = n < N ? (uint32_t)n * 4u : OUT_OF_RANGE;
-    c1[pa] = n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE;
+  for (int cg = 0; cg < NCG; ++cg) {
+    const int n = nbase + col(cg);
+    c0[cg] = n < N ? (uint32_t)n * 4u : OUT_OF_RANGE;
+    c1[cg] = n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE;
   }
-  const uint32_t ro = (uint32_t)fr * (uint32_t)e.ldo * 4u, rstep = 16u * (uint32_t)e.ldo * 4u;
-  f32x4 h[PIPE][JB][2], c[CM == 2 ? PIPE : 1][JB][2], b[NP][2], g[NP][2];
+  const uint32_t ro = (uint32_t)r0 * (uint32_t)e.ldo * 4u, rstep = (uint32_t)RS * (uint32_t)e.ldo * 4u;
+  f32x4 h[PIPE][JB][2], c[CM == 2 ? PIPE : 1][JB][2], b[NCG][2], g[NCG][2];
   auto fetch = [&](int x, int buf) {   // batch x: column group x / NJ, row blocks JB (x % NJ) ..
-    const int pa = x / NJ, j0 = JB * (x % NJ);
+    const int cg = x / NJ, j0 = JB * (x % NJ);
     if (x % NJ == 0) {
-      b[pa][0] = ld4(rsB, c0[pa]);
-      b[pa][1] = ld4(rsB, c1[pa]);
+      b[cg][0] = ld4(rsB, c0[cg]);
+      b[cg][1] = ld4(rsB, c1[cg]);
       if (has_gate) {
-        g[pa][0] = ld4(rsG, c0[pa]);
-        g[pa][1] = ld4(rsG, c1[pa]);
+        g[cg][0] = ld4(rsG, c0[cg]);
+        g[cg][1] = ld4(rsG, c1[cg]);
       } else {
-        g[pa][0] = g[pa][1] = f32x4{1.f, 1.f, 1.f, 1.f};
+        g[cg][0] = g[cg][1] = f32x4{1.f, 1.f, 1.f, 1.f};
       }
     }
 #pragma unroll
     for (int jj = 0; jj < JB; ++jj) {
       const uint32_t r = ro + (uint32_t)(j0 + jj) * rstep;
-      h[buf][jj][0] = ld4(rsO, r + c0[pa]);
-      h[buf][jj][1] = ld4(rsO, r + c1[pa]);
+      h[buf][jj][0] = ld4(rsO, r + c0[cg]);
+      h[buf][jj][1] = ld4(rsO, r + c1[cg]);
       if constexpr (CM == 2) {
-        c[buf][jj][0] = ld4(rsC, r + c0[pa]);
-        c[buf][jj][1] = ld4(rsC, r + c1[pa]);
+        c[buf][jj][0] = ld4(rsC, r + c0[cg]);
+        c[buf][jj][1] = ld4(rsC, r + c1[cg]);
       }
     }
   };
   if constexpr (PIPE == 2) fetch(0, 0);
 #pragma unroll
   for (int x = 0; x < NB; ++x) {
-    const int pa = x / NJ, j0 = JB * (x % NJ);
+    const int cg = x / NJ, j0 = JB * (x % NJ);
     const int buf = PIPE == 2 ? (x & 1) : 0;
     if constexpr (PIPE == 2) {
       if (x + 1 < NB) fetch(x + 1, (x + 1) & 1);
@@ -235,11 +239,10 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&ac
     for (int jj = 0; jj < JB; ++jj) {
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const f32x4 a = acc[2 * pa + hf][j0 + jj];
         f32x4 o = h[buf][jj][hf];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] += g[pa][hf][q] * (a[q] + b[pa][hf][q]);
-        const uint32_t off = ro + (uint32_t)(j0 + jj) * rstep + (hf ? c1[pa] : c0[pa]);
+        for (int q = 0; q < 4; ++q) o[q] += g[cg][hf][q] * (val(cg, j0 + jj, 4 * hf + q) + b[cg][hf][q]);
+        const uint32_t off = ro + (uint32_t)(j0 + jj) * rstep + (hf ? c1[cg] : c0[cg]);
         st4(rsO, off, o);
         if constexpr (CM == 1) st4(rsC, off, o);
         if constexpr (CM == 2) st4(rsC, off, o - c[buf][jj][hf]);
@@ -248,47 +251,42 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, const f32x4 (&ac
   }
 }
 
-// Store (bf16 or fp32), GELU-and-store, or fp32 store of one wave's tile; bias loaded first, no load
-// between the stores.
-// WHOLE8: N % 8 == 0, one 16-byte store per 8 bf16 values; else two 8-byte stores.
-template <int EPI, typename TO, int WTN, int WTM, bool WHOLE8>
-__device__ __forceinline__ void store_tile(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
-                                           int mbase, int nbase, int fr, int fq) {
+// Store (bf16 or fp32), GELU-and-store, or fp32 store; bias loaded first, no load between the
+// stores.  WHOLE8: N % 8 == 0, one 16-byte store per 8 bf16 values; else two 8-byte stores.
+template <int EPI, typename TO, int NCG, int NRB, int RS, bool WHOLE8, typename Col, typename Val>
+__device__ __forceinline__ void store_tile(const EpiArgs &e, int M, int N, int mbase, int nbase, int r0, Col col,
+                                           Val val) {
   using namespace epi;
-  constexpr int NP = WTN / 2;
   constexpr bool F32 = EPI == EPI_STORE_F32 || sizeof(TO) == 4;
   constexpr uint32_t ES = F32 ? 4u : 2u;
-  const int rows = max(0, min(M - mbase, 16 * WTM));
+  const int rows = max(0, min(M - mbase, RS * NRB));
   const __amdgpu_buffer_rsrc_t rsO = rsrc((char *)e.out + (int64_t)mbase * e.ldo * ES, (uint32_t)rows * (uint32_t)e.ldo * ES);
   const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
-  uint32_t c0[NP], c1[NP];
-  f32x4 b[NP][2];
+  uint32_t c0[NCG], c1[NCG];
+  f32x4 b[NCG][2];
 #pragma unroll
-  for (int pa = 0; pa < NP; ++pa) {
-    const int n = nbase + 32 * pa + 8 * fq;
-    c0[pa] = n < N ? (uint32_t)n : OUT_OF_RANGE;
-    c1[pa] = n + 4 < N ? (uint32_t)(n + 4) : OUT_OF_RANGE;
-    b[pa][0] = ld4(rsB, n < N ? (uint32_t)n * 4u : OUT_OF_RANGE);
-    b[pa][1] = ld4(rsB, n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE);
+  for (int cg = 0; cg < NCG; ++cg) {
+    const int n = nbase + col(cg);
+    c0[cg] = n < N ? (uint32_t)n : OUT_OF_RANGE;
+    c1[cg] = n + 4 < N ? (uint32_t)(n + 4) : OUT_OF_RANGE;
+    b[cg][0] = ld4(rsB, n < N ? (uint32_t)n * 4u : OUT_OF_RANGE);
+    b[cg][1] = ld4(rsB, n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE);
   }
 #pragma unroll
-  for (int pa = 0; pa < NP; ++pa) {
+  for (int cg = 0; cg < NCG; ++cg) {
 #pragma unroll
-    for (int j = 0; j < WTM; ++j) {
-      const uint32_t ro = (uint32_t)(16 * j + fr) * (uint32_t)e.ldo;
+    for (int rb = 0; rb < NRB; ++rb) {
+      const uint32_t ro = (uint32_t)(RS * rb + r0) * (uint32_t)e.ldo;
       float v[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v[q] = acc[2 * pa][j][q] + b[pa][0][q];
-        v[4 + q] = acc[2 * pa + 1][j][q] + b[pa][1][q];
-      }
+      for (int q = 0; q < 8; ++q) v[q] = val(cg, rb, q) + b[cg][q >> 2][q & 3];
       if constexpr (EPI == EPI_GELU) {
 #pragma unroll
         for (int q = 0; q < 8; ++q) v[q] = gelu_tanh(v[q]);
       }
       // an out-of-range column offset stays out of range after the row offset and scaling are added
-      const uint32_t o0 = c0[pa] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c0[pa]) * ES;
-      const uint32_t o1 = c1[pa] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c1[pa]) * ES;
+      const uint32_t o0 = c0[cg] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c0[cg]) * ES;
+      const uint32_t o1 = c1[cg] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c1[cg]) * ES;
       if constexpr (F32) {
         st4(rsO, o0, f32x4{v[0], v[1], v[2], v[3]});
         st4(rsO, o1, f32x4{v[4], v[5], v[6], v[7]});
@@ -307,26 +305,26 @@ __device__ __forceinline__ void store_tile(const EpiArgs &e, const f32x4 (&acc)[
   }
 }
 
-// The epilogue of a wave's tile for every epilogue kind.  PIPE: residual rows fetched one column
-// group ahead (2) or per group (1), by the kernel's register budget.
-template <int EPI, typename TO, int WTN, int WTM, int PIPE, bool WHOLE8>
-__device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
-                                              int mbase, int nbase, int fr, int fq) {
+// The epilogue of a wave's output for every epilogue kind, on the group/block walk above.  PIPE:
+// residual rows fetched one batch ahead (2) or per batch (1), by the kernel's register budget.
+template <int EPI, typename TO, int NCG, int NRB, int RS, int PIPE, bool WHOLE8, typename Col, typename Val>
+__device__ __forceinline__ void wave_epilogue(const EpiArgs &e, int M, int N, int mbase, int nbase, int r0, Col col,
+                                              Val val) {
   if constexpr (EPI == EPI_RESIDUAL) {
-    constexpr int JB = PIPE == 2 ? (WTM % 2 == 0 ? 2 : 1) : (WTM % 4 == 0 ? 4 : (WTM % 2 == 0 ? 2 : 1));
-    if (!e.cache) residual_tile<WTN, WTM, 0, PIPE, JB>(e, acc, M, N, mbase, nbase, fr, fq);
-    else if (!e.cache_delta) residual_tile<WTN, WTM, 1, PIPE, JB>(e, acc, M, N, mbase, nbase, fr, fq);
-    else residual_tile<WTN, WTM, 2, 1, JB>(e, acc, M, N, mbase, nbase, fr, fq);
+    constexpr int JB = PIPE == 2 ? (NRB % 2 == 0 ? 2 : 1) : (NRB % 4 == 0 ? 4 : (NRB % 2 == 0 ? 2 : 1));
+    if (!e.cache) residual_tile<NCG, NRB, RS, 0, PIPE, JB>(e, M, N, mbase, nbase, r0, col, val);
+    else if (!e.cache_delta) residual_tile<NCG, NRB, RS, 1, PIPE, JB>(e, M, N, mbase, nbase, r0, col, val);
+    else residual_tile<NCG, NRB, RS, 2, 1, JB>(e, M, N, mbase, nbase, r0, col, val);
   } else if constexpr (EPI == EPI_EULER) {
 #pragma unroll
-    for (int pa = 0; pa < WTN / 2; ++pa) {
-      const int n = nbase + 32 * pa + 8 * fq;
+    for (int cg = 0; cg < NCG; ++cg) {
+      const int n = nbase + col(cg);
 #pragma unroll
-      for (int j = 0; j < WTM; ++j) {
-        const int m = mbase + 16 * j + fr;
-        const float v[8] = {acc[2 * pa][j][0], acc[2 * pa][j][1], acc[2 * pa][j][2], acc[2 * pa][j][3],
-                            acc[2 * pa + 1][j][0], acc[2 * pa + 1][j][1], acc[2 * pa + 1][j][2],
-                            acc[2 * pa + 1][j][3]};
+      for (int rb = 0; rb < NRB; ++rb) {
+        const int m = mbase + RS * rb + r0;
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = val(cg, rb, q);
         if (m < M && n < N) {
           if (n + 8 <= N) epilogue8<EPI, TO>(e, m, n, v);
           else epilogue4<EPI, TO>(e, m, n, v[0], v[1], v[2], v[3]);   // N % 8 == 4 edge
@@ -334,8 +332,19 @@ __device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&ac
       }
     }
   } else {
-    store_tile<EPI, TO, WTN, WTM, WHOLE8>(e, acc, M, N, mbase, nbase, fr, fq);
+    store_tile<EPI, TO, NCG, NRB, RS, WHOLE8>(e, M, N, mbase, nbase, r0, col, val);
   }
+}
+
+// 16x16 MFMA tiles: acc[i][j] (i over 16-column W fragments, permuted so that fragments 2a and 2a+1
+// give a lane 8 consecutive columns; j over 16-row A fragments) holds rows mbase + 16 j + fr and
+// columns nbase + 32 a + 8 fq .. + 7 (fr = lane & 15, fq = lane >> 4).
+template <int EPI, typename TO, int WTN, int WTM, int PIPE, bool WHOLE8>
+__device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
+                                              int mbase, int nbase, int fr, int fq) {
+  wave_epilogue<EPI, TO, WTN / 2, WTM, 16, PIPE, WHOLE8>(
+      e, M, N, mbase, nbase, fr, [&](int cg) { return 32 * cg + 8 * fq; },
+      [&](int cg, int rb, int q) { return acc[2 * cg + (q >> 2)][rb][q & 3]; });
 }
 
 // ---------------------------------------------------------------------------------- MFMA path
