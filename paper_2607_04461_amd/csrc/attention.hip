@@ -31,6 +31,7 @@ struct AttnP {
   const int32_t *kv_index; int n_kv;
   void *out; int64_t o_bs, o_rs;
   float qscale;  // log2(e) / sqrt(head_dim)
+  float lazy_thr;  // k_attn_fa: how far a tile maximum may pass the running one before O is rescaled
 };
 
 __device__ __forceinline__ int kv_batch(const AttnP &p, int b) {
@@ -392,8 +393,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) tmax = fmaxf(tmax, sc[sl][q]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(mrun, tmax);
-    if (__any(mnew > mrun)) {
+    // Lazy rescaling: the running maximum moves only once some row's tile maximum passes it by more
+    // than 8 / qscale (a factor 2^8 after exp2).  Until then the probabilities stay at most 256, well
+    // inside bf16 (P) and fp32 (O, l), and O / l is the same quotient, so the wave skips the O rescale
+    // on almost every tile.  The first tile always moves it (mrun = -inf, tile maxima are finite).
+    if (__any(tmax > mrun + p.lazy_thr)) {
+      const float mnew = fmaxf(mrun, tmax);
       const float corr = __builtin_amdgcn_exp2f((mrun - mnew) * p.qscale);
       lsum *= corr;
 #pragma unroll
@@ -483,6 +488,9 @@ hipError_t launch_attention(ActType t, const AttnArgs &a, hipStream_t s) {
   p.kv_index = a.kv_index; p.n_kv = a.n_kv;
   p.out = a.out; p.o_bs = a.o_bs; p.o_rs = a.o_rs;
   p.qscale = (float)(1.4426950408889634 / sqrt((double)a.head_dim));
+  // FLASHBON_ATTN_LAZY=0 (tests and tuning): rescale whenever a row maximum grows
+  const char *lazy = getenv("FLASHBON_ATTN_LAZY");
+  p.lazy_thr = lazy && !strcmp(lazy, "0") ? 0.0f : 8.0f / p.qscale;
   if (t == ACT_BF16 && a.head_dim == fa::DH) {
     dim3 grid((p.tq + fa::QB - 1) / fa::QB, p.heads, p.batch);
     const char *sel = getenv("FLASHBON_ATTN");   // "mfma": the unpipelined kernel (tuning)

@@ -201,6 +201,29 @@ def test_attention_mfma_kernels_tile_edges(kernel, tq, tk, monkeypatch):
     assert rel_l2(got, ref) <= 1e-2
 
 
+@pytest.mark.parametrize("lazy", ["1", "0"])
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_attention_lazy_rescale_moving_maximum(lazy, order, monkeypatch):
+    """Keys scaled so that the logits grow (or shrink) by far more than the lazy-rescale margin from
+    one 64-key tile to the next: with "rising" the running maximum has to move on every tile, with
+    "falling" only on the first.  Both settings of FLASHBON_ATTN_LAZY match the fp64 softmax."""
+    monkeypatch.setenv("FLASHBON_ATTN_LAZY", lazy)
+    F = fb()
+    heads, dh, tq, tk = 2, 128, 130, 321
+    D = heads * dh
+    q = _operand((1, tq, D), 61, "bf16")
+    ramp = np.linspace(0.5, 12.0, tk) if order == "rising" else np.linspace(12.0, 0.5, tk)
+    k = synth.round_to_bf16(_operand((tk, D), 62, "bf16") * ramp[:, None].astype(np.float32))
+    v = _operand((tk, D), 63, "bf16")
+    out = torch.empty((1, tq, D), device="cuda", dtype=torch.bfloat16)
+    F.flashbon_op_attention(F.BF16, 1, heads, dh, tq, tk, _dev(q, "bf16"), tq * D, D, _dev(k, "bf16"),
+                            _dev(v, "bf16"), tk * D, D, None, 0, out, tq * D, D)
+    torch.cuda.synchronize()
+    got = out[0].float().cpu().numpy()
+    assert np.isfinite(got).all()
+    assert rel_l2(got, _attn_ref(q[0], k, v, heads)) <= 1e-2
+
+
 @pytest.mark.parametrize("B,heads,T,tk", [(16, 12, 1560, 1560), (16, 12, 1560, 512), (4, 40, 4096, 4096)])
 def test_attention_full_shapes_bf16_sampled_queries(B, heads, T, tk):
     F = fb()
