@@ -533,9 +533,10 @@ __host__ __device__ constexpr int vmcnt_imm(int n) {   // s_waitcnt vmcnt(n), ex
   return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00;
 }
 
+// One (32 WTA)x256 tile at rows m0.., columns n0.. (the body of k_linear_dma).
 template <int EPI, typename TO, int WTA>
-__global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, const bf16 *__restrict__ A,
-                                                const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT) {
+__device__ __forceinline__ void dma_tile(int M, int N, int K, const bf16 *__restrict__ A, const bf16 *__restrict__ Wt,
+                                         const EpiArgs &e, int m0, int n0, bf16 *smem) {
   using namespace mf;
   static_assert(WTA >= 4 && WTA <= 8, "tile height 128..256");
   constexpr int BM = 32 * WTA, BN = 256, WT = 8;
@@ -543,13 +544,9 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
   constexpr int NL = WTA + 8;      // load instructions per wave per K tile (A rows, then W rows)
   constexpr int NR = WTA + 8;      // fragment reads per wave per substep (W, then A)
   constexpr int NS = 2 * WTA;      // MFMA groups of 4 per substep, the slots the reads and loads ride in
-  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  int mt, nt;
-  tile_of(blockIdx.x, MT, NT, mt, nt);
-  const int m0 = mt * BM, n0 = nt * BN;
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
   const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
   // load x of this wave: x < WTA -> A rows 8 WTA wave + 8 x .. + 7, else W rows 64 wave + 8 (x - WTA)
@@ -658,6 +655,29 @@ __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, cons
   substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
   tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 128 * wn, fr, fq);
 }
+
+// MT row blocks x NT column tiles of 256.  Row blocks come in two heights: `tall` of them 32 WTA rows
+// high and the rest 32 (WTA - 1), the tall ones spread evenly over the block index (block i is tall
+// when floor((i + 1) tall / MT) > floor(i tall / MT)), so that every XCD's range of tiles holds its
+// share.  tall == MT is a launch of one height.  Mixing two heights lets a launch fill whole rounds
+// of the chip with tiles of nearly equal duration.
+template <int EPI, typename TO, int WTA>
+__global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, const bf16 *__restrict__ A,
+                                                const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT, int tall) {
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  int mt, nt;
+  mf::tile_of(blockIdx.x, MT, NT, mt, nt);
+  const int before = (int)((int64_t)mt * tall / MT), upto = (int)((int64_t)(mt + 1) * tall / MT);
+  const int m0 = 32 * ((WTA - 1) * mt + before), n0 = nt * 256;
+  if (m0 >= M) return;   // a block past the last row (a forced plan with more blocks than M needs)
+  if constexpr (WTA > 4) {
+    if (upto == before) {
+      dma_tile<EPI, TO, WTA - 1>(M, N, K, A, Wt, e, m0, n0, smem);
+      return;
+    }
+  }
+  dma_tile<EPI, TO, WTA>(M, N, K, A, Wt, e, m0, n0, smem);
+}
 // ---------------------------------------------------------------------------------- VALU path
 template <typename TI, int EPI, typename TO>
 __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const TI *__restrict__ A,
@@ -704,55 +724,94 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
 // Tile choice for bf16 operands.  The 256x256 kernel runs one workgroup per CU, the 128x128 kernel
 // two; a launch takes ceil(tiles / slots) rounds.  Measured on MI355X, a round of 128x128 tiles
 // costs 0.64 of a round of 256x256 tiles at the same K (so the small tile does 0.78 of the big
-// tile's work per CU).  Candidates: all 256x256; all 128x128; or the whole rows of 256x256 tiles
-// that fill complete rounds plus the remaining rows as 128x128 tiles (a second launch), which
-// trims a last round that would leave most CUs idle.
-enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT };
+// tile's work per CU).  Candidates: all 256x256; all 128x128; the whole rows of 256x256 tiles that
+// fill complete rounds plus the remaining rows as 128x128 tiles (a second launch), which trims a
+// last round that would leave most CUs idle; and the 4-wave kernel with row blocks of two adjacent
+// heights (32 w and 32 (w - 1) rows), as many blocks as fill whole rounds.
+enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT, PLAN_MIX };
 struct TileChoice {
   TilePlan plan;
-  int wta;    // PLAN_BIG with the 4-wave kernel: tile height 32 wta
+  int wta;    // PLAN_BIG / PLAN_MIX with the 4-wave kernel: the taller height, 32 wta rows
   int rows;   // PLAN_SPLIT: rows on 256x256 tiles
+  int mb;     // PLAN_MIX: row blocks
+  int tall;   // PLAN_MIX: row blocks of the taller height (the others are 32 (wta - 1) rows)
 };
 static int cu_count();
 
-// Round-count model, in units of one K step of a 256x256 round: a launch takes ceil(tiles / CUs)
-// rounds; a round of 256x256 tiles costs K + kFix (kFix: per-tile prologue and epilogue), of 224x256
-// tiles k224 K + kFix, of 128x128 tiles (two per CU) kSmallA K + kSmallFix.  Fitted to the 1.3B-shaped
-// projections at M = 24960 (K = 1536 and 8960).  Picks the cheapest of: one launch of 256- or 224-row
-// tiles, one launch of 128x128 tiles, or 256x256 tiles on the rows that fill whole rounds plus 128x128
-// tiles on the rest.
+// Round-count model, in units of one K step of a 256x256 round: a launch takes ceil(tiles / slots)
+// rounds; a round of 4-wave tiles 32 w rows high costs kF[w] K + kG (the constant: per-tile prologue
+// and epilogue), of 128x128 tiles (two per CU) kSmallA K + kSmallFix.  Measured on MI355X at
+// M = 24960, K = 1536 and 8960: per round, 224-row tiles take 0.85 of the time of 256-row tiles
+// (for 0.875 of the rows), 192-row tiles 0.82, 160-row tiles 0.79.  The plans of one height are
+// compared first.  A launch of two heights spreads its taller tiles over all rounds and lets CUs
+// that finish a shorter tile early take the next one; it is costed at the block-weighted mean of
+// the two heights, and taken only when that beats the best one-height plan by more than kMixGain
+// (mixed launches measured a few percent slower than this estimate at wide N).
+static constexpr double kF[9] = {0, 0, 0, 0, 0, 0.79, 0.82, 0.85, 1.0};
+static constexpr double kG = 130.0, kMixGain = 0.02;
 static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
-  // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", "bm:224" (4-wave kernel with
-  // 224-row tiles), or "split:<rows>" (rows a multiple of 256 with 0 < rows < M: the first rows on
-  // 256x256 tiles, the rest on 128x128 tiles)
+  // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", "bm:<rows>" (4-wave kernel, one
+  // tile height: rows 160, 192 or 224), "mix:<w>:<blocks>:<tall>" (4-wave kernel, `blocks` row blocks,
+  // `tall` of them 32 w rows high and the rest 32 (w - 1), w in 6..8, covering M), or
+  // "split:<rows>" (rows a multiple of 256 with 0 < rows < M: the first rows on 256x256 tiles, the
+  // rest on 128x128 tiles)
   const char *force = getenv("FLASHBON_LINEAR_TILE");
   if (force) {
     if (!strncmp(force, "split:", 6)) {
       const int rows = atoi(force + 6);
-      if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) return {PLAN_SPLIT, 8, rows};
-      return {PLAN_BIG, 8, 0};
+      if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) return {PLAN_SPLIT, 8, rows, 0, 0};
+      return {PLAN_BIG, 8, 0, 0, 0};
     }
-    if (!strcmp(force, "bm:224")) return {PLAN_BIG, dma_ok ? 7 : 8, 0};
-    return {strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL, 8, 0};
+    if (dma_ok && !strncmp(force, "bm:", 3)) {
+      const int rows = atoi(force + 3);
+      if (rows == 160 || rows == 192 || rows == 224) {
+        const int w = rows / 32, mb = (M + rows - 1) / rows;
+        return {PLAN_MIX, w + 1, 0, mb, 0};   // all blocks of the shorter height of the w + 1 kernel
+      }
+    }
+    if (dma_ok && !strncmp(force, "mix:", 4)) {
+      int w = 0, mb = 0, tall = 0;
+      if (sscanf(force + 4, "%d:%d:%d", &w, &mb, &tall) == 3 && w >= 6 && w <= 8 && mb > 0 && tall >= 0 &&
+          tall <= mb && 32 * ((int64_t)(w - 1) * mb + tall) >= M)
+        return {PLAN_MIX, w, 0, mb, tall};
+    }
+    return {strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL, 8, 0, 0, 0};
   }
-  constexpr double kFix = 358.0, k224 = 0.92, kSmallA = 0.704, kSmallFix = 604.0;
+  constexpr double kSmallA = 0.704, kSmallFix = 604.0;
   const int cus = cu_count();
   auto rounds = [&](int64_t tiles, int per_cu) { return (double)((tiles + per_cu * cus - 1) / (per_cu * cus)); };
+  auto cost = [&](int w) { return kF[w] * K + kG; };
   const int64_t NT = (N + 255) / 256, T = (int64_t)((M + 255) / 256) * NT, NT2 = (N + 127) / 128;
-  const double big = K + kFix, small = kSmallA * K + kSmallFix;
-  TileChoice best = {PLAN_BIG, 8, 0};
+  const double big = cost(8), small = kSmallA * K + kSmallFix;
+  TileChoice best = {PLAN_BIG, 8, 0, 0, 0};
   double t_best = rounds(T, 1) * big;
   if (dma_ok) {
-    const double t = rounds((int64_t)((M + 223) / 224) * NT, 1) * (k224 * K + kFix);
-    if (t < t_best) { t_best = t; best = {PLAN_BIG, 7, 0}; }
+    for (int w = 7; w >= 5; --w) {   // one height, 32 w rows: the kernel for w + 1 with no tall blocks
+      const int mb = (M + 32 * w - 1) / (32 * w);
+      const double t = rounds((int64_t)mb * NT, 1) * cost(w);
+      if (t < t_best) { t_best = t; best = {PLAN_MIX, w + 1, 0, mb, 0}; }
+    }
   }
   const double t_small = rounds((int64_t)((M + 127) / 128) * NT2, 2) * small;
-  if (t_small < t_best) { t_best = t_small; best = {PLAN_SMALL, 8, 0}; }
+  if (t_small < t_best) { t_best = t_small; best = {PLAN_SMALL, 8, 0, 0, 0}; }
   const int64_t mt_big = (T - T % cus) / NT;
   const int rows = (int)(mt_big * 256);
   if (K % mf::BK == 0 && rows > 0 && rows < M) {
     const double t_split = rounds(mt_big * NT, 1) * big + rounds(((M - rows + 127) / 128) * NT2, 2) * small;
-    if (t_split < t_best) { t_best = t_split; best = {PLAN_SPLIT, 8, rows}; }
+    if (t_split < t_best) { t_best = t_split; best = {PLAN_SPLIT, 8, rows, 0, 0}; }
+  }
+  if (dma_ok) {
+    const double t_pure = t_best;
+    for (int w = 7; w >= 6; --w) {   // two heights, 32 w and 32 (w - 1) rows
+      const int lo = 32 * (w - 1);
+      const int mb_min = (M + 32 * w - 1) / (32 * w), mb_max = (M + lo - 1) / lo;
+      for (int mb = mb_min; mb <= mb_max; ++mb) {
+        const int tall = max(0, (int)(((int64_t)M - (int64_t)lo * mb + 31) / 32));
+        if (tall == 0 || tall == mb) continue;
+        const double t = rounds((int64_t)mb * NT, 1) * ((double)tall * cost(w) + (double)(mb - tall) * cost(w - 1)) / mb;
+        if (t < (1.0 - kMixGain) * t_pure && t < t_best) { t_best = t; best = {PLAN_MIX, w, 0, mb, tall}; }
+      }
+    }
   }
   return best;
 }
@@ -776,9 +835,10 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
   return hipGetLastError();
 }
 
+// The 4-wave kernel over mb row blocks, `tall` of them 32 WTA rows high, the rest 32 (WTA - 1).
 template <int EPI, int WTA>
 static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
-                             hipStream_t s) {
+                             hipStream_t s, int mb, int tall) {
   constexpr int BM = 32 * WTA;
   const size_t lds = (size_t)2 * (BM + 256) * mf::BK * sizeof(bf16);
   auto kern = k_linear_dma<EPI, bf16, WTA>;
@@ -788,9 +848,9 @@ static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt,
     if (err != hipSuccess) return err;
     attr_set = true;
   }
-  const int MT = (M + BM - 1) / BM, NT = (N + 255) / 256;
-  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(256), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
-                     MT, NT);
+  const int NT = (N + 255) / 256;
+  hipLaunchKernelGGL(kern, dim3(mb * NT), dim3(256), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
+                     mb, NT, tall);
   return hipGetLastError();
 }
 
@@ -821,11 +881,11 @@ static EpiArgs rows_from(const EpiArgs &e, int m) {
 // 8-wave kernel (K % 64 != 0, K < 128 or N % 8 != 0, and the latent scatter, which stays on 2 waves
 // per SIMD).
 template <int EPI>
-static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s,
-                             int wta) {
+static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s) {
   if constexpr (EPI != EPI_EULER) {
     if (K % mf::BK == 0 && K >= 2 * mf::BK && N % 8 == 0) {
-      return wta == 7 ? launch_dma<EPI, 7>(M, N, K, A, Wt, e, s) : launch_dma<EPI, 8>(M, N, K, A, Wt, e, s);
+      const int mb = (M + 255) / 256;
+      return launch_dma<EPI, 8>(M, N, K, A, Wt, e, s, mb, mb);
     }
   }
   return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
@@ -837,10 +897,17 @@ static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, cons
   if (t == ACT_BF16) {
     const bool dma_ok = EPI != EPI_EULER && K % mf::BK == 0 && K >= 2 * mf::BK && N % 8 == 0;
     TileChoice c = pick_tiles(M, N, K, dma_ok);
-    if (c.plan == PLAN_SPLIT && EPI == EPI_EULER) c = {PLAN_BIG, 8, 0};   // the latent scatter needs whole rows
+    if (c.plan == PLAN_SPLIT && EPI == EPI_EULER) c = {PLAN_BIG, 8, 0, 0, 0};   // the latent scatter needs whole rows
     if (c.plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
-    if (c.plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s, c.wta);
-    hipError_t err = launch_big<EPI>(c.rows, N, K, A, Wt, e, s, 8);
+    if (c.plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s);
+    if constexpr (EPI != EPI_EULER) {
+      if (c.plan == PLAN_MIX) {
+        if (c.wta == 8) return launch_dma<EPI, 8>(M, N, K, A, Wt, e, s, c.mb, c.tall);
+        if (c.wta == 7) return launch_dma<EPI, 7>(M, N, K, A, Wt, e, s, c.mb, c.tall);
+        return launch_dma<EPI, 6>(M, N, K, A, Wt, e, s, c.mb, c.tall);
+      }
+    }
+    hipError_t err = launch_big<EPI>(c.rows, N, K, A, Wt, e, s);
     if (err != hipSuccess) return err;
     return launch_mfma<4, 4, 2, 2, EPI, 2>(M - c.rows, N, K, (const bf16 *)A + (size_t)c.rows * K, Wt,
                                            rows_from<EPI>(e, c.rows), s);

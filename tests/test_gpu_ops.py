@@ -83,15 +83,18 @@ def test_linear_small(dtype, M, N, K, epi):
     assert rel_l2(got, ref) <= tol
 
 
-@pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256", "bm:224"])
+@pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256", "bm:224", "bm:192", "bm:160", "mix:7:3:1",
+                                  "mix:8:3:1", "mix:6:4:2"])
 @pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
                                    (520, 776, 1024)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
 def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
     """Every MFMA tiling (forced: "256x256" is the 4-wave kernel with LDS-writing loads when K % 64 == 0
     and K >= 128, else the 8-wave kernel; "split:256" puts rows 0..255 on 256x256 tiles and the rest
-    on 128x128 tiles, when M > 256 and K % 64 == 0; "bm:224" the 4-wave kernel with 224-row tiles)
-    on ragged M, N and K tails, against the oracle.
+    on 128x128 tiles, when M > 256 and K % 64 == 0; "bm:<rows>" the 4-wave kernel with tiles of one
+    height; "mix:w:blocks:tall" the 4-wave kernel with row blocks of two heights, 32 w and 32 (w - 1)
+    rows, spread over the blocks; plans the shape cannot take fall back to 256x256) on ragged M, N
+    and K tails, against the oracle.
     The residual case also writes the cache copy."""
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
     F = fb()
@@ -115,6 +118,34 @@ def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
         assert torch.equal(cache, out)
     torch.cuda.synchronize()
     assert rel_l2(out.float().cpu().numpy(), ref) <= tol
+
+
+@pytest.mark.parametrize("epi", ["store", "residual"])
+def test_linear_tile_plans_bit_identical(epi, monkeypatch):
+    """Every tiling accumulates K in the same order, so an output element does not depend on the tile
+    that computed it: all plans give bit-identical results (this is what keeps a candidate's draft
+    independent of its position in the pool)."""
+    F = fb()
+    M, N, K = 1100, 776, 512
+    A = _dev(_operand((M, K), 81, "bf16"), "bf16")
+    W = _dev(_operand((N, K), 82, "bf16", 0.05), "bf16")
+    bias = _dev(synth.random_matrix((N,), 83), "fp32")
+    gate = _dev(synth.random_matrix((N,), 84), "fp32")
+    h0 = _dev(synth.random_matrix((M, N), 85), "fp32")
+    outs = []
+    for tile in ["256x256", "128x128", "split:512", "bm:224", "bm:192", "bm:160", "mix:7:6:1", "mix:8:5:1",
+                 "mix:6:7:3"]:
+        monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
+        if epi == "store":
+            out = torch.empty((M, N), device="cuda", dtype=torch.float32)
+            F.flashbon_op_linear(F.BF16, M, N, K, A, W, bias, F.EPI_STORE_F32, out)
+        else:
+            out = h0.clone()
+            F.flashbon_op_linear(F.BF16, M, N, K, A, W, bias, F.EPI_RESIDUAL, out, gate)
+        torch.cuda.synchronize()
+        outs.append(out)
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
 
 
 @pytest.mark.parametrize("M,N,K", [(24960, 4608, 1536), (24960, 8960, 1536), (24960, 1536, 8960),
