@@ -32,6 +32,15 @@ flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t 
                                    const void *W, const float *bias, int32_t epilogue, void *out,
                                    const float *gate, float *cache_out, void *stream);
 
+/* The tile plan flashbon_op_linear (and every projection of the draft step) takes for this shape,
+ * without launching anything or touching the GPU: *kernels = the number of kernel launches, desc =
+ * a NUL-terminated one-line description of the kernels and tiles (truncated to desc_len - 1
+ * characters; desc may be NULL).  Same argument rules as flashbon_op_linear; follows the
+ * FLASHBON_LINEAR_TILE override like the launch does.  The plan depends on the device's CU count
+ * (256 when no device is visible). */
+flashbon_status flashbon_op_linear_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue,
+                                        int32_t *kernels, char *desc, int32_t desc_len);
+
 /* Multi-head softmax attention, softmax(q k^T / sqrt(head_dim)) v per (batch b, head h):
  * q row i of batch b, head h is at q + b*q_batch_stride + i*q_row_stride + h*head_dim (act);
  * k/v row j at k/v + kvb*kv_batch_stride + j*kv_row_stride + h*head_dim, where kvb = b, or

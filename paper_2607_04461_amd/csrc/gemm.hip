@@ -12,7 +12,9 @@
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
+#include <string>
 #include <type_traits>
 
 #include "common.h"
@@ -916,6 +918,43 @@ static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, cons
   hipLaunchKernelGGL((k_linear_valu<float, EPI, float>), grid, dim3(256), 0, s, M, N, K,
                      (const float *)A, (const float *)Wt, e);
   return hipGetLastError();
+}
+
+int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len) {
+  std::string d;
+  int kernels = 1;
+  auto rows_of = [](int w) { return std::to_string(32 * w); };
+  if (t != ACT_BF16) {
+    d = "k_linear_valu: 64x64 tiles, fp32 vector ALUs";
+  } else {
+    const bool dma_ok = epi != EPI_EULER && K % mf::BK == 0 && K >= 2 * mf::BK && N % 8 == 0;
+    TileChoice c = pick_tiles(M, N, K, dma_ok);
+    if (c.plan == PLAN_SPLIT && epi == EPI_EULER) c = {PLAN_BIG, 8, 0, 0, 0};
+    const std::string nt = std::to_string((N + 255) / 256);
+    if (c.plan == PLAN_SMALL) {
+      d = "k_linear_mfma: 128x128 tiles, 4 waves, two workgroups per CU";
+    } else if (c.plan == PLAN_BIG) {
+      d = dma_ok ? "k_linear_dma: 256x256 tiles, " + std::to_string((M + 255) / 256) + " row blocks x " + nt
+                 : std::string("k_linear_mfma: 256x256 tiles, 8 waves");
+    } else if (c.plan == PLAN_MIX) {
+      const std::string blocks = std::to_string(c.mb) + " row blocks x " + nt;
+      if (c.tall == c.mb) d = "k_linear_dma: " + rows_of(c.wta) + "x256 tiles, " + blocks;
+      else if (c.tall == 0) d = "k_linear_dma: " + rows_of(c.wta - 1) + "x256 tiles, " + blocks;
+      else
+        d = "k_linear_dma: " + blocks + ", " + std::to_string(c.tall) + " of " + rows_of(c.wta) + " rows and " +
+            std::to_string(c.mb - c.tall) + " of " + rows_of(c.wta - 1);
+    } else {
+      kernels = 2;
+      d = "k_linear_dma: 256x256 tiles on rows 0.." + std::to_string(c.rows - 1) +
+          " + k_linear_mfma: 128x128 tiles on the remaining " + std::to_string(M - c.rows) + " rows";
+    }
+  }
+  if (buf && len > 0) {
+    const size_t n = std::min((size_t)len - 1, d.size());
+    memcpy(buf, d.data(), n);
+    buf[n] = 0;
+  }
+  return kernels;
 }
 
 hipError_t launch_linear(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt,

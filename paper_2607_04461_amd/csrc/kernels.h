@@ -35,6 +35,9 @@ struct EpiArgs {
 // C[m][n] = sum_k A[m][k] * Wt[n][k] (+ epilogue).  K % 8 == 0.
 hipError_t launch_linear(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt,
                          const EpiArgs &e, hipStream_t s);
+// The kernels launch_linear would use for this shape, without launching: returns the number of
+// launches and writes a NUL-terminated description (truncated to len - 1 characters) into buf.
+int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len);
 
 struct AttnArgs {
   int batch, heads, head_dim, tq, tk;

@@ -34,6 +34,17 @@ flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t 
   return launched(launch_linear(t, epilogue, M, N, K, A, W, e, (hipStream_t)stream), "linear");
 }
 
+flashbon_status flashbon_op_linear_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue,
+                                        int32_t *kernels, char *desc, int32_t desc_len) {
+  if (dtype != FLASHBON_FP32 && dtype != FLASHBON_BF16) return fail(FLASHBON_EINVAL, "bad dtype");
+  if (M < 1 || N < 1 || K < 1 || K % 8 || N % 4 || K > 65536)
+    return fail(FLASHBON_ESHAPE, "need M,N,K >= 1, K <= 65536, K % 8 == 0, N % 4 == 0");
+  if (epilogue < FLASHBON_EPI_STORE || epilogue > FLASHBON_EPI_RESIDUAL) return fail(FLASHBON_EINVAL, "bad epilogue");
+  if (!kernels || (desc && desc_len < 1)) return fail(FLASHBON_EINVAL, "kernels is required; desc_len >= 1 with desc");
+  *kernels = describe_linear(dtype == FLASHBON_BF16 ? ACT_BF16 : ACT_F32, epilogue, M, N, K, desc, desc ? desc_len : 0);
+  return FLASHBON_OK;
+}
+
 flashbon_status flashbon_op_attention(int32_t dtype, int32_t batch, int32_t heads, int32_t head_dim,
                                       int32_t tq, int32_t tk, const void *q, int64_t q_batch_stride,
                                       int64_t q_row_stride, const void *k, const void *v,

@@ -68,7 +68,7 @@ class StepArgs(ctypes.Structure):
 EXPORTS = [
     "flashbon_weight_count", "flashbon_init_model", "flashbon_text_kv_bytes", "flashbon_cache_bytes",
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
-    "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_attention", "flashbon_op_ln_mod",
+    "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_linear_plan", "flashbon_op_attention", "flashbon_op_ln_mod",
     "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde", "flashbon_select",
 ]
 
@@ -114,6 +114,8 @@ def load() -> ctypes.CDLL:
     L.flashbon_last_error.restype = ctypes.c_char_p
     L.flashbon_op_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
     L.flashbon_op_linear.restype = i32
+    L.flashbon_op_linear_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_char_p, i32]
+    L.flashbon_op_linear_plan.restype = i32
     L.flashbon_op_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, i64, i64, vp, vp, i64, i64,
                                         vp, i32, vp, i64, i64, vp]
     L.flashbon_op_attention.restype = i32
@@ -323,6 +325,15 @@ def flashbon_read_timing(model: int, site: str):
 def flashbon_op_linear(dtype, M, N, K, A, W, bias, epilogue, out, gate=None, cache_out=None, stream=None):
     _check(load().flashbon_op_linear(dtype, M, N, K, _ptr(A), _ptr(W), _ptr(bias), epilogue, _ptr(out),
                                      _ptr(gate), _ptr(cache_out), _stream(stream)), "flashbon_op_linear")
+
+
+def flashbon_op_linear_plan(dtype, M, N, K, epilogue):
+    """(number of kernel launches, description) of the tile plan flashbon_op_linear takes."""
+    n = ctypes.c_int32()
+    buf = ctypes.create_string_buffer(256)
+    _check(load().flashbon_op_linear_plan(dtype, M, N, K, epilogue, ctypes.byref(n), buf, len(buf)),
+           "flashbon_op_linear_plan")
+    return n.value, buf.value.decode()
 
 
 def flashbon_op_attention(dtype, batch, heads, head_dim, tq, tk, q, q_bs, q_rs, k, v, kv_bs, kv_rs,

@@ -193,3 +193,49 @@ def test_select_rejects_bad_arguments():
         raise KeyError("verifier down")
     with pytest.raises(KeyError):
         fb.flashbon_select([5, 6, 7, 8], broken)
+
+
+@pytest.mark.parametrize("shape,kernels,desc", [
+    ((24960, 4608, 1536, 0), 1, "k_linear_dma: 224x256 tiles, 112 row blocks x 18"),
+    ((24960, 8960, 1536, 1), 1, "k_linear_dma: 224x256 tiles, 112 row blocks x 35"),
+    ((24960, 1536, 1536, 3), 1, "k_linear_dma: 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
+    ((24960, 1536, 8960, 3), 1, "k_linear_dma: 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
+    ((16384, 15360, 5120, 0), 1, "k_linear_dma: 256x256 tiles, 64 row blocks x 60"),
+    ((200, 136, 72, 0), 1, "k_linear_mfma: 256x256 tiles, 8 waves"),
+])
+def test_linear_plan_of_model_shapes(shape, kernels, desc, monkeypatch):
+    """The tile plan is a host decision (no device needed; 256 CUs assumed without one).  At the
+    1.3B-shaped pool's M = 16 x 1560 rows: QKV and MLP up on 224-row tiles, the N = 1536 projections
+    on 128 row blocks of 224 and 192 rows that fill three rounds exactly; K % 64 != 0 takes the
+    generic 8-wave kernel."""
+    monkeypatch.delenv("FLASHBON_LINEAR_TILE", raising=False)
+    assert fb.flashbon_op_linear_plan(fb.BF16, *shape) == (kernels, desc)
+    # the row blocks named cover M with no block starting past it
+    m = re.search(r"(\d+) row blocks x \d+, (\d+) of (\d+) rows and (\d+) of (\d+)", desc)
+    if m:
+        mb, tall, hi, short, lo = map(int, m.groups())
+        assert tall + short == mb and hi == lo + 32
+        total = tall * hi + short * lo
+        assert shape[0] <= total < shape[0] + lo
+
+
+def test_linear_plan_follows_override_and_rejects_bad_arguments(monkeypatch):
+    monkeypatch.setenv("FLASHBON_LINEAR_TILE", "split:24320")
+    n, d = fb.flashbon_op_linear_plan(fb.BF16, 24960, 8960, 1536, 1)
+    assert n == 2 and "rows 0..24319" in d and "remaining 640 rows" in d
+    monkeypatch.setenv("FLASHBON_LINEAR_TILE", "mix:7:128:12")
+    assert fb.flashbon_op_linear_plan(fb.BF16, 24960, 1536, 1536, 3)[1] == \
+        "k_linear_dma: 128 row blocks x 6, 12 of 224 rows and 116 of 192"
+    monkeypatch.setenv("FLASHBON_LINEAR_TILE", "mix:7:100:0")    # does not cover M: ignored
+    assert "256x256" in fb.flashbon_op_linear_plan(fb.BF16, 24960, 1536, 1536, 3)[1]
+    monkeypatch.delenv("FLASHBON_LINEAR_TILE")
+    assert fb.flashbon_op_linear_plan(fb.FP32, 100, 64, 64, 0)[1].startswith("k_linear_valu")
+    lib = fb.load()
+    n = ctypes.c_int32()
+    buf = ctypes.create_string_buffer(8)
+    for args in [(fb.BF16, 0, 64, 64, 0), (fb.BF16, 64, 62, 64, 0), (fb.BF16, 64, 64, 12, 0), (7, 64, 64, 64, 0),
+                 (fb.BF16, 64, 64, 64, 4)]:
+        assert lib.flashbon_op_linear_plan(*args, ctypes.byref(n), buf, len(buf)) != 0
+    assert lib.flashbon_op_linear_plan(fb.BF16, 64, 64, 64, 0, None, buf, len(buf)) != 0
+    assert lib.flashbon_op_linear_plan(fb.BF16, 64, 64, 64, 0, ctypes.byref(n), buf, len(buf)) == 0
+    assert len(buf.value) == 7    # truncated to desc_len - 1 characters
