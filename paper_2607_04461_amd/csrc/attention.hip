@@ -351,14 +351,17 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
     for (int j = 0; j < 16; ++j) o[dt][j] = 0.f;
   float mrun = -INFINITY, lsum = 0.f;
 
-  // S^T of the tile in K stage st: lane holds query li, keys 32 sl + (j/4)*8 + 4 g + (j%4)
+  // S^T of the tile in K stage st: lane holds query li, keys 32 sl + (j/4)*8 + 4 g + (j%4).  The two
+  // slabs' accumulations alternate, so consecutive MFMAs never wait on each other's result.
   auto scores = [&](int st, f32x16 (&sc)[2]) {
 #pragma unroll
-    for (int sl = 0; sl < 2; ++sl) {
+    for (int sl = 0; sl < 2; ++sl)
 #pragma unroll
       for (int j = 0; j < 16; ++j) sc[sl][j] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
+    for (int ks = 0; ks < 8; ++ks) {
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(lds + K_OFF + st * TILE_B + sl * 32 * DH * 2 + ko[ks]);
         sc[sl] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[sl], 0, 0, 0);
       }
