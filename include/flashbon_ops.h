@@ -32,6 +32,16 @@ flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t 
                                    const void *W, const float *bias, int32_t epilogue, void *out,
                                    const float *gate, float *cache_out, void *stream);
 
+/* Residual linear layer reading the residual rows from a separate buffer:
+ * out[m][n] = residual_in[m][n] + gate[n] * (acc[m][n] + bias[n]) (gate NULL -> 1), acc as in
+ * flashbon_op_linear (a block's gated residual update, Eq. 7, with the input stream and the output in
+ * different buffers).  residual_in: device fp32 [M][N], read only; it may be out itself (then this is
+ * flashbon_op_linear with FLASHBON_EPI_RESIDUAL) and must not otherwise overlap out.  out: device
+ * fp32 [M][N].  Shape rules and errors as flashbon_op_linear; residual_in and out are required. */
+flashbon_status flashbon_op_linear_residual(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
+                                            const void *W, const float *bias, const float *gate,
+                                            const float *residual_in, float *out, void *stream);
+
 /* The tile plan flashbon_op_linear (and every projection of the draft step) takes for this shape,
  * without launching anything or touching the GPU: *kernels = the number of kernel launches, desc =
  * a NUL-terminated one-line description of the kernels and tiles (truncated to desc_len - 1

@@ -48,7 +48,7 @@ __device__ __forceinline__ void epilogue4(const EpiArgs &e, int m, int n, float 
     *reinterpret_cast<float4 *>(o) = make_float4(v[0], v[1], v[2], v[3]);
   } else if constexpr (EPI == EPI_RESIDUAL) {
     float *o = reinterpret_cast<float *>(e.out) + (int64_t)m * e.ldo + n;
-    float4 h = *reinterpret_cast<float4 *>(o);
+    float4 h = *reinterpret_cast<const float4 *>(e.res_in ? e.res_in + (int64_t)m * e.ldo + n : o);
     if (e.gate) {
       float4 g = *reinterpret_cast<const float4 *>(e.gate + n);
       h.x += g.x * v[0]; h.y += g.y * v[1]; h.z += g.z * v[2]; h.w += g.w * v[3];
@@ -118,7 +118,8 @@ __device__ __forceinline__ void epilogue8(const EpiArgs &e, int m, int n, const 
       reinterpret_cast<float4 *>(o)[1] = make_float4(v[4], v[5], v[6], v[7]);
     } else if constexpr (EPI == EPI_RESIDUAL) {
       float *o = reinterpret_cast<float *>(e.out) + (int64_t)m * e.ldo + n;
-      float4 h0 = reinterpret_cast<float4 *>(o)[0], h1 = reinterpret_cast<float4 *>(o)[1];
+      const float4 *hi = reinterpret_cast<const float4 *>(e.res_in ? e.res_in + (int64_t)m * e.ldo + n : o);
+      float4 h0 = hi[0], h1 = hi[1];
       if (e.gate) {
         float4 g0 = *reinterpret_cast<const float4 *>(e.gate + n);
         float4 g1 = *reinterpret_cast<const float4 *>(e.gate + n + 4);
@@ -178,8 +179,8 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
 // block rb the lane owns row mbase + RS rb + r0 and, in column group cg, the 8 consecutive columns
 // nbase + col(cg) .. + 7 with values val(cg, rb, q), q = 0..7 (two 4-column halves).
 
-// Residual update h += gate (acc + bias), optional cache write (CM 1: copy of the new row, CM 2: new
-// row minus what the cache held).  Batches of JB row blocks of one column group; a column group's
+// Residual update out = in + gate (acc + bias), in = e.res_in or out itself, optional cache write
+// (CM 1: copy of the new row, CM 2: new row minus what the cache held).  Batches of JB row blocks of one column group; a column group's
 // bias and gate come with its first batch.  PIPE 2: the loads of batch x + 1 are issued before the
 // stores of batch x.
 template <int NCG, int NRB, int RS, int CM, int PIPE, int JB, typename Col, typename Val>
@@ -191,6 +192,7 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, in
   const int rows = max(0, min(M - mbase, RS * NRB));
   const uint32_t bytes = (uint32_t)rows * (uint32_t)e.ldo * 4u;
   const __amdgpu_buffer_rsrc_t rsO = rsrc((float *)e.out + (int64_t)mbase * e.ldo, bytes);
+  const __amdgpu_buffer_rsrc_t rsI = rsrc((e.res_in ? e.res_in : (const float *)e.out) + (int64_t)mbase * e.ldo, bytes);
   const __amdgpu_buffer_rsrc_t rsC = rsrc(CM ? e.cache + (int64_t)mbase * e.ldo : nullptr, CM ? bytes : 0u);
   const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
   const __amdgpu_buffer_rsrc_t rsG = rsrc(e.gate, e.gate ? (uint32_t)N * 4u : 0u);
@@ -219,8 +221,8 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, in
 #pragma unroll
     for (int jj = 0; jj < JB; ++jj) {
       const uint32_t r = ro + (uint32_t)(j0 + jj) * rstep;
-      h[buf][jj][0] = ld4(rsO, r + c0[cg]);
-      h[buf][jj][1] = ld4(rsO, r + c1[cg]);
+      h[buf][jj][0] = ld4(rsI, r + c0[cg]);
+      h[buf][jj][1] = ld4(rsI, r + c1[cg]);
       if constexpr (CM == 2) {
         c[buf][jj][0] = ld4(rsC, r + c0[cg]);
         c[buf][jj][1] = ld4(rsC, r + c1[cg]);
@@ -368,17 +370,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const bf16 *base, in
 }
 
 // Workgroup id -> (m tile, n tile).  Workgroups are dispatched round-robin over the 8 XCDs; each XCD
-// is given a contiguous range of tiles, and tiles are ordered in groups of GROUP_M m-tiles sweeping
-// all n-tiles, so the workgroups resident on one XCD share A rows and W rows in that XCD's L2.
+// is given a contiguous range of tiles, and tiles are ordered in groups of `group` m-tiles sweeping
+// all n-tiles, so the workgroups resident on one XCD share A rows and W rows in that XCD's L2
+// (group 1: every n-tile of one row block before the next row block).
 constexpr int GROUP_M = 8;
-__device__ __forceinline__ void tile_of(int bid, int MT, int NT, int &mt, int &nt) {
+__device__ __forceinline__ void tile_of(int bid, int MT, int NT, int &mt, int &nt, int group_m = GROUP_M) {
   const int total = MT * NT;
   const int xcd = bid & 7, local = bid >> 3;
   const int base = total >> 3, rem = total & 7;
   const int t = xcd * base + min(xcd, rem) + local;
-  const int per_group = GROUP_M * NT;
-  const int group = t / per_group, first_m = group * GROUP_M;
-  const int gm = min(MT - first_m, GROUP_M);
+  const int per_group = group_m * NT;
+  const int group = t / per_group, first_m = group * group_m;
+  const int gm = min(MT - first_m, group_m);
   const int r = t - group * per_group;
   mt = first_m + r % gm;
   nt = r / gm;
@@ -665,10 +668,11 @@ __device__ __forceinline__ void dma_tile(int M, int N, int K, const bf16 *__rest
 // of the chip with tiles of nearly equal duration.
 template <int EPI, typename TO, int WTA>
 __global__ __launch_bounds__(256, 1) void k_linear_dma(int M, int N, int K, const bf16 *__restrict__ A,
-                                                const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT, int tall) {
+                                                const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT, int tall,
+                                                int group_m) {
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   int mt, nt;
-  mf::tile_of(blockIdx.x, MT, NT, mt, nt);
+  mf::tile_of(blockIdx.x, MT, NT, mt, nt, group_m);
   const int before = (int)((int64_t)mt * tall / MT), upto = (int)((int64_t)(mt + 1) * tall / MT);
   const int m0 = 32 * ((WTA - 1) * mt + before), n0 = nt * 256;
   if (m0 >= M) return;   // a block past the last row (a forced plan with more blocks than M needs)
@@ -837,6 +841,22 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
   return hipGetLastError();
 }
 
+// Row blocks per tile group of the 4-wave kernel's order (see mf::tile_of).  Wide outputs keep
+// groups of 8 row blocks (the 32 tiles an XCD runs at once then span 8 row blocks x 4 column tiles).
+// Narrow outputs (at most 8 column tiles) take groups of 4, and with a long K groups of 1, so an
+// XCD runs every column tile of a row block together and each A row block (3.4 MB at K = 8960) is
+// fetched once rather than again in a later round.  Measured in the 1.3B-shaped draft (M = 24960):
+// the MLP down-projection (N = 1536, K = 8960) 68.5 -> 66.0 ms per draft with groups of 1, the
+// N = 1536, K = 1536 projections 17.2 -> 16.8 ms with groups of 4; QKV and MLP up are best at 8.
+// The order does not change any output.  FLASHBON_LINEAR_GROUP (tuning): a fixed group height.
+static int group_rows(int MT, int NT, int K) {
+  const char *force = getenv("FLASHBON_LINEAR_GROUP");
+  if (force && atoi(force) > 0) return atoi(force);
+  (void)MT;
+  if (NT <= 8) return K >= 4096 ? 1 : 4;
+  return mf::GROUP_M;
+}
+
 // The 4-wave kernel over mb row blocks, `tall` of them 32 WTA rows high, the rest 32 (WTA - 1).
 template <int EPI, int WTA>
 static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
@@ -852,7 +872,7 @@ static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt,
   }
   const int NT = (N + 255) / 256;
   hipLaunchKernelGGL(kern, dim3(mb * NT), dim3(256), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e,
-                     mb, NT, tall);
+                     mb, NT, tall, group_rows(mb, NT, K));
   return hipGetLastError();
 }
 
@@ -876,6 +896,7 @@ static EpiArgs rows_from(const EpiArgs &e, int m) {
   const size_t osz = (EPI == EPI_STORE || EPI == EPI_GELU) ? sizeof(bf16) : sizeof(float);
   r.out = (char *)e.out + (size_t)m * e.ldo * osz;
   if (r.cache) r.cache = e.cache + (size_t)m * e.ldo;
+  if (r.res_in) r.res_in = e.res_in + (size_t)m * e.ldo;
   return r;
 }
 

@@ -13,7 +13,7 @@ enum Epilogue {
   EPI_STORE = 0,      // out act  = acc + bias
   EPI_GELU = 1,       // out act  = gelu(acc + bias)
   EPI_STORE_F32 = 2,  // out fp32 = acc + bias
-  EPI_RESIDUAL = 3,   // out fp32 += gate * (acc + bias); optional cache copy of the result
+  EPI_RESIDUAL = 3,   // out fp32 = (res_in or out) + gate * (acc + bias); optional cache copy of the result
   EPI_EULER = 4       // latent z[scatter(m, n)] += dt * (acc + bias)   (head + unpatchify + Euler)
 };
 
@@ -22,6 +22,8 @@ struct EpiArgs {
   int64_t ldo = 0;
   const float *bias = nullptr; // [N] or null
   const float *gate = nullptr; // [N] or null (RESIDUAL)
+  const float *res_in = nullptr; // RESIDUAL: [M][ldo] fp32 rows added to (out = res_in + ...), or null:
+                                 // out is updated in place.  Read only; equal to out or disjoint from it.
   float *cache = nullptr;      // [M][ldo] fp32 or null (RESIDUAL)
   bool cache_delta = false;    // RESIDUAL: cache = updated out - cache (the cache held the block input)
   // EULER: z [n][C][H][W] fp32, tokens per candidate T = (H/p)(W/p), N = C p p

@@ -375,9 +375,15 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   }
 
   const int64_t MD = M * D;
+  // Where the residual stream currently lives.  A computed block of a draft step (output reading of
+  // the proxy) writes its new rows only into its cache slot, which then serves as the stream until the
+  // next block writes: the next computed block reads it there and its self-attention output
+  // projection writes the updated rows back into m->h; a proxy writes m->h; a skip leaves it.  This
+  // saves the second copy of every computed block's output.
+  const float *hcur = m->h;
   auto dump = [&](int idx) -> flashbon_status {
     if (!a->hidden_dump) return FLASHBON_OK;
-    HIPCHK(hipMemcpyAsync(a->hidden_dump + (int64_t)idx * MD, m->h, MD * 4, hipMemcpyDeviceToDevice, s), "hidden dump");
+    HIPCHK(hipMemcpyAsync(a->hidden_dump + (int64_t)idx * MD, hcur, MD * 4, hipMemcpyDeviceToDevice, s), "hidden dump");
     return FLASHBON_OK;
   };
   flashbon_status st;
@@ -410,6 +416,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       auto slot_ptr = [&](int sl) { return a->cache + ((int64_t)l * 3 + sl) * MD; };
       HIPCHK(timed(m, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s, residual); }),
              "activation proxy");
+      hcur = m->h;
       if ((st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
     }
@@ -418,7 +425,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     if (residual)
       HIPCHK(hipMemcpyAsync(a->cache + ((int64_t)l * 3 + tr.slot) * MD, m->h, MD * 4, hipMemcpyDeviceToDevice, s),
              "block input to cache");
-    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 0 * D, mod + 1 * D, m->a, s); }), "adaLN 1");
+    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, mod + 0 * D, mod + 1 * D, m->a, s); }), "adaLN 1");
     {
       EpiArgs e; e.out = m->qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
       HIPCHK(timed(m, FLASHBON_SITE_QKV, s, [&] { return launch_linear(act, EPI_STORE, (int)M, 3 * D, D, m->a, Wp(b.wqkv), e, s); }), "qkv projection");
@@ -439,7 +446,9 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     {
       EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.bo); e.gate = mod + 2 * D;
+      if (hcur != m->h) e.res_in = hcur;
       HIPCHK(timed(m, FLASHBON_SITE_OUT, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.wo), e, s); }), "self-attn out projection");
+      hcur = m->h;
     }
     HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, nullptr, nullptr, m->a, s); }), "cross LN");
     {
@@ -469,15 +478,22 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     {
       EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
-      if (draft) e.cache = a->cache + ((int64_t)l * 3 + tr.slot) * MD;
-      e.cache_delta = residual;
+      float *slot = draft ? a->cache + ((int64_t)l * 3 + tr.slot) * MD : nullptr;
+      if (slot && !residual) {   // the new rows go to the cache slot only, which becomes the stream
+        e.out = slot;
+        e.res_in = m->h;
+      } else {
+        e.cache = slot;
+        e.cache_delta = residual;
+      }
       HIPCHK(timed(m, FLASHBON_SITE_MLP_DOWN, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, F, m->u, Wp(b.w2), e, s); }), "mlp down");
+      hcur = (const float *)e.out;
     }
     if ((st = dump(l + 1)) != FLASHBON_OK) return st;
   }
 
   // head + unpatchify + Euler update of the latents (or the stochastic update of Eq. 20)
-  HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, m->hmod, m->hmod + D, m->a, s); }), "head adaLN");
+  HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, m->hmod, m->hmod + D, m->a, s); }), "head adaLN");
   if (stochastic || guided) {
     if (!stochastic) {                      // Euler update through the same kernel: no drift term, no noise
       sde = SdeArgs{};

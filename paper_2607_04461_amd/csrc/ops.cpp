@@ -34,6 +34,20 @@ flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t 
   return launched(launch_linear(t, epilogue, M, N, K, A, W, e, (hipStream_t)stream), "linear");
 }
 
+flashbon_status flashbon_op_linear_residual(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
+                                            const void *W, const float *bias, const float *gate,
+                                            const float *residual_in, float *out, void *stream) {
+  if (dtype != FLASHBON_FP32 && dtype != FLASHBON_BF16) return fail(FLASHBON_EINVAL, "bad dtype");
+  if (M < 1 || N < 1 || K < 1 || K % 8 || N % 4 || K > 65536)
+    return fail(FLASHBON_ESHAPE, "need M,N,K >= 1, K <= 65536, K % 8 == 0, N % 4 == 0");
+  if (!A || !W || !out || !residual_in) return fail(FLASHBON_EINVAL, "A, W, residual_in and out are required");
+  EpiArgs e;
+  e.out = out; e.ldo = N; e.bias = bias; e.gate = gate;
+  if (residual_in != out) e.res_in = residual_in;
+  ActType t = dtype == FLASHBON_BF16 ? ACT_BF16 : ACT_F32;
+  return launched(launch_linear(t, FLASHBON_EPI_RESIDUAL, M, N, K, A, W, e, (hipStream_t)stream), "linear");
+}
+
 flashbon_status flashbon_op_linear_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue,
                                         int32_t *kernels, char *desc, int32_t desc_len) {
   if (dtype != FLASHBON_FP32 && dtype != FLASHBON_BF16) return fail(FLASHBON_EINVAL, "bad dtype");

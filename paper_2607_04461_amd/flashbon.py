@@ -68,7 +68,7 @@ class StepArgs(ctypes.Structure):
 EXPORTS = [
     "flashbon_weight_count", "flashbon_init_model", "flashbon_text_kv_bytes", "flashbon_cache_bytes",
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
-    "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_linear_plan", "flashbon_op_attention", "flashbon_op_ln_mod",
+    "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_linear_residual", "flashbon_op_linear_plan", "flashbon_op_attention", "flashbon_op_ln_mod",
     "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde", "flashbon_select",
 ]
 
@@ -114,6 +114,8 @@ def load() -> ctypes.CDLL:
     L.flashbon_last_error.restype = ctypes.c_char_p
     L.flashbon_op_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
     L.flashbon_op_linear.restype = i32
+    L.flashbon_op_linear_residual.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.flashbon_op_linear_residual.restype = i32
     L.flashbon_op_linear_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_char_p, i32]
     L.flashbon_op_linear_plan.restype = i32
     L.flashbon_op_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, i64, i64, vp, vp, i64, i64,
@@ -325,6 +327,12 @@ def flashbon_read_timing(model: int, site: str):
 def flashbon_op_linear(dtype, M, N, K, A, W, bias, epilogue, out, gate=None, cache_out=None, stream=None):
     _check(load().flashbon_op_linear(dtype, M, N, K, _ptr(A), _ptr(W), _ptr(bias), epilogue, _ptr(out),
                                      _ptr(gate), _ptr(cache_out), _stream(stream)), "flashbon_op_linear")
+
+
+def flashbon_op_linear_residual(dtype, M, N, K, A, W, bias, gate, residual_in, out, stream=None):
+    _check(load().flashbon_op_linear_residual(dtype, M, N, K, _ptr(A), _ptr(W), _ptr(bias), _ptr(gate),
+                                              _ptr(residual_in), _ptr(out), _stream(stream)),
+           "flashbon_op_linear_residual")
 
 
 def flashbon_op_linear_plan(dtype, M, N, K, epilogue):

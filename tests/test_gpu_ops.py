@@ -148,6 +148,66 @@ def test_linear_tile_plans_bit_identical(epi, monkeypatch):
         assert torch.equal(o, outs[0])
 
 
+@pytest.mark.parametrize("tile", [None, "256x256", "128x128", "split:256", "bm:192", "mix:7:3:1"])
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_linear_residual_separate_source(tile, dtype, monkeypatch):
+    """out = residual_in + gate (A W^T + bias) with the residual rows read from another buffer (the
+    draft step's self-attention output projection reads the stream from the previous block's cache
+    slot): matches the oracle, leaves residual_in untouched, and equals the in-place update bit for bit
+    (every tiling; ragged M, N and K)."""
+    if tile is None:
+        monkeypatch.delenv("FLASHBON_LINEAR_TILE", raising=False)
+    else:
+        monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
+    F = fb()
+    M, N, K = 517, 300, 640
+    A = _operand((M, K), 91, dtype)
+    W = _operand((N, K), 92, dtype, 0.05)
+    bias = synth.random_matrix((N,), 93)
+    gate = synth.random_matrix((N,), 94)
+    h0 = synth.random_matrix((M, N), 95)
+    dt = F.BF16 if dtype == "bf16" else F.FP32
+    res = _dev(h0, "fp32")
+    out = torch.full((M, N), 3.0, device="cuda", dtype=torch.float32)
+    Ad, Wd, bd, gd = _dev(A, dtype), _dev(W, dtype), _dev(bias, "fp32"), _dev(gate, "fp32")
+    F.flashbon_op_linear_residual(dt, M, N, K, Ad, Wd, bd, gd, res, out)
+    inplace = _dev(h0, "fp32")
+    F.flashbon_op_linear(dt, M, N, K, Ad, Wd, bd, F.EPI_RESIDUAL, inplace, gd)
+    torch.cuda.synchronize()
+    assert torch.equal(res, _dev(h0, "fp32"))
+    assert torch.equal(out, inplace)
+    ref = h0 + gate * odit.linear(A.astype(np.float64), W, bias)
+    assert rel_l2(out.cpu().numpy(), ref) <= 2e-6
+
+
+def test_linear_tile_orders_bit_identical(monkeypatch):
+    """The 4-wave kernel's tile order (groups of 1..8 row blocks sweeping the column tiles, groups that
+    do not divide the row blocks, two tile heights) moves tiles between XCDs and rounds only: outputs
+    are bit-identical to the default order and match the oracle."""
+    F = fb()
+    M, N, K = 1100, 1800, 256
+    A_h = _operand((M, K), 86, "bf16")
+    W_h = _operand((N, K), 87, "bf16", 0.05)
+    bias_h = synth.random_matrix((N,), 88)
+    A, W, bias = _dev(A_h, "bf16"), _dev(W_h, "bf16"), _dev(bias_h, "fp32")
+    ref = odit.linear(A_h.astype(np.float64), W_h, bias_h)
+    for tile in ["bm:160", "mix:7:6:1"]:
+        monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
+        outs = []
+        for group in [None, 1, 2, 3, 5, 8, 16]:
+            if group is None:
+                monkeypatch.delenv("FLASHBON_LINEAR_GROUP", raising=False)
+            else:
+                monkeypatch.setenv("FLASHBON_LINEAR_GROUP", str(group))
+            out = torch.empty((M, N), device="cuda", dtype=torch.float32)
+            F.flashbon_op_linear(F.BF16, M, N, K, A, W, bias, F.EPI_STORE_F32, out)
+            torch.cuda.synchronize()
+            outs.append(out)
+        assert rel_l2(outs[0].cpu().numpy(), ref) <= 2e-6
+        for o in outs[1:]:
+            assert torch.equal(o, outs[0])
+
+
 @pytest.mark.parametrize("M,N,K", [(24960, 4608, 1536), (24960, 8960, 1536), (24960, 1536, 8960),
                                    (24960, 64, 1536), (16384, 15360, 5120)])
 def test_linear_full_shapes_bf16_sampled_rows(M, N, K):
