@@ -661,6 +661,139 @@ __device__ __forceinline__ void dma_tile(int M, int N, int K, const bf16 *__rest
   tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 128 * wn, fr, fq);
 }
 
+// ------------------------------------------------- MFMA path, 8 waves, LDS filled directly
+// (32 WTA)x256 workgroup tile (WTA = 6..8), 8 waves in a 2 (m) x 4 (n) grid, each (16 WTA) x 64 (4 WTA
+// MFMAs of 16x16x32 per K substep, 16 WTA accumulators), two waves per SIMD: one wave alone issues
+// these MFMAs well below the matrix cores' rate (about 1.46 of 1.9 PFLOP/s in an MFMA-only loop), two
+// alternating waves keep them busy.  Same LDS layout, LDS-writing loads (waves 0-3 fill the A rows,
+// WTA instructions each per K tile, waves 4-7 the W rows, 8 each), two stages of K = 64 and the same
+// interleaving of fragment reads and loads with the MFMA groups as dma_tile.
+template <int EPI, typename TO, int WTA>
+__device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__restrict__ A, const bf16 *__restrict__ Wt,
+                                          const EpiArgs &e, int m0, int n0, bf16 *smem) {
+  using namespace mf;
+  static_assert(WTA >= 5 && WTA <= 8, "tile height 160..256");
+  constexpr int BM = 32 * WTA, BN = 256, WT = 4;
+  constexpr int STAGE = (BM + BN) * BK;
+  constexpr int NL = 8;            // load slots per wave per K tile (A waves use the first WTA)
+  constexpr int NR = WT + WTA;     // fragment reads per wave per substep (W, then A)
+  constexpr int NS = WTA;          // MFMA groups of 4 per substep
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const bool loads_a = wave < 4;
+  const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
+  const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
+  // load x of this wave: rows 8 WTA wave + 8 x .. + 7 of A (waves 0-3, x < WTA) or 64 (wave - 4) +
+  // 8 x .. + 7 of W (waves 4-7); lane l -> row + (l >> 3), slot l & 7
+  uint32_t voff[NL];
+  const int row0 = loads_a ? 8 * WTA * wave : 64 * (wave - 4);
+#pragma unroll
+  for (int x = 0; x < NL; ++x) {
+    const int r = row0 + 8 * x + (lane >> 3);
+    voff[x] = (uint32_t)((r * K + (((lane & 7) ^ swz(r)) << 3)) * 2);
+  }
+  const uint32_t lds_row0 = (uint32_t)((loads_a ? 0 : BM * BK) + row0 * BK) * 2u;
+  auto dma_one = [&](int kt, int st, int x) {
+    if (loads_a && x >= WTA) return;
+    char *dst = reinterpret_cast<char *>(smem) + st * (STAGE * 2) + lds_row0 + x * (8 * BK * 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(loads_a ? rsA : rsW, (__attribute__((address_space(3))) void *)dst, 16,
+                                             voff[x], kt * BK * 2, 0, 0);
+  };
+  auto dma_all = [&](int kt, int st) {
+#pragma unroll
+    for (int x = 0; x < NL; ++x) dma_one(kt, st, x);
+  };
+  f32x4 acc[WT][WTA];
+  const int fr = lane & 15, fq = lane >> 4;
+  // Fragment x of substep ks: x < WT -> W fragment i = x, rows 64 wn + 32 (i/2) + 8 (fr/4) + 4 (i%2) +
+  // fr%4; x >= WT -> A fragment j = x - WT, rows 16 WTA wm + 16 j + fr.  Rows 32 apart share the swizzle.
+  uint32_t offW[2][2], offA[2][2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      offW[ks][q] = 2 * (BM * BK + lds_off(64 * wn + 8 * (fr >> 2) + 4 * q + (fr & 3), fq + 4 * ks));
+      offA[ks][q] = 2 * lds_off(16 * WTA * wm + 16 * q + fr, fq + 4 * ks);
+    }
+  const char *lds = reinterpret_cast<const char *>(smem);
+  bf16x8 fw0[WT], fa0[WTA], fw1[WT], fa1[WTA];
+  auto rd = [&](int st, int ks, bf16x8 *fw, bf16x8 *fa, int x) {
+    const char *base = lds + st * (STAGE * 2);
+    if (x < WT) fw[x] = *reinterpret_cast<const bf16x8 *>(base + offW[ks][x & 1] + 4096 * (x >> 1));
+    else fa[x - WT] = *reinterpret_cast<const bf16x8 *>(base + offA[ks][x & 1] + 4096 * ((x - WT) >> 1));
+  };
+  auto substep = [&](auto READ, auto LOAD, const bf16x8 *fw, const bf16x8 *fa, int nst, int nks, bf16x8 *nfw,
+                     bf16x8 *nfa, int dma_kt, int dma_st) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+#pragma unroll
+      for (int i = 0; i < WT; ++i)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j], 0, 0, 0);
+      if constexpr (decltype(READ)::value) {
+#pragma unroll
+        for (int x = j * NR / NS; x < (j + 1) * NR / NS; ++x) rd(nst, nks, nfw, nfa, x);
+      }
+      if constexpr (decltype(LOAD)::value) {
+#pragma unroll
+        for (int x = j * NL / NS; x < (j + 1) * NL / NS; ++x) dma_one(dma_kt, dma_st, x);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  const int KT = K / BK;   // >= 2
+  dma_all(0, 0);
+  dma_all(1, 1);
+  // tile 0 has landed once only this wave's loads of tile 1 may be in flight
+  if (loads_a) __builtin_amdgcn_s_waitcnt(vmcnt_imm(WTA));
+  else __builtin_amdgcn_s_waitcnt(vmcnt_imm(NL));
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < NR; ++x) rd(0, 0, fw0, fa0, x);
+#pragma unroll
+  for (int i = 0; i < WT; ++i)
+#pragma unroll
+    for (int j = 0; j < WTA; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+  int kt = 0;
+  for (; kt + 2 < KT; ++kt) {
+    substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // tile kt+1 has landed
+    __syncthreads();                            // nobody reads stage kt & 1 any more
+    substep(T_{}, T_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, kt + 2, kt & 1);
+  }
+  substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the last K tile has landed
+  __syncthreads();
+  substep(T_{}, F_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, 0, 0);
+  ++kt;
+  substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+  substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
+  tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 64 * wn, fr, fq);
+}
+
+// MT row blocks x NT column tiles of 256 on the 8-wave tile; row blocks of two heights as in
+// k_linear_dma.
+template <int EPI, typename TO, int WTA>
+__global__ __launch_bounds__(512, 1) void k_linear_dma8(int M, int N, int K, const bf16 *__restrict__ A,
+                                                 const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT, int tall,
+                                                 int group_m) {
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  int mt, nt;
+  mf::tile_of(blockIdx.x, MT, NT, mt, nt, group_m);
+  const int before = (int)((int64_t)mt * tall / MT), upto = (int)((int64_t)(mt + 1) * tall / MT);
+  const int m0 = 32 * ((WTA - 1) * mt + before), n0 = nt * 256;
+  if (m0 >= M) return;   // a block past the last row (a forced plan with more blocks than M needs)
+  if constexpr (WTA > 5) {
+    if (upto == before) {
+      dma8_tile<EPI, TO, WTA - 1>(M, N, K, A, Wt, e, m0, n0, smem);
+      return;
+    }
+  }
+  dma8_tile<EPI, TO, WTA>(M, N, K, A, Wt, e, m0, n0, smem);
+}
+
 // MT row blocks x NT column tiles of 256.  Row blocks come in two heights: `tall` of them 32 WTA rows
 // high and the rest 32 (WTA - 1), the tall ones spread evenly over the block index (block i is tall
 // when floor((i + 1) tall / MT) > floor(i tall / MT)), so that every XCD's range of tiles holds its
@@ -732,15 +865,19 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
 // costs 0.64 of a round of 256x256 tiles at the same K (so the small tile does 0.78 of the big
 // tile's work per CU).  Candidates: all 256x256; all 128x128; the whole rows of 256x256 tiles that
 // fill complete rounds plus the remaining rows as 128x128 tiles (a second launch), which trims a
-// last round that would leave most CUs idle; and the 4-wave kernel with row blocks of two adjacent
-// heights (32 w and 32 (w - 1) rows), as many blocks as fill whole rounds.
+// last round that would leave most CUs idle; and row blocks of two adjacent heights (32 w and
+// 32 (w - 1) rows), as many blocks as fill whole rounds.  Where the LDS-writing loads apply (K % 64
+// == 0, K >= 128, N % 8 == 0) the 256-column tiles run on the 8-wave kernel, which measured 6-7%
+// faster than the 4-wave kernel on the same tiles at every projection of the draft; the 4-wave
+// kernel is kept for forced plans.
 enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT, PLAN_MIX };
 struct TileChoice {
   TilePlan plan;
-  int wta;    // PLAN_BIG / PLAN_MIX with the 4-wave kernel: the taller height, 32 wta rows
+  int wta;    // PLAN_MIX: the taller height, 32 wta rows
   int rows;   // PLAN_SPLIT: rows on 256x256 tiles
   int mb;     // PLAN_MIX: row blocks
   int tall;   // PLAN_MIX: row blocks of the taller height (the others are 32 (wta - 1) rows)
+  int waves = 4;   // PLAN_MIX: the 4-wave (k_linear_dma) or the 8-wave (k_linear_dma8) kernel
 };
 static int cu_count();
 
@@ -754,13 +891,19 @@ static int cu_count();
 // the two heights, and taken only when that beats the best one-height plan by more than kMixGain
 // (mixed launches measured a few percent slower than this estimate at wide N).
 static constexpr double kF[9] = {0, 0, 0, 0, 0, 0.79, 0.82, 0.85, 1.0};
+// The same for the 8-wave kernel (M = 24960, K = 1536): 224-row rounds 0.885 and 192-row rounds
+// 0.826 of a 256-row round, 160 rows estimated; a 128x128 round costs kSmall8 more in these units
+// than in the 4-wave kernel's (its 256-row round is that much faster).
+static constexpr double kF8[9] = {0, 0, 0, 0, 0, 0.78, 0.826, 0.885, 1.0};
+static constexpr double kSmall8 = 1.064;
 static constexpr double kG = 130.0, kMixGain = 0.02;
 static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
   // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", "bm:<rows>" (4-wave kernel, one
   // tile height: rows 160, 192 or 224), "mix:<w>:<blocks>:<tall>" (4-wave kernel, `blocks` row blocks,
   // `tall` of them 32 w rows high and the rest 32 (w - 1), w in 6..8, covering M), or
   // "split:<rows>" (rows a multiple of 256 with 0 < rows < M: the first rows on 256x256 tiles, the
-  // rest on 128x128 tiles)
+  // rest on 128x128 tiles); "w8" (the 8-wave kernel, 256x256 tiles), "w8:bm:<rows>" and
+  // "w8:mix:<w>:<blocks>:<tall>" (the 8-wave kernel with those row blocks)
   const char *force = getenv("FLASHBON_LINEAR_TILE");
   if (force) {
     if (!strncmp(force, "split:", 6)) {
@@ -768,42 +911,57 @@ static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
       if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) return {PLAN_SPLIT, 8, rows, 0, 0};
       return {PLAN_BIG, 8, 0, 0, 0};
     }
+    int waves = 4;
+    if (dma_ok && !strncmp(force, "w8", 2)) {
+      waves = 8;
+      force += force[2] == ':' ? 3 : 2;
+      if (!*force) {
+        const int mb = (M + 255) / 256;
+        return {PLAN_MIX, 8, 0, mb, mb, 8};
+      }
+    }
     if (dma_ok && !strncmp(force, "bm:", 3)) {
       const int rows = atoi(force + 3);
       if (rows == 160 || rows == 192 || rows == 224) {
         const int w = rows / 32, mb = (M + rows - 1) / rows;
-        return {PLAN_MIX, w + 1, 0, mb, 0};   // all blocks of the shorter height of the w + 1 kernel
+        return {PLAN_MIX, w + 1, 0, mb, 0, waves};   // all blocks of the shorter height of the w + 1 kernel
       }
     }
     if (dma_ok && !strncmp(force, "mix:", 4)) {
       int w = 0, mb = 0, tall = 0;
       if (sscanf(force + 4, "%d:%d:%d", &w, &mb, &tall) == 3 && w >= 6 && w <= 8 && mb > 0 && tall >= 0 &&
           tall <= mb && 32 * ((int64_t)(w - 1) * mb + tall) >= M)
-        return {PLAN_MIX, w, 0, mb, tall};
+        return {PLAN_MIX, w, 0, mb, tall, waves};
     }
     return {strcmp(force, "128x128") ? PLAN_BIG : PLAN_SMALL, 8, 0, 0, 0};
   }
   constexpr double kSmallA = 0.704, kSmallFix = 604.0;
   const int cus = cu_count();
   auto rounds = [&](int64_t tiles, int per_cu) { return (double)((tiles + per_cu * cus - 1) / (per_cu * cus)); };
-  auto cost = [&](int w) { return kF[w] * K + kG; };
+  const double *F = dma_ok ? kF8 : kF;
+  auto cost = [&](int w) { return F[w] * K + kG; };
   const int64_t NT = (N + 255) / 256, T = (int64_t)((M + 255) / 256) * NT, NT2 = (N + 127) / 128;
-  const double big = cost(8), small = kSmallA * K + kSmallFix;
+  const double big = cost(8), small = (kSmallA * K + kSmallFix) * (dma_ok ? kSmall8 : 1.0);
   TileChoice best = {PLAN_BIG, 8, 0, 0, 0};
   double t_best = rounds(T, 1) * big;
   if (dma_ok) {
     for (int w = 7; w >= 5; --w) {   // one height, 32 w rows: the kernel for w + 1 with no tall blocks
       const int mb = (M + 32 * w - 1) / (32 * w);
       const double t = rounds((int64_t)mb * NT, 1) * cost(w);
-      if (t < t_best) { t_best = t; best = {PLAN_MIX, w + 1, 0, mb, 0}; }
+      if (t < t_best) { t_best = t; best = {PLAN_MIX, w + 1, 0, mb, 0, 8}; }
     }
   }
-  const double t_small = rounds((int64_t)((M + 127) / 128) * NT2, 2) * small;
+  // a 128x128 launch with no more tiles than CUs runs one workgroup per CU, each faster than when
+  // two share the CU: costed at kAlone of a shared round (the refinement of one candidate, M = 1560,
+  // has its N = 1536 projections here: 156 tiles)
+  constexpr double kAlone = 0.6;
+  auto rounds_small = [&](int64_t tiles) { return tiles <= cus ? kAlone : rounds(tiles, 2); };
+  const double t_small = rounds_small((int64_t)((M + 127) / 128) * NT2) * small;
   if (t_small < t_best) { t_best = t_small; best = {PLAN_SMALL, 8, 0, 0, 0}; }
   const int64_t mt_big = (T - T % cus) / NT;
   const int rows = (int)(mt_big * 256);
   if (K % mf::BK == 0 && rows > 0 && rows < M) {
-    const double t_split = rounds(mt_big * NT, 1) * big + rounds(((M - rows + 127) / 128) * NT2, 2) * small;
+    const double t_split = rounds(mt_big * NT, 1) * big + rounds_small(((M - rows + 127) / 128) * NT2) * small;
     if (t_split < t_best) { t_best = t_split; best = {PLAN_SPLIT, 8, rows, 0, 0}; }
   }
   if (dma_ok) {
@@ -815,7 +973,7 @@ static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
         const int tall = max(0, (int)(((int64_t)M - (int64_t)lo * mb + 31) / 32));
         if (tall == 0 || tall == mb) continue;
         const double t = rounds((int64_t)mb * NT, 1) * ((double)tall * cost(w) + (double)(mb - tall) * cost(w - 1)) / mb;
-        if (t < (1.0 - kMixGain) * t_pure && t < t_best) { t_best = t; best = {PLAN_MIX, w, 0, mb, tall}; }
+        if (t < (1.0 - kMixGain) * t_pure && t < t_best) { t_best = t; best = {PLAN_MIX, w, 0, mb, tall, 8}; }
       }
     }
   }
@@ -876,6 +1034,24 @@ static hipError_t launch_dma(int M, int N, int K, const void *A, const void *Wt,
   return hipGetLastError();
 }
 
+// The 8-wave kernel over mb row blocks, `tall` of them 32 WTA rows high, the rest 32 (WTA - 1).
+template <int EPI, int WTA>
+static hipError_t launch_dma8(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s,
+                              int mb, int tall) {
+  const size_t lds = (size_t)2 * (32 * WTA + 256) * mf::BK * sizeof(bf16);
+  auto kern = k_linear_dma8<EPI, bf16, WTA>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int NT = (N + 255) / 256;
+  hipLaunchKernelGGL(kern, dim3(mb * NT), dim3(512), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e, mb, NT,
+                     tall, group_rows(mb, NT, K));
+  return hipGetLastError();
+}
+
 static int cu_count() {
   static int n = 0;
   if (!n) {
@@ -900,15 +1076,15 @@ static EpiArgs rows_from(const EpiArgs &e, int m) {
   return r;
 }
 
-// 256x256 tiles: the 4-wave kernel with LDS-writing loads when it takes the shape, else the generic
-// 8-wave kernel (K % 64 != 0, K < 128 or N % 8 != 0, and the latent scatter, which stays on 2 waves
-// per SIMD).
+// 256x256 tiles: the 8-wave kernel with LDS-writing loads when it takes the shape, else the generic
+// 8-wave kernel with register-staged loads (K % 64 != 0, K < 128 or N % 8 != 0, and the latent
+// scatter).
 template <int EPI>
 static hipError_t launch_big(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s) {
   if constexpr (EPI != EPI_EULER) {
     if (K % mf::BK == 0 && K >= 2 * mf::BK && N % 8 == 0) {
       const int mb = (M + 255) / 256;
-      return launch_dma<EPI, 8>(M, N, K, A, Wt, e, s, mb, mb);
+      return launch_dma8<EPI, 8>(M, N, K, A, Wt, e, s, mb, mb);
     }
   }
   return launch_mfma<8, 4, 2, 4, EPI, 1>(M, N, K, A, Wt, e, s);
@@ -924,6 +1100,11 @@ static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, cons
     if (c.plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
     if (c.plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s);
     if constexpr (EPI != EPI_EULER) {
+      if (c.plan == PLAN_MIX && c.waves == 8) {
+        if (c.wta == 8) return launch_dma8<EPI, 8>(M, N, K, A, Wt, e, s, c.mb, c.tall);
+        if (c.wta == 7) return launch_dma8<EPI, 7>(M, N, K, A, Wt, e, s, c.mb, c.tall);
+        return launch_dma8<EPI, 6>(M, N, K, A, Wt, e, s, c.mb, c.tall);
+      }
       if (c.plan == PLAN_MIX) {
         if (c.wta == 8) return launch_dma<EPI, 8>(M, N, K, A, Wt, e, s, c.mb, c.tall);
         if (c.wta == 7) return launch_dma<EPI, 7>(M, N, K, A, Wt, e, s, c.mb, c.tall);
@@ -955,18 +1136,19 @@ int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len)
     if (c.plan == PLAN_SMALL) {
       d = "k_linear_mfma: 128x128 tiles, 4 waves, two workgroups per CU";
     } else if (c.plan == PLAN_BIG) {
-      d = dma_ok ? "k_linear_dma: 256x256 tiles, " + std::to_string((M + 255) / 256) + " row blocks x " + nt
+      d = dma_ok ? "k_linear_dma8 (8 waves): 256x256 tiles, " + std::to_string((M + 255) / 256) + " row blocks x " + nt
                  : std::string("k_linear_mfma: 256x256 tiles, 8 waves");
     } else if (c.plan == PLAN_MIX) {
       const std::string blocks = std::to_string(c.mb) + " row blocks x " + nt;
-      if (c.tall == c.mb) d = "k_linear_dma: " + rows_of(c.wta) + "x256 tiles, " + blocks;
-      else if (c.tall == 0) d = "k_linear_dma: " + rows_of(c.wta - 1) + "x256 tiles, " + blocks;
+      const std::string kn = c.waves == 8 ? "k_linear_dma8 (8 waves): " : "k_linear_dma: ";
+      if (c.tall == c.mb) d = kn + rows_of(c.wta) + "x256 tiles, " + blocks;
+      else if (c.tall == 0) d = kn + rows_of(c.wta - 1) + "x256 tiles, " + blocks;
       else
-        d = "k_linear_dma: " + blocks + ", " + std::to_string(c.tall) + " of " + rows_of(c.wta) + " rows and " +
+        d = kn + blocks + ", " + std::to_string(c.tall) + " of " + rows_of(c.wta) + " rows and " +
             std::to_string(c.mb - c.tall) + " of " + rows_of(c.wta - 1);
     } else {
       kernels = 2;
-      d = "k_linear_dma: 256x256 tiles on rows 0.." + std::to_string(c.rows - 1) +
+      d = std::string(dma_ok ? "k_linear_dma8" : "k_linear_mfma") + ": 256x256 tiles on rows 0.." + std::to_string(c.rows - 1) +
           " + k_linear_mfma: 128x128 tiles on the remaining " + std::to_string(M - c.rows) + " rows";
     }
   }

@@ -84,16 +84,18 @@ def test_linear_small(dtype, M, N, K, epi):
 
 
 @pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256", "bm:224", "bm:192", "bm:160", "mix:7:3:1",
-                                  "mix:8:3:1", "mix:6:4:2"])
+                                  "mix:8:3:1", "mix:6:4:2", "w8", "w8:bm:160", "w8:mix:7:3:1", "w8:mix:8:3:1"])
 @pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
                                    (520, 776, 1024)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
 def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
-    """Every MFMA tiling (forced: "256x256" is the 4-wave kernel with LDS-writing loads when K % 64 == 0
+    """Every MFMA tiling (forced: "256x256" is the 8-wave kernel with LDS-writing loads when K % 64 == 0
     and K >= 128, else the 8-wave kernel; "split:256" puts rows 0..255 on 256x256 tiles and the rest
     on 128x128 tiles, when M > 256 and K % 64 == 0; "bm:<rows>" the 4-wave kernel with tiles of one
     height; "mix:w:blocks:tall" the 4-wave kernel with row blocks of two heights, 32 w and 32 (w - 1)
-    rows, spread over the blocks; plans the shape cannot take fall back to 256x256) on ragged M, N
+    rows, spread over the blocks; "w8", "w8:bm:<rows>", "w8:mix:..." the 8-wave kernel with LDS-writing
+    loads on the same row blocks; plans the
+    shape cannot take fall back to 256x256) on ragged M, N
     and K tails, against the oracle.
     The residual case also writes the cache copy."""
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
@@ -134,7 +136,7 @@ def test_linear_tile_plans_bit_identical(epi, monkeypatch):
     h0 = _dev(synth.random_matrix((M, N), 85), "fp32")
     outs = []
     for tile in ["256x256", "128x128", "split:512", "bm:224", "bm:192", "bm:160", "mix:7:6:1", "mix:8:5:1",
-                 "mix:6:7:3"]:
+                 "mix:6:7:3", "w8", "w8:bm:224", "w8:bm:192", "w8:bm:160", "w8:mix:7:6:1", "w8:mix:6:7:3"]:
         monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
         if epi == "store":
             out = torch.empty((M, N), device="cuda", dtype=torch.float32)
@@ -148,7 +150,7 @@ def test_linear_tile_plans_bit_identical(epi, monkeypatch):
         assert torch.equal(o, outs[0])
 
 
-@pytest.mark.parametrize("tile", [None, "256x256", "128x128", "split:256", "bm:192", "mix:7:3:1"])
+@pytest.mark.parametrize("tile", [None, "256x256", "128x128", "split:256", "bm:192", "mix:7:3:1", "w8"])
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_linear_residual_separate_source(tile, dtype, monkeypatch):
     """out = residual_in + gate (A W^T + bias) with the residual rows read from another buffer (the
@@ -191,7 +193,7 @@ def test_linear_tile_orders_bit_identical(monkeypatch):
     bias_h = synth.random_matrix((N,), 88)
     A, W, bias = _dev(A_h, "bf16"), _dev(W_h, "bf16"), _dev(bias_h, "fp32")
     ref = odit.linear(A_h.astype(np.float64), W_h, bias_h)
-    for tile in ["bm:160", "mix:7:6:1"]:
+    for tile in ["bm:160", "mix:7:6:1", "w8", "w8:mix:7:6:1"]:
         monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
         outs = []
         for group in [None, 1, 2, 3, 5, 8, 16]:

@@ -196,18 +196,18 @@ def test_select_rejects_bad_arguments():
 
 
 @pytest.mark.parametrize("shape,kernels,desc", [
-    ((24960, 4608, 1536, 0), 1, "k_linear_dma: 224x256 tiles, 112 row blocks x 18"),
-    ((24960, 8960, 1536, 1), 1, "k_linear_dma: 224x256 tiles, 112 row blocks x 35"),
-    ((24960, 1536, 1536, 3), 1, "k_linear_dma: 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
-    ((24960, 1536, 8960, 3), 1, "k_linear_dma: 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
-    ((16384, 15360, 5120, 0), 1, "k_linear_dma: 256x256 tiles, 64 row blocks x 60"),
+    ((24960, 4608, 1536, 0), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 98 row blocks x 18"),
+    ((24960, 8960, 1536, 1), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 98 row blocks x 35"),
+    ((24960, 1536, 1536, 3), 1, "k_linear_dma8 (8 waves): 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
+    ((24960, 1536, 8960, 3), 1, "k_linear_dma8 (8 waves): 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
+    ((16384, 15360, 5120, 0), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 64 row blocks x 60"),
     ((200, 136, 72, 0), 1, "k_linear_mfma: 256x256 tiles, 8 waves"),
 ])
 def test_linear_plan_of_model_shapes(shape, kernels, desc, monkeypatch):
     """The tile plan is a host decision (no device needed; 256 CUs assumed without one).  At the
-    1.3B-shaped pool's M = 16 x 1560 rows: QKV and MLP up on 224-row tiles, the N = 1536 projections
-    on 128 row blocks of 224 and 192 rows that fill three rounds exactly; K % 64 != 0 takes the
-    generic 8-wave kernel."""
+    1.3B-shaped pool's M = 16 x 1560 rows: QKV and MLP up on 256-row tiles of the 8-wave kernel, the
+    N = 1536 projections on 128 row blocks of 224 and 192 rows that fill three rounds exactly;
+    K % 64 != 0 takes the generic 8-wave kernel with register-staged loads."""
     monkeypatch.delenv("FLASHBON_LINEAR_TILE", raising=False)
     assert fb.flashbon_op_linear_plan(fb.BF16, *shape) == (kernels, desc)
     # the row blocks named cover M with no block starting past it
@@ -226,6 +226,12 @@ def test_linear_plan_follows_override_and_rejects_bad_arguments(monkeypatch):
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", "mix:7:128:12")
     assert fb.flashbon_op_linear_plan(fb.BF16, 24960, 1536, 1536, 3)[1] == \
         "k_linear_dma: 128 row blocks x 6, 12 of 224 rows and 116 of 192"
+    monkeypatch.setenv("FLASHBON_LINEAR_TILE", "w8:mix:7:128:12")
+    assert fb.flashbon_op_linear_plan(fb.BF16, 24960, 1536, 1536, 3)[1] == \
+        "k_linear_dma8 (8 waves): 128 row blocks x 6, 12 of 224 rows and 116 of 192"
+    monkeypatch.setenv("FLASHBON_LINEAR_TILE", "w8:bm:192")
+    assert fb.flashbon_op_linear_plan(fb.BF16, 24960, 1536, 1536, 3)[1] == \
+        "k_linear_dma8 (8 waves): 192x256 tiles, 130 row blocks x 6"
     monkeypatch.setenv("FLASHBON_LINEAR_TILE", "mix:7:100:0")    # does not cover M: ignored
     assert "256x256" in fb.flashbon_op_linear_plan(fb.BF16, 24960, 1536, 1536, 3)[1]
     monkeypatch.delenv("FLASHBON_LINEAR_TILE")
