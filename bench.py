@@ -50,6 +50,33 @@ def draft_flops(wl, traces):
     return total * wl.n
 
 
+def site_rooflines(wl, traces, breakdown):
+    """Per launch site of one draft: algorithmic TFLOP/s against the bf16 MFMA peak (projections,
+    attention) or algorithmic HBM GB/s against 8 TB/s (LayerNorms: read 4 + write 2 bytes per element;
+    proxies: (order + 1) fp32 reads + 1 write per element), from the site timings of that draft."""
+    s = wl.shape
+    M, D, F, T, Lt = wl.n * wl.tokens, s.hidden, s.mlp_hidden, wl.tokens, wl.text_len
+    flops = {"qkv": 2.0 * M * 3 * D * D, "out": 2.0 * M * D * D, "cross_q": 2.0 * M * D * D,
+             "out_cross": 2.0 * M * D * D, "mlp_up": 2.0 * M * F * D, "mlp_down": 2.0 * M * D * F,
+             "attn_self": 4.0 * wl.n * T * T * D, "attn_cross": 4.0 * wl.n * T * Lt * D}
+    out = {}
+    for site, f in flops.items():
+        b = breakdown.get(site)
+        if b:
+            tf = f * b["launches"] / (b["ms"] / 1e3) / 1e12
+            out[site] = {"bound": "mfma", "TFLOPs": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+    b = breakdown.get("norm")
+    if b:
+        gbs = 6.0 * M * D * b["launches"] / (b["ms"] / 1e3) / 1e9
+        out["norm"] = {"bound": "hbm", "GBs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    b = breakdown.get("proxy")
+    if b:
+        nbytes = sum(4.0 * M * D * (e[1] + 2) for tr in traces for e in tr if e[0] == 2 and e[3])
+        gbs = nbytes / (b["ms"] / 1e3) / 1e9
+        out["proxy"] = {"bound": "hbm", "GBs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
+
+
 def recorded_traffic():
     """HBM bytes per launch of the dominant kernel from the committed counter summary, or None if
     the kernel source has changed since the counters were taken."""
@@ -278,6 +305,7 @@ def main():
         "refine_ms": refine_ms,
         "refine_steps": wl.steps_total - wl.steps_draft,
         "site_breakdown_one_draft": breakdown,
+        "site_rooflines_one_draft": site_rooflines(wl, traces, breakdown) if breakdown else None,
     }
     pool.close()
     if not args.no_cpu_baseline:

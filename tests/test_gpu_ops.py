@@ -339,7 +339,8 @@ def test_attention_full_shapes_bf16_sampled_queries(B, heads, T, tk):
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 @pytest.mark.parametrize("M,D,mod", [(37, 64, True), (24960, 1536, True), (300, 5120, False), (5, 256, False),
-                                     (23, 1000, True), (9, 68, True)])
+                                     (23, 1000, True), (9, 68, True), (1, 4096, True), (2, 8, False),
+                                     (4097, 1536, False)])
 def test_ln_mod(dtype, M, D, mod):
     F = fb()
     dt = F.BF16 if dtype == "bf16" else F.FP32
