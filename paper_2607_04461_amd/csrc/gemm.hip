@@ -893,9 +893,10 @@ static int cu_count();
 static constexpr double kF[9] = {0, 0, 0, 0, 0, 0.79, 0.82, 0.85, 1.0};
 // The same for the 8-wave kernel (M = 24960, K = 1536): 224-row rounds 0.885 and 192-row rounds
 // 0.826 of a 256-row round, 160 rows estimated; a 128x128 round costs kSmall8 more in these units
-// than in the 4-wave kernel's (its 256-row round is that much faster).
+// than in the 4-wave kernel's (its 256-row round is that much faster); its two-height launches are
+// taken when kMixGain8 better than the best one-height plan.
 static constexpr double kF8[9] = {0, 0, 0, 0, 0, 0.78, 0.826, 0.885, 1.0};
-static constexpr double kSmall8 = 1.064;
+static constexpr double kSmall8 = 1.064, kMixGain8 = 0.01;
 static constexpr double kG = 130.0, kMixGain = 0.02;
 static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
   // FLASHBON_LINEAR_TILE (tests and tuning): "256x256", "128x128", "bm:<rows>" (4-wave kernel, one
@@ -965,15 +966,18 @@ static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
     if (t_split < t_best) { t_best = t_split; best = {PLAN_SPLIT, 8, rows, 0, 0}; }
   }
   if (dma_ok) {
-    const double t_pure = t_best;
-    for (int w = 7; w >= 6; --w) {   // two heights, 32 w and 32 (w - 1) rows
+    // two heights, 32 w and 32 (w - 1) rows.  The 8-wave kernel also mixes 256- with 224-row blocks:
+    // at M = 24960 that fills whole rounds for MLP up (102 blocks, 66 of 256 rows: 579 -> 567 us) and
+    // QKV (99 blocks, 87 of 256: 292.5 -> 286.9 us), where the 4-wave kernel measured such mixes slower
+    const double t_pure = t_best, gain = kMixGain8;
+    for (int w = 8; w >= 6; --w) {
       const int lo = 32 * (w - 1);
       const int mb_min = (M + 32 * w - 1) / (32 * w), mb_max = (M + lo - 1) / lo;
       for (int mb = mb_min; mb <= mb_max; ++mb) {
         const int tall = max(0, (int)(((int64_t)M - (int64_t)lo * mb + 31) / 32));
         if (tall == 0 || tall == mb) continue;
         const double t = rounds((int64_t)mb * NT, 1) * ((double)tall * cost(w) + (double)(mb - tall) * cost(w - 1)) / mb;
-        if (t < (1.0 - kMixGain) * t_pure && t < t_best) { t_best = t; best = {PLAN_MIX, w, 0, mb, tall, 8}; }
+        if (t < (1.0 - gain) * t_pure && t < t_best) { t_best = t; best = {PLAN_MIX, w, 0, mb, tall, 8}; }
       }
     }
   }

@@ -196,8 +196,8 @@ def test_select_rejects_bad_arguments():
 
 
 @pytest.mark.parametrize("shape,kernels,desc", [
-    ((24960, 4608, 1536, 0), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 98 row blocks x 18"),
-    ((24960, 8960, 1536, 1), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 98 row blocks x 35"),
+    ((24960, 4608, 1536, 0), 1, "k_linear_dma8 (8 waves): 99 row blocks x 18, 87 of 256 rows and 12 of 224"),
+    ((24960, 8960, 1536, 1), 1, "k_linear_dma8 (8 waves): 102 row blocks x 35, 66 of 256 rows and 36 of 224"),
     ((24960, 1536, 1536, 3), 1, "k_linear_dma8 (8 waves): 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
     ((24960, 1536, 8960, 3), 1, "k_linear_dma8 (8 waves): 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
     ((16384, 15360, 5120, 0), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 64 row blocks x 60"),
@@ -205,8 +205,9 @@ def test_select_rejects_bad_arguments():
 ])
 def test_linear_plan_of_model_shapes(shape, kernels, desc, monkeypatch):
     """The tile plan is a host decision (no device needed; 256 CUs assumed without one).  At the
-    1.3B-shaped pool's M = 16 x 1560 rows: QKV and MLP up on 256-row tiles of the 8-wave kernel, the
-    N = 1536 projections on 128 row blocks of 224 and 192 rows that fill three rounds exactly;
+    1.3B-shaped pool's M = 16 x 1560 rows: QKV and MLP up on row blocks of 256 and 224 rows of the
+    8-wave kernel that fill 7 and 14 rounds, the N = 1536 projections on 128 row blocks of 224 and 192
+    rows that fill three rounds exactly;
     K % 64 != 0 takes the generic 8-wave kernel with register-staged loads."""
     monkeypatch.delenv("FLASHBON_LINEAR_TILE", raising=False)
     assert fb.flashbon_op_linear_plan(fb.BF16, *shape) == (kernels, desc)
