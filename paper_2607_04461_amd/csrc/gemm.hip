@@ -1003,20 +1003,21 @@ static hipError_t launch_mfma(int M, int N, int K, const void *A, const void *Wt
   return hipGetLastError();
 }
 
-// Row blocks per tile group of the 4-wave kernel's order (see mf::tile_of).  Wide outputs keep
-// groups of 8 row blocks (the 32 tiles an XCD runs at once then span 8 row blocks x 4 column tiles).
-// Narrow outputs (at most 8 column tiles) take groups of 4, and with a long K groups of 1, so an
-// XCD runs every column tile of a row block together and each A row block (3.4 MB at K = 8960) is
-// fetched once rather than again in a later round.  Measured in the 1.3B-shaped draft (M = 24960):
-// the MLP down-projection (N = 1536, K = 8960) 68.5 -> 66.0 ms per draft with groups of 1, the
-// N = 1536, K = 1536 projections 17.2 -> 16.8 ms with groups of 4; QKV and MLP up are best at 8.
-// The order does not change any output.  FLASHBON_LINEAR_GROUP (tuning): a fixed group height.
+// Row blocks per tile group of the linear kernels' order (see mf::tile_of).  Narrow outputs (at most
+// 8 column tiles) take groups of 1, so an XCD runs every column tile of a row block together and each
+// A row block (3.4 MB at K = 8960) is fetched once rather than again in a later round; up to 24 column
+// tiles groups of 8 (the 32 tiles an XCD runs at once then span 8 row blocks x 4 column tiles), wider
+// outputs groups of 6.  Swept in the 1.3B-shaped draft (M = 24960) on the 8-wave kernel: MLP down
+// (N = 1536, K = 8960) best at 1 (61.2 ms per draft against 65.0 at 8), the K = 1536, N = 1536
+// projections at 1 (about 1% ahead of 4), QKV (18 column tiles) at 8, MLP up (35) at 6 (55.8 against
+// 56.5 ms at 8).  The order does not change any output.  FLASHBON_LINEAR_GROUP (tuning): a fixed
+// group height.
 static int group_rows(int MT, int NT, int K) {
   const char *force = getenv("FLASHBON_LINEAR_GROUP");
   if (force && atoi(force) > 0) return atoi(force);
-  (void)MT;
-  if (NT <= 8) return K >= 4096 ? 1 : 4;
-  return mf::GROUP_M;
+  (void)MT; (void)K;
+  if (NT <= 8) return 1;
+  return NT <= 24 ? mf::GROUP_M : 6;
 }
 
 // The 4-wave kernel over mb row blocks, `tall` of them 32 WTA rows high, the rest 32 (WTA - 1).
