@@ -289,6 +289,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
   if (u >= p.batch * p.heads) return;
   const int h = u / p.batch, b = u % p.batch;
   const int q0 = qblk * QB + w * QW;
+  // a wave whose 32 queries all lie past tq (the last query block of a unit) still loads its share
+  // of every K/V tile and meets every barrier, but forms no scores, probabilities or outputs, leaving
+  // its SIMD's issue slots to the co-resident workgroup's wave
+  const bool idle = q0 >= p.tq;
   const int kb = kv_batch(p, b);
   const bf16 *Q = (const bf16 *)p.q + (int64_t)b * p.q_bs + h * DH;
   const bf16 *Kb = (const bf16 *)p.k + (int64_t)kb * p.kv_bs + h * DH;
@@ -383,6 +387,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
     __syncthreads();
     if (j + 2 < nt) load_k(j + 2, st);
     if (j + 1 < nt) load_v(j + 1, st ^ 1);
+    if (idle) return;
     if ((j + 1) * KT > p.tk) {   // ragged last tile: keys at or past tk get -inf
       const int lim = p.tk - j * KT - 4 * g;
 #pragma unroll
@@ -448,7 +453,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
   f32x16 s0[2], s1[2];
-  scores(0, s0);
+  if (!idle) scores(0, s0);
   for (int j = 0; j < nt; j += 2) {
     tile(std::integral_constant<int, 0>{}, j, s0, s1);
     if (j + 1 >= nt) break;
