@@ -1,10 +1,11 @@
 // Linear layers of the DiT step: C[m][n] = sum_k A[m][k] Wt[n][k] with fused epilogues.
-//   * k_linear_dma / k_linear_mfma: bf16 operands on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16),
-//     fp32 accumulation.  Workgroup tiles of 256x256 (k_linear_dma: 4 waves of 128x128, LDS filled
-//     by buffer loads that write LDS themselves, K % 64 == 0; k_linear_mfma<8,4,2,4>: 8 waves of
-//     128x64 for other K) or 128x128 (4 waves of 64x64, two workgroups per CU), chosen per shape by
-//     a round-count model; K tiles of 64 in double-buffered, XOR-swizzled LDS; XCD-aware grouped tile
-//     order.  Operands are swapped (the weight tile feeds the MFMA "A" side) and the weight rows
+//   * k_linear_dma8 / k_linear_dma / k_linear_mfma: bf16 operands on gfx950 matrix cores
+//     (v_mfma_f32_16x16x32_bf16), fp32 accumulation.  Workgroup tiles of 160..256 rows x 256 columns
+//     (k_linear_dma8: 8 waves, two per SIMD, LDS filled by buffer loads that write LDS themselves,
+//     K % 64 == 0 -- the default; k_linear_dma: the same tiles on 4 waves, one per SIMD, for forced
+//     plans; k_linear_mfma<8,4,2,4>: 8 waves of 128x64 with register-staged loads for other K) or
+//     128x128 (4 waves of 64x64, two workgroups per CU), chosen per shape by a round-count model; K
+//     tiles of 64 in double-buffered, XOR-swizzled LDS; XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) and the weight rows
 //     permuted so that every lane owns 8 consecutive output columns of one row.  Every kernel
 //     accumulates K in the same order, so an output element does not depend on the tiling.
 //   * k_linear_valu: fp32 (or bf16) operands on the vector ALUs, 64x64 tiles; used by the fp32 mode
