@@ -72,6 +72,37 @@ def test_draft_trajectory_matches_oracle(name, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_cache_slots_hold_block_outputs(dtype):
+    """After every draft step, each cache slot the oracle has filled holds the same block output on the
+    GPU (Sec. 4.1 (2): the features of visited timesteps).  The library writes a computed block's new
+    residual rows only into its slot and reads them there as the next block's input, so this also
+    checks that no later launch of the step disturbs a slot.  Tolerance: the step's latent tolerance."""
+    wl = synth.WORKLOADS["mid"]
+    flat, W, z0, text = _inputs(wl)
+    sched = wl.schedule()
+    kv = odit.prepare_text(W, wl.shape, text)
+    cache = odit.PoolCache(wl.shape.num_blocks)
+    pool = _pool(wl, dtype, flat)
+    pool.reset(z0)
+    L, n, T, D = wl.shape.num_blocks, wl.n, wl.tokens, wl.shape.hidden
+    assert pool.cache.numel() == L * 3 * n * T * D
+    z_ref = z0.astype(np.float64)
+    tol = TOL[dtype][0]
+    for k in range(wl.steps_draft):
+        skip, proxy = wl.masks(k)
+        z_ref, _ = odit.draft_step(W, wl.shape, z_ref, sched[k], sched[k + 1], kv, wl.cond_index(), skip, proxy,
+                                   cache)
+        pool.draft_step(k)
+        torch.cuda.synchronize()
+        slots = pool.cache.view(L, 3, n, T, D).cpu().numpy().astype(np.float64)
+        assert cache.data, "the oracle filled no slot"
+        for (j, l, s), h in cache.data.items():
+            err = rel_l2(slots[l, s, j], h)
+            assert err <= tol, (k, j, l, s, err)
+    pool.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_refine_after_draft_matches_oracle(dtype):
     wl = synth.WORKLOADS["mid"]
     flat, W, z0, text = _inputs(wl)
