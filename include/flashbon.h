@@ -133,10 +133,12 @@ typedef struct {
   flashbon_cache_meta *meta;   /* host [num_blocks] in/out (draft only) */
   flashbon_trace_entry *trace; /* host [num_blocks] out, optional (NULL = not reported) */
 
-  float *hidden_dump; /* optional debug output, device fp32 [num_blocks+1][n][T][hidden]: the residual
-                         stream after the patch embedding (index 0) and after block l (index l+1).
-                         Entries whose value is never formed (a dead proxy, or the embedding when the
-                         first non-skipped block is a proxy) are left untouched.  NULL = off. */
+  float *hidden_dump; /* optional debug output, device fp32 [num_blocks+1][rows][T][hidden] (rows = n, or
+                         2n with guidance): the residual stream after the patch embedding (index 0) and
+                         after block l (index l+1).  Entries whose value the step never forms are left
+                         untouched: the embedding when the first non-skipped block is a proxy, a dead
+                         proxy, and a skipped block whose input was not formed (it follows one of
+                         those with no launched block in between).  NULL = off. */
   void *stream;       /* hipStream_t */
 
   /* Stochastic update (App. A.1, Eq. 20) in place of the Euler one; sde_a = 0 (a zero-initialised

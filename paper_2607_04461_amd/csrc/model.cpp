@@ -138,6 +138,9 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
 
   auto cleanup = [&](flashbon_status st, const std::string &msg) {
     flashbon_free(m);
+    // a failed allocation is also recorded as the thread's last HIP error, which the next launch check
+    // (hipGetLastError after a launch) would report as that launch's failure: clear it
+    if (st == FLASHBON_ENOMEM) (void)hipGetLastError();
     return fail(st, msg);
   };
   const size_t total = m->lay.total;
@@ -392,6 +395,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   bool embed_live = true;
   for (int l = 0; l < L && !residual; ++l)
     if (trace[l].action != FLASHBON_SKIP) { embed_live = trace[l].action == FLASHBON_COMPUTE; break; }
+  // `formed`: the stream buffer holds this step's value at the current point of the block loop.  It is
+  // false from an elided embedding or a dead proxy up to the next launched proxy, and the hidden-state
+  // dump then leaves those entries untouched (their values are never formed).
+  bool formed = embed_live;
   if (embed_live) {
     HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, R, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s); }), "patchify");
     EpiArgs e;
@@ -406,17 +413,21 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     const BlockOff &b = m->lay.blk[l];
     const float *mod = m->bmods + (int64_t)l * 6 * D;
     if (tr.action == FLASHBON_SKIP) {
-      if ((st = dump(l + 1)) != FLASHBON_OK) return st;
+      if (formed && (st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
     }
     if (tr.action == FLASHBON_PROXY) {
-      if (!tr.live) continue;
+      if (!tr.live) {
+        formed = false;
+        continue;
+      }
       const flashbon_cache_meta &mb = a->meta[l];
       const int s1 = (mb.head + 2) % 3, s2 = (mb.head + 1) % 3, s3 = mb.head;
       auto slot_ptr = [&](int sl) { return a->cache + ((int64_t)l * 3 + sl) * MD; };
       HIPCHK(timed(m, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s, residual); }),
              "activation proxy");
       hcur = m->h;
+      formed = true;
       if ((st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
     }

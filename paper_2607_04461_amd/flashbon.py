@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional, Sequence
+from typing import Dict, Optional, Sequence
 
 import numpy as np
 
@@ -174,17 +174,115 @@ def flashbon_weight_count(cfg: ModelConfig) -> int:
     return int(load().flashbon_weight_count(ctypes.byref(cfg)))
 
 
+# Shape of every live model handle, so that the step wrappers can check the caller's tensors before
+# their addresses cross the C ABI (which cannot see sizes, dtypes or devices).
+_MODELS: Dict[int, ModelConfig] = {}
+
+
 def flashbon_init_model(cfg: ModelConfig, host_weights: np.ndarray) -> int:
     w = np.ascontiguousarray(host_weights, dtype=np.float32)
     h = ctypes.c_void_p()
     _check(load().flashbon_init_model(ctypes.byref(cfg), w.ctypes.data, w.size, ctypes.byref(h)),
            "flashbon_init_model")
+    kept = ModelConfig()
+    ctypes.pointer(kept)[0] = cfg
+    _MODELS[int(h.value)] = kept
     return int(h.value)
 
 
 def flashbon_free(model: Optional[int]) -> None:
     if model:
+        _MODELS.pop(int(model), None)
         load().flashbon_free(model)
+
+
+def model_config(model: int) -> ModelConfig:
+    """The configuration a live handle was created with (ValueError for an unknown handle)."""
+    try:
+        return _MODELS[int(model)]
+    except (KeyError, TypeError):
+        raise ValueError("not a live model handle from flashbon_init_model") from None
+
+
+def text_kv_nbytes(cfg: ModelConfig, n_cond: int, text_len: int) -> int:
+    """flashbon_text_kv_bytes for a configuration: [L][n_cond][text_len][2 D] act elements."""
+    return cfg.num_blocks * n_cond * text_len * 2 * cfg.hidden * (2 if cfg.dtype == BF16 else 4)
+
+
+def cache_nbytes(cfg: ModelConfig, rows: int, tokens: int) -> int:
+    """flashbon_cache_bytes for a configuration: fp32 [L][3][rows][tokens][D]."""
+    return cfg.num_blocks * 3 * rows * tokens * cfg.hidden * 4
+
+
+def _nbytes(t) -> int:
+    return int(t.numel()) * int(t.element_size())
+
+
+def _check_tensor(name: str, t, *, dtype=None, ndim=None, require_device: bool = True) -> None:
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if require_device:
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the current device (a GPU), got {t.device}")
+        if t.device.index != torch.cuda.current_device():
+            raise ValueError(f"{name} must be on the current device (cuda:{torch.cuda.current_device()}), "
+                             f"got {t.device}")
+
+
+def validate_step(cfg: ModelConfig, latents, text, text_kv, *, draft: bool, guided: bool = False,
+                  cache=None, hidden_dump=None, preview=None, meta=None, trace=None,
+                  require_device: bool = True) -> None:
+    """Raise ValueError unless every buffer a step would hand to the library has the dtype, layout,
+    device and size the step's kernels read and write (include/flashbon.h, flashbon_step_args).
+    ``require_device=False`` skips only the device check (host-only tests of the other checks)."""
+    import torch
+    f32 = torch.float32
+    _check_tensor("latents", latents, dtype=f32, ndim=4, require_device=require_device)
+    n, C, H, W = (int(x) for x in latents.shape)
+    if C != cfg.latent_channels:
+        raise ValueError(f"latents have {C} channels, the model {cfg.latent_channels}")
+    _check_tensor("text", text, dtype=f32, ndim=3, require_device=require_device)
+    n_cond, text_len, text_dim = (int(x) for x in text.shape)
+    if text_dim != cfg.text_dim:
+        raise ValueError(f"text tokens are {text_dim} wide, the model takes {cfg.text_dim}")
+    _check_tensor("text_kv", text_kv, require_device=require_device)
+    need = text_kv_nbytes(cfg, n_cond, text_len)
+    if _nbytes(text_kv) < need:
+        raise ValueError(f"text_kv holds {_nbytes(text_kv)} bytes, needs {need}")
+    rows = 2 * n if guided else n
+    p = max(cfg.patch, 1)
+    tokens = (H // p) * (W // p)
+    if draft:
+        if cache is None:
+            raise ValueError("a draft step needs the activation cache")
+        _check_tensor("cache", cache, dtype=f32, require_device=require_device)
+        need = cache_nbytes(cfg, rows, tokens)
+        if _nbytes(cache) < need:
+            raise ValueError(f"cache holds {_nbytes(cache)} bytes, needs {need} for {rows} rows x {tokens} tokens")
+        if meta is None or len(meta) != cfg.num_blocks:
+            raise ValueError(f"meta must hold {cfg.num_blocks} entries")
+    if trace is not None and len(trace) != cfg.num_blocks:
+        raise ValueError(f"trace must hold {cfg.num_blocks} entries")
+    if hidden_dump is not None:
+        _check_tensor("hidden_dump", hidden_dump, dtype=f32, require_device=require_device)
+        need = (cfg.num_blocks + 1) * rows * tokens * cfg.hidden
+        if int(hidden_dump.numel()) < need:
+            raise ValueError(f"hidden_dump holds {int(hidden_dump.numel())} floats, needs {need}")
+    if preview is not None:
+        _check_tensor("preview", preview, dtype=f32, ndim=4, require_device=require_device)
+        if tuple(preview.shape) != tuple(latents.shape):
+            raise ValueError(f"preview must have the latents' shape {tuple(latents.shape)}")
+        a0, a1 = latents.data_ptr(), latents.data_ptr() + _nbytes(latents)
+        b0, b1 = preview.data_ptr(), preview.data_ptr() + _nbytes(preview)
+        if a0 < b1 and b0 < a1:
+            raise ValueError("preview must not overlap latents")
 
 
 def flashbon_text_kv_bytes(model: int, n_cond: int, text_len: int) -> int:
@@ -209,7 +307,20 @@ def trace_list(trace) -> list:
 
 def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
           skip=None, proxy=None, cache=None, meta=None, trace=None, hidden_dump=None, stream=None,
-          num_blocks=None, sde=None, preview=None, cfg=None, proxy_mode=0):
+          num_blocks=None, sde=None, preview=None, cfg=None, proxy_mode=0, draft=True):
+    validate_step(model_config(model), latents, text, text_kv, draft=draft, guided=cfg is not None,
+                  cache=cache, hidden_dump=hidden_dump, preview=preview, meta=meta, trace=trace)
+    a = step_args(latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid, skip, proxy, cache,
+                  meta, trace, hidden_dump, stream, num_blocks, sde, preview, cfg, proxy_mode)
+    _check(fn(model, ctypes.byref(a)), where)
+
+
+def step_args(latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid, skip=None, proxy=None,
+              cache=None, meta=None, trace=None, hidden_dump=None, stream=None, num_blocks=None, sde=None,
+              preview=None, cfg=None, proxy_mode=0) -> StepArgs:
+    """flashbon_step_args for the given buffers, without any check (the library validates the rest;
+    tests of the library's own validation build arguments with this).  The host arrays it points to
+    are kept alive on the returned structure."""
     n, C, H, W = (int(x) for x in latents.shape)
     n_cond, text_len = int(text.shape[0]), int(text.shape[1])
     cond = np.ascontiguousarray(np.asarray(cond_index, dtype=np.int32))
@@ -244,7 +355,8 @@ def _step(fn, where, model, latents, t_cur, t_next, text, cond_index, text_kv, t
     if sde is not None:
         a.sde_a, a.sde_seed, a.sde_step = float(sde[0]), int(sde[1]), int(sde[2])
         a.sde_row0 = int(sde[3]) if len(sde) > 3 else 0
-    _check(fn(model, ctypes.byref(a)), where)
+    a._keep = (cond, sk, px, unc if cfg is not None else None, text_kv_valid)
+    return a
 
 
 def flashbon_draft_step(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
@@ -264,7 +376,7 @@ def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_k
                          trace=None, hidden_dump=None, stream=None, sde=None, preview=None, cfg=None):
     _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde,
-          preview=preview, cfg=cfg)
+          preview=preview, cfg=cfg, draft=False)
 
 
 def flashbon_select(scores, judge, rho1=0.5, rho2=0.5, kappa=1.5):

@@ -6,7 +6,7 @@ import pytest
 
 from oracle import dit as odit
 from paper_2607_04461_amd import synth
-from tests._util import rel_l2
+from tests._util import TOL_V, rel_l2, step_velocity
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -44,25 +44,35 @@ def test_guided_draft_matches_oracle(name, sde, dtype, tol):
     z_ref = z0.astype(np.float64)
     for k in range(wl.steps_draft):
         skip, proxy = wl.masks(k)
+        z_prev_ref, z_prev = z_ref, pool.latents.cpu().numpy().astype(np.float64)
         z_ref, tr_ref = odit.draft_step(W, wl.shape, z_ref, sched[k], sched[k + 1], kv, wl.cond_index(), skip,
                                         proxy, cache, sde_args=None if sde is None else (sde[0], sde[1], k),
                                         cfg=(scale, unc))
         tr = pool.draft_step(k, sde=sde)
         torch.cuda.synchronize()
         assert tr == [tuple(e) for e in tr_ref], f"trace step {k}"
-        ez = rel_l2(pool.latents.cpu().numpy().astype(np.float64), z_ref)
-        print(f"{name} {dtype} cfg {scale} sde={sde} step {k}: z {ez:.2e}", flush=True)
-        assert ez <= tol, (k, ez)
-    # refinement of candidate 1 with guidance
-    out = pool.refine(1)
-    torch.cuda.synchronize()
-    ref = z_ref[1:2]
+        got = pool.latents.cpu().numpy().astype(np.float64)
+        noise = None if sde is None else (sde[0], sde[1], k, 0)
+        ez = rel_l2(got, z_ref)
+        ev = rel_l2(step_velocity(got, z_prev, sched[k], sched[k + 1], noise),
+                    step_velocity(z_ref, z_prev_ref, sched[k], sched[k + 1], noise))
+        print(f"{name} {dtype} cfg {scale} sde={sde} step {k}: z {ez:.2e} v {ev:.2e}", flush=True)
+        assert ez <= tol and ev <= TOL_V[dtype], (k, ez, ev)
+    # refinement of candidate 1 with guidance, step by step from the GPU's own draft latent
+    lat = pool.latents[1:2].clone()
+    ref = lat.cpu().numpy().astype(np.float64)
     for k in range(wl.steps_draft, wl.steps_total):
+        prev, prev_ref = lat.cpu().numpy().astype(np.float64), ref
+        pool.refine_step(k, latents=lat, cond_index=wl.cond_index()[1:2])
         ref = odit.refine_step(W, wl.shape, ref, sched[k], sched[k + 1], kv, wl.cond_index()[1:2],
                                cfg=(scale, unc[:1]))
-    err = rel_l2(out.cpu().numpy().astype(np.float64), ref)
-    print(f"{name} {dtype} guided refine: {err:.2e}", flush=True)
-    assert err <= tol
+        torch.cuda.synchronize()
+        got = lat.cpu().numpy().astype(np.float64)
+        err = rel_l2(got, ref)
+        ev = rel_l2(step_velocity(got, prev, sched[k], sched[k + 1]),
+                    step_velocity(ref, prev_ref, sched[k], sched[k + 1]))
+        print(f"{name} {dtype} guided refine step {k}: z {err:.2e} v {ev:.2e}", flush=True)
+        assert err <= tol and ev <= TOL_V[dtype], (k, err, ev)
     pool.close()
 
 

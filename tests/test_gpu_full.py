@@ -1,15 +1,23 @@
 """Full-size parity: the draft step at the workloads' real shapes and launch configurations, on
 candidates the oracle can follow one by one (candidates are independent, so a subset is a valid
 check of the whole pool's launch).  Tolerances as in test_gpu_step.py (bf16 mode: latents 2e-2,
-velocity 5e-2, rel-L2 per step); traces bit-exact."""
+velocity 3e-2, rel-L2 per step); traces bit-exact.
+
+The two 1.3B-shaped pools run their whole truncated trajectories (Sec. 4.1 (1)-(3), Eq. 2-7): every
+computed step, the order-0/1/2 proxy steps and the wrap of the three-slot cache ring.  The 14B-shaped
+pool is too large for the oracle to follow a whole step (80 TFLOP per candidate step in fp64), so it
+is checked at its real shape by sampled outputs: one computed block of one candidate against the
+oracle's block from the same input, dispatch against the oracle's dispatcher at every step, and a
+bit-identical repeat; the 2-block stand-in at the same layer shapes is followed end to end."""
 import time
 
 import numpy as np
 import pytest
 
+from oracle import dispatch as odisp
 from oracle import dit as odit
 from paper_2607_04461_amd import synth
-from tests._util import rel_l2
+from tests._util import TOL_V, rel_l2, step_velocity
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -23,7 +31,10 @@ def _gpu():
     flashbon.load()
 
 
-def _run(name, candidates, steps):
+def _run(name, candidates, steps, refine_steps=0):
+    """Draft ``steps`` steps of the named pool on the GPU, then follow ``candidates`` with the oracle
+    step by step; then refine the last candidate ``refine_steps`` steps from the GPU's draft latent on
+    both sides (Sec. 4.2 Stage 3, Eq. 13)."""
     from paper_2607_04461_amd.pool import DraftPool
     wl = synth.WORKLOADS[name]
     flat, W = synth.make_weights(wl.shape, wl.seed_w, threads=16)
@@ -37,37 +48,123 @@ def _run(name, candidates, steps):
         gpu_tr.append(pool.draft_step(k))
         torch.cuda.synchronize()
         gpu_z.append(pool.latents.cpu().numpy()[candidates].astype(np.float64))
+    sel = candidates[-1]
+    refined = []
+    if refine_steps:
+        lat = pool.latents[sel:sel + 1].clone()
+        for k in range(steps, steps + refine_steps):
+            pool.refine_step(k, latents=lat, cond_index=wl.cond_index()[sel:sel + 1])
+            torch.cuda.synchronize()
+            refined.append(lat.cpu().numpy().astype(np.float64))
     pool.close()
     del pool, flat
     t0 = time.time()
     kv = odit.prepare_text(W, wl.shape, text)
     cache = odit.PoolCache(wl.shape.num_blocks)
     z = z0.astype(np.float64)
+    orders = set()
     for k in range(steps):
         skip, proxy = wl.masks(k)
         z_prev = z
         z, tr = odit.draft_step(W, wl.shape, z, sched[k], sched[k + 1], kv, wl.cond_index(), skip, proxy,
                                 cache, candidates=candidates)
         assert gpu_tr[k] == [tuple(e) for e in tr], f"trace step {k}"
-        dt = float(sched[k + 1]) - float(sched[k])
+        orders |= {e[1] for e in tr if e[0] == odisp.PROXY and e[3]}
         prev = z0[candidates].astype(np.float64) if k == 0 else gpu_z[k - 1]
         ez = rel_l2(gpu_z[k], z[candidates])
-        ev = rel_l2((gpu_z[k] - prev) / dt, (z[candidates] - z_prev[candidates]) / dt)
-        print(f"{name} step {k} candidates {candidates}: z {ez:.2e} v {ev:.2e} "
-              f"(oracle {time.time() - t0:.0f}s)", flush=True)
-        assert ez <= 2e-2 and ev <= 5e-2
+        ev = rel_l2(step_velocity(gpu_z[k], prev, sched[k], sched[k + 1]),
+                    step_velocity(z[candidates], z_prev[candidates], sched[k], sched[k + 1]))
+        n_skip = int(skip.sum())
+        print(f"{name} step {k} ({n_skip} skipped, live proxy orders {sorted(orders)}) candidates {candidates}: "
+              f"z {ez:.2e} v {ev:.2e} (oracle {time.time() - t0:.0f}s)", flush=True)
+        assert ez <= 2e-2 and ev <= TOL_V["bf16"], (k, ez, ev)
+    if refine_steps:
+        ref = gpu_z[-1][-1:]                      # the GPU's draft of `sel`, the same input on both sides
+        prev_g = ref
+        for i, k in enumerate(range(steps, steps + refine_steps)):
+            prev_ref = ref
+            ref = odit.refine_step(W, wl.shape, ref, sched[k], sched[k + 1], kv, wl.cond_index()[sel:sel + 1])
+            ez = rel_l2(refined[i], ref)
+            ev = rel_l2(step_velocity(refined[i], prev_g, sched[k], sched[k + 1]),
+                        step_velocity(ref, prev_ref, sched[k], sched[k + 1]))
+            prev_g = refined[i]
+            print(f"{name} refine step {k} candidate {sel}: z {ez:.2e} v {ev:.2e} "
+                  f"(oracle {time.time() - t0:.0f}s)", flush=True)
+            assert ez <= 2e-2 and ev <= TOL_V["bf16"], (k, ez, ev)
+    return orders
 
 
-def test_pool16_last_candidate_compute_and_proxy_steps():
-    """The benchmark pool (N=16, 1560 tokens): step 0 computes 20 blocks, step 1 is all proxies."""
-    _run("wan1.3b_pool16", [15], 2)
+@pytest.mark.timeout(900)
+def test_pool16_whole_draft_and_refinement():
+    """The benchmark pool (N=16, 1560 tokens), all 10 draft steps on candidate 15: 20 blocks computed on
+    even steps, the last non-skipped block's proxy on odd steps, orders 0, 1 and 2, the ring wrapping
+    at step 6; then the first two refinement steps of that candidate."""
+    orders = _run("wan1.3b_pool16", [15], 10, refine_steps=2)
+    assert orders == {0, 1, 2}
 
 
-def test_pool64_four_prompts():
-    """N=64 at 1024 tokens, candidates split over 4 prompts; one candidate of prompt 1 and 3."""
-    _run("wan1.3b_pool64", [16, 63], 2)
+@pytest.mark.timeout(900)
+def test_pool64_whole_draft():
+    """N=64 at 1024 tokens over 4 prompts, all 12 steps on one candidate of prompt 3 (index 63): per-step
+    skip masks of 6 up to 15 blocks."""
+    wl = synth.WORKLOADS["wan1.3b_pool64"]
+    assert int(wl.cond_index()[63]) == 3
+    assert {int(wl.masks(k)[0].sum()) for k in range(12)} >= {6, 15}
+    _run("wan1.3b_pool64", [63], 12)
 
 
 def test_14b_shaped_layers():
-    """D=5120, 40 heads, MLP 13824, 4096 tokens, N=4: step 0 computed, step 1 skip + proxy."""
+    """Stand-in at the 14B layer shapes (D=5120, 40 heads, MLP 13824, 4096 tokens, N=4) in a 2-block
+    model the oracle follows end to end: step 0 computed, step 1 skip + proxy."""
     _run("wan14b_2block", [3], 2)
+
+
+@pytest.mark.timeout(900)
+def test_14b_pool_as_specified():
+    """The 14B-shaped pool as specified (40 blocks, N=4, 4096 tokens, S'=8, blocks 24..35 skipped,
+    proxies on odd steps) on the GPU:
+      * dispatch of every step equals the oracle dispatcher's, bit for bit;
+      * block 0 of candidate 3 at step 0 (its input and output from the hidden-state dump) matches the
+        oracle's block from the same input (rel-L2 of the block's update <= 2e-2);
+      * the latents stay finite, and a second run of the whole draft is bit-identical."""
+    from paper_2607_04461_amd.pool import DraftPool
+    wl = synth.WORKLOADS["wan14b_pool4"]
+    L, T, D, n = wl.shape.num_blocks, wl.tokens, wl.shape.hidden, wl.n
+    t0 = time.time()
+    flat, W = synth.make_weights(wl.shape, wl.seed_w, threads=16)
+    z0 = synth.make_latents(n, wl.shape.latent_channels, wl.latent_h, wl.latent_w)
+    text = synth.make_text(wl.n_cond, wl.text_len, wl.shape.text_dim)
+    print(f"14B weights drawn in {time.time() - t0:.0f}s", flush=True)
+    pool = DraftPool(wl, dtype="bf16", weights=flat)
+    print(f"14B model initialised at {time.time() - t0:.0f}s", flush=True)
+    sched = wl.schedule()
+    meta = odisp.empty_meta(L)
+    finals = []
+    dump = torch.empty((L + 1, n, T, D), dtype=torch.float32, device="cuda")
+    for rep in range(2):
+        pool.reset(z0)
+        for k in range(wl.steps_draft):
+            tr = pool.draft_step(k, hidden_dump=dump if (rep == 0 and k == 0) else None)
+            if rep == 0:
+                skip, proxy = wl.masks(k)
+                tr_ref, meta = odisp.plan_step(skip, proxy, meta, sched[k])
+                assert tr == [tuple(e) for e in tr_ref], f"trace step {k}"
+                if k == 0:
+                    torch.cuda.synchronize()
+                    h_in = dump[0, 3].cpu().numpy().astype(np.float64)
+                    h_out = dump[1, 3].cpu().numpy().astype(np.float64)
+        torch.cuda.synchronize()
+        finals.append(pool.latents.clone())
+        print(f"14B pool draft {rep} done at {time.time() - t0:.0f}s", flush=True)
+    pool.close()
+    del pool, dump, flat
+    assert torch.isfinite(finals[0]).all()
+    assert torch.equal(finals[0], finals[1])
+    # oracle: block 0 of candidate 3 at t_0 from the GPU's own block input
+    bm, _ = odit.modulations(W, 1, wl.shape.freq_dim, sched[0])
+    kv0 = odit.text_kv(W, 1, text[0], wl.shape.ln_eps)[0]
+    ref = odit.block_forward(W, 0, h_in, bm[0], kv0, wl.shape.heads, wl.shape.ln_eps)
+    err = rel_l2(h_out - h_in, ref - h_in)
+    print(f"14B block 0 candidate 3 step 0: update rel-L2 {err:.2e}, output rel-L2 {rel_l2(h_out, ref):.2e} "
+          f"(oracle at {time.time() - t0:.0f}s)", flush=True)
+    assert err <= 2e-2

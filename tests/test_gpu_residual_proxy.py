@@ -5,7 +5,7 @@ import pytest
 
 from oracle import dit as odit
 from paper_2607_04461_amd import synth
-from tests._util import rel_l2
+from tests._util import TOL_V, rel_l2, step_velocity
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -36,15 +36,19 @@ def test_residual_proxy_trajectory_matches_oracle(name, dtype, tol):
     live_proxies = 0
     for k in range(wl.steps_draft):
         skip, proxy = wl.masks(k)
+        z_prev_ref, z_prev = z_ref, pool.latents.cpu().numpy().astype(np.float64)
         z_ref, tr_ref = odit.draft_step(W, wl.shape, z_ref, sched[k], sched[k + 1], kv, wl.cond_index(), skip,
                                         proxy, cache, residual=True)
         tr = pool.draft_step(k)
         torch.cuda.synchronize()
         assert tr == [tuple(e) for e in tr_ref], f"trace step {k}"
         live_proxies += sum(1 for e in tr if e[0] == 2)
-        ez = rel_l2(pool.latents.cpu().numpy().astype(np.float64), z_ref)
-        print(f"{name} {dtype} residual proxy step {k}: z {ez:.2e}", flush=True)
-        assert ez <= tol, (k, ez)
+        got = pool.latents.cpu().numpy().astype(np.float64)
+        ez = rel_l2(got, z_ref)
+        ev = rel_l2(step_velocity(got, z_prev, sched[k], sched[k + 1]),
+                    step_velocity(z_ref, z_prev_ref, sched[k], sched[k + 1]))
+        print(f"{name} {dtype} residual proxy step {k}: z {ez:.2e} v {ev:.2e}", flush=True)
+        assert ez <= tol and ev <= TOL_V[dtype], (k, ez, ev)
     assert live_proxies > 0
     pool.close()
 

@@ -12,7 +12,7 @@ import pytest
 from oracle import dit as odit
 from oracle import sde as osde
 from paper_2607_04461_amd import synth
-from tests._util import rel_l2
+from tests._util import TOL_V, rel_l2, step_velocity
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -122,6 +122,7 @@ def test_stochastic_draft_trajectory_matches_oracle(name, dtype, tol):
     a, seed = 0.3, 4242
     for k in range(wl.steps_draft):
         skip, proxy = wl.masks(k)
+        z_prev_ref, z_prev = z_ref, pool.latents.cpu().numpy().astype(np.float64)
         z_ref, tr_ref = odit.draft_step(W, wl.shape, z_ref, sched[k], sched[k + 1], kv, wl.cond_index(),
                                         skip, proxy, cache, sde_args=(a, seed, k))
         tr = pool.draft_step(k, sde=(a, seed))
@@ -129,8 +130,11 @@ def test_stochastic_draft_trajectory_matches_oracle(name, dtype, tol):
         got = pool.latents.cpu().numpy().astype(np.float64)
         assert tr == [tuple(e) for e in tr_ref], f"trace step {k}"
         ez = rel_l2(got, z_ref)
-        print(f"{name} {dtype} sde step {k}: z {ez:.2e}", flush=True)
-        assert ez <= tol, (k, ez)
+        # drift v + sigma^2 / (2 t) (z + (1 - t) v): the known noise term removed on both sides
+        ev = rel_l2(step_velocity(got, z_prev, sched[k], sched[k + 1], (a, seed, k, 0)),
+                    step_velocity(z_ref, z_prev_ref, sched[k], sched[k + 1], (a, seed, k, 0)))
+        print(f"{name} {dtype} sde step {k}: z {ez:.2e} drift {ev:.2e}", flush=True)
+        assert ez <= tol and ev <= TOL_V[dtype], (k, ez, ev)
     pool.close()
 
 

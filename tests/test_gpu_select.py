@@ -9,7 +9,7 @@ import pytest
 from oracle import dit as odit
 from oracle import select as osel
 from paper_2607_04461_amd import synth
-from tests._util import rel_l2
+from tests._util import TOL_V, rel_l2, step_velocity
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -62,4 +62,23 @@ def test_select_then_refine_matches_oracle(dtype, tol):
     err_s = rel_l2(out_s.cpu().numpy().astype(np.float64), ref_s)
     print(f"select+refine {dtype} stochastic: rel-L2 {err_s:.2e}", flush=True)
     assert err_s <= tol
+    # per refinement step, from the same input on both sides (the GPU's draft of the winner): latent and
+    # velocity (Euler), latent and drift with the known noise removed (stochastic, counter row j)
+    for sde in (None, (a, seed)):
+        lat = drafts[j:j + 1].clone()
+        ref = lat.cpu().numpy().astype(np.float64)
+        for k in range(wl.steps_draft, wl.steps_total):
+            prev, prev_ref = lat.cpu().numpy().astype(np.float64), ref
+            pool.refine_step(k, latents=lat, cond_index=wl.cond_index()[j:j + 1],
+                             sde=None if sde is None else (sde[0], sde[1], j))
+            ref = odit.refine_step(W, wl.shape, ref, sched[k], sched[k + 1], kv, wl.cond_index()[j:j + 1],
+                                   sde_args=None if sde is None else (sde[0], sde[1], k, j))
+            torch.cuda.synchronize()
+            got = lat.cpu().numpy().astype(np.float64)
+            noise = None if sde is None else (sde[0], sde[1], k, j)
+            ez = rel_l2(got, ref)
+            ev = rel_l2(step_velocity(got, prev, sched[k], sched[k + 1], noise),
+                        step_velocity(ref, prev_ref, sched[k], sched[k + 1], noise))
+            print(f"refine {dtype} sde={sde} step {k}: z {ez:.2e} v {ev:.2e}", flush=True)
+            assert ez <= tol and ev <= TOL_V[dtype], (k, ez, ev)
     pool.close()
