@@ -213,6 +213,21 @@ flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args)
  * skip, proxy, cache and meta are ignored (may be NULL).  trace, if given, reports all COMPUTE. */
 flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args);
 
+/* Refinement step that allocates nothing and touches no model workspace -- for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * it), and for refining one pool's winner on one stream while the same model drafts on another.
+ * Same arguments, results (bit for bit) and validation as flashbon_refine_step.  The step's working
+ * buffers (residual stream, activations, timestep path, text projection when *text_kv_valid is 0,
+ * prompt indices, rotary table) come from a static device array of FLASHBON_NOALLOC_SCRATCH_BYTES that
+ * the library holds on every GPU it runs on until the process ends; nothing in it has to start at
+ * zero.  FLASHBON_ESHAPE, before any device work, if a call needs more (about 70 MB for one candidate
+ * of the 1.3B-shaped model at 1560 tokens in bf16 mode, 118 MB in fp32 mode) or more than 128 token-row
+ * blocks; FLASHBON_EINVAL if the current device is not the model's.  Every call on a GPU shares that
+ * GPU's array: calls of this entry point that overlap on one GPU (other streams, other threads, other
+ * models) race.  No timing sites are recorded. */
+#define FLASHBON_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+flashbon_status flashbon_refine_step_noalloc(void *model, const flashbon_step_args *args);
+
 /* Release the model.  NULL is a no-op.  Synchronises the device before freeing. */
 void flashbon_free(void *model);
 

@@ -395,6 +395,25 @@ hipError_t launch_block_mods(int L, int width, const float *m, const float *tabl
 }
 
 // ------------------------------------------------------------------------------------ conversion
+// up to 128 int32 values carried in the kernel arguments, written to dst[0 .. n)
+struct I32Args {
+  int32_t n;
+  int32_t v[128];
+};
+__global__ __launch_bounds__(128) void k_store_i32(I32Args args, int32_t *__restrict__ dst) {
+  const int i = threadIdx.x;
+  if (i < args.n) dst[i] = args.v[i];
+}
+
+hipError_t launch_store_i32(int n, const int32_t *vals, int32_t *dst, hipStream_t s) {
+  if (n < 0 || n > 128) return hipErrorInvalidValue;
+  I32Args args{};
+  args.n = n;
+  for (int i = 0; i < n; ++i) args.v[i] = vals[i];
+  hipLaunchKernelGGL(k_store_i32, dim3(1), dim3(128), 0, s, args, dst);
+  return hipGetLastError();
+}
+
 __global__ __launch_bounds__(256) void k_f32_to_bf16(int64_t n, const float *__restrict__ x,
                                                      bf16 *__restrict__ y) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;

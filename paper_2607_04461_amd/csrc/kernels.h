@@ -75,6 +75,10 @@ hipError_t launch_block_mods(int L, int width, const float *m, const float *tabl
 
 hipError_t launch_f32_to_bf16(int64_t count, const float *x, void *y, hipStream_t s);
 
+// dst[i] = vals[i], i < n <= 128, the values travelling in the kernel's arguments (nothing on the host
+// has to outlive the call)
+hipError_t launch_store_i32(int n, const int32_t *vals, int32_t *dst, hipStream_t s);
+
 // qk RMSNorm + 3-D rotary embedding: (cos, sin) table [T][dh/2] for a token grid of width wp; and the
 // in-place normalisation (gain over D, eps) of M rows of x (act, row stride rs), rotated by the table
 // (row % tokens) when tab is not null.  D % 8 == 0.

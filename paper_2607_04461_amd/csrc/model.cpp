@@ -4,6 +4,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -78,6 +79,51 @@ Layout make_layout(const flashbon_model_config &c) {
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---------------------------------------------------------------- scratch of the allocation-free step
+// One array per GPU, loaded with the library's code object and held until the process ends.  In host
+// code its name is only a stand-in: the device address comes from hipGetSymbolAddress, taken once per
+// device with that device current, and only that address is handed to kernels.
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+static std::mutex g_scratch_mu;
+static char *g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t scratch_base(int device, char **out) {
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device) return hipErrorInvalidDevice;
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = (char *)p;
+  }
+  *out = g_scratch_ptr[device];
+  return hipSuccess;
+}
+
+size_t scratch_layout(const Model *m, int rows, int tokens, int text_rows, char *base, StepBufs *B) {
+  const size_t D = m->D, F = m->F, P = m->P, M = (size_t)rows * tokens, a = m->asz;
+  size_t off = 0;
+  auto carve = [&](size_t bytes) { size_t r = off; off += align256(bytes); return base ? base + r : nullptr; };
+  char *h = carve(M * D * 4), *act = carve(M * D * a), *qkv = carve(M * 3 * D * a), *o = carve(M * D * a),
+       *u = carve(M * F * a), *tok = carve(M * P * a), *vtok = carve(M * P * 4),
+       *txt = carve(m->act == ACT_BF16 ? (size_t)text_rows * m->Dt * a : 0), *ctx = carve((size_t)text_rows * D * a),
+       *tf = carve(m->fd * 4), *e1 = carve(D * 4), *e = carve(D * 4), *m6 = carve(6 * D * 4),
+       *bm = carve((size_t)m->L * 6 * D * 4), *hm = carve(2 * D * 4), *cond = carve((size_t)rows * 4),
+       *rope = carve(m->c.qk_norm_rope ? (size_t)tokens * (m->dh / 2) * 8 : 0);
+  if (B) {
+    B->h = (float *)h; B->a = act; B->qkv = qkv; B->o = o; B->u = u; B->tok = tok; B->vtok = (float *)vtok;
+    B->txt = txt; B->ctx = ctx; B->tf = (float *)tf; B->e1 = (float *)e1; B->e = (float *)e; B->m6 = (float *)m6;
+    B->bmods = (float *)bm; B->hmod = (float *)hm; B->d_cond = (int32_t *)cond;
+    B->rope = m->c.qk_norm_rope ? (float2 *)rope : nullptr;
+  }
+  return off;
+}
 
 }  // namespace fb
 
@@ -163,12 +209,19 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
   if (hipMalloc(&m->ws, off) != hipSuccess) return cleanup(FLASHBON_ENOMEM, "workspace of " + std::to_string(off) + " bytes");
   m->ws_bytes = off;
   char *w = (char *)m->ws;
-  m->h = (float *)(w + o_h); m->a = w + o_a; m->qkv = w + o_qkv; m->o = w + o_o; m->u = w + o_u;
-  m->tok = w + o_tok; m->txt = w + o_txt; m->ctx = w + o_ctx;
-  m->tf = (float *)(w + o_tf); m->e1 = (float *)(w + o_e1); m->e = (float *)(w + o_e);
-  m->m6 = (float *)(w + o_m6); m->bmods = (float *)(w + o_bm); m->hmod = (float *)(w + o_hm);
-  m->d_cond = (int32_t *)(w + o_cond); m->vtok = (float *)(w + o_v);
-  if (cfg->qk_norm_rope) m->rope = (float2 *)(w + o_rope);
+  StepBufs &B = m->bufs;
+  B.h = (float *)(w + o_h); B.a = w + o_a; B.qkv = w + o_qkv; B.o = w + o_o; B.u = w + o_u;
+  B.tok = w + o_tok; B.txt = w + o_txt; B.ctx = w + o_ctx;
+  B.tf = (float *)(w + o_tf); B.e1 = (float *)(w + o_e1); B.e = (float *)(w + o_e);
+  B.m6 = (float *)(w + o_m6); B.bmods = (float *)(w + o_bm); B.hmod = (float *)(w + o_hm);
+  B.d_cond = (int32_t *)(w + o_cond); B.vtok = (float *)(w + o_v);
+  if (cfg->qk_norm_rope) B.rope = (float2 *)(w + o_rope);
+  // the allocation-free step's scratch array of this device: its address, once per device
+  {
+    char *base = nullptr;
+    hipError_t e = scratch_base(m->device, &base);
+    if (e != hipSuccess) return cleanup(FLASHBON_EHIP, std::string("scratch address: ") + hipGetErrorString(e));
+  }
 
   if (hipMemcpy(m->w32, host_weights, total * 4, hipMemcpyHostToDevice) != hipSuccess)
     return cleanup(FLASHBON_EHIP, "weight upload");
@@ -240,8 +293,8 @@ static hipError_t harvest(Model *m, int site) {
 
 // Run `launch` (returning hipError_t), bracketed by events when the site is timed.
 template <typename F>
-static hipError_t timed(Model *m, int site, hipStream_t s, F &&launch) {
-  if (!(m->timing_mask & (1u << site))) return launch();
+static hipError_t timed(Model *m, uint32_t mask, int site, hipStream_t s, F &&launch) {
+  if (!(mask & (1u << site))) return launch();
   hipEvent_t e0, e1;
   hipError_t e = take_event(m, &e0);
   if (e == hipSuccess) e = take_event(m, &e1);
@@ -254,7 +307,7 @@ static hipError_t timed(Model *m, int site, hipStream_t s, F &&launch) {
   return hipSuccess;
 }
 
-static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draft) {
+static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draft, bool noalloc = false) {
   if (!m) return fail(FLASHBON_EINVAL, "model is NULL");
   if (!a) return fail(FLASHBON_EINVAL, "args is NULL");
   const flashbon_model_config &c = m->c;
@@ -322,6 +375,23 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   if (stochastic && !sde_coefficients(a->t_cur, a->t_next, a->sde_a, a->sde_seed, a->sde_step, a->sde_row0, &sde))
     return fail(FLASHBON_EINVAL, "stochastic update needs sde_a >= 0, finite, and 0 < t_cur <= 1 (t_next < 1 when t_cur = 1)");
 
+  // the step's working buffers: the model workspace, or this device's scratch array (sized for this call)
+  StepBufs B = m->bufs;
+  const uint32_t tmask = noalloc ? 0u : m->timing_mask;
+  if (noalloc) {
+    if (R > kMaxScratchRows) return fail(FLASHBON_ESHAPE, "allocation-free step: more than 128 token rows of candidates");
+    const size_t need = scratch_layout(m, R, T, *a->text_kv_valid ? 0 : a->n_cond * a->text_len, nullptr, nullptr);
+    if (need > kScratchBytes)
+      return fail(FLASHBON_ESHAPE, "allocation-free step needs " + std::to_string(need) + " bytes of scratch, the limit is " +
+                                       std::to_string(kScratchBytes));
+    int dev = -1;
+    HIPCHK(hipGetDevice(&dev), "hipGetDevice");
+    if (dev != m->device) return fail(FLASHBON_EINVAL, "allocation-free step: the model's device must be current");
+    char *base = nullptr;
+    HIPCHK(scratch_base(dev, &base), "scratch address");
+    scratch_layout(m, R, T, *a->text_kv_valid ? 0 : a->n_cond * a->text_len, base, &B);
+  }
+
   // ---------------------------------------------------------------- enqueue
   hipStream_t s = (hipStream_t)a->stream;
   const ActType act = m->act;
@@ -331,12 +401,15 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   };
   auto Bp = [&](size_t off) -> const float * { return m->w32 + off; };
 
-  // cond_index -> device, only when it changed (the previous step may still read the old copy)
+  // cond_index -> device.  Model workspace: only when it changed (the previous step may still read the
+  // old copy).  Scratch: every call, as kernel arguments (no host memory outlives the call).
   std::vector<int32_t> cond(a->cond_index, a->cond_index + a->n);
   if (guided) cond.insert(cond.end(), a->uncond_index, a->uncond_index + a->n);
-  if (cond != m->last_cond) {
+  if (noalloc) {
+    HIPCHK(launch_store_i32((int)cond.size(), cond.data(), B.d_cond, s), "cond_index upload");
+  } else if (cond != m->last_cond) {
     HIPCHK(hipStreamSynchronize(s), "synchronise before cond_index upload");
-    HIPCHK(hipMemcpy(m->d_cond, cond.data(), sizeof(int32_t) * cond.size(), hipMemcpyHostToDevice), "cond_index upload");
+    HIPCHK(hipMemcpy(B.d_cond, cond.data(), sizeof(int32_t) * cond.size(), hipMemcpyHostToDevice), "cond_index upload");
     m->last_cond = cond;
   }
 
@@ -345,45 +418,48 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   if (*a->text_kv_valid == 0) {
     const void *txt = a->text;
     if (act == ACT_BF16) {
-      HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_f32_to_bf16((int64_t)NC * Lt * m->Dt, a->text, m->txt, s); }), "text convert");
-      txt = m->txt;
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_f32_to_bf16((int64_t)NC * Lt * m->Dt, a->text, B.txt, s); }), "text convert");
+      txt = B.txt;
     }
     EpiArgs e;
-    e.out = m->ctx; e.ldo = D; e.bias = Bp(m->lay.txt_b);
-    HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s); }), "text projection");
+    e.out = B.ctx; e.ldo = D; e.bias = Bp(m->lay.txt_b);
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s); }), "text projection");
     for (int l = 0; l < L; ++l) {
       EpiArgs k;
       k.out = (char *)a->text_kv + (size_t)l * kv_block * asz; k.ldo = 2 * D; k.bias = Bp(m->lay.blk[l].bkvc);
-      HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, m->ctx, Wp(m->lay.blk[l].wkvc), k, s); }), "text K/V");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, B.ctx, Wp(m->lay.blk[l].wkvc), k, s); }), "text K/V");
       if (c.qk_norm_rope)
-        HIPCHK(timed(m, FLASHBON_SITE_TEXT, s, [&] { return launch_qk_norm(act, NC * Lt, D, m->dh, k.out, 2 * D, Bp(m->lay.blk[l].nkc), c.ln_eps, nullptr, 1, s); }),
+        HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_qk_norm(act, NC * Lt, D, m->dh, k.out, 2 * D, Bp(m->lay.blk[l].nkc), c.ln_eps, nullptr, 1, s); }),
                "text key RMSNorm");
     }
   }
 
   // timestep conditioning, shared by all candidates
-  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_time_features((double)a->t_cur, m->fd, m->tf, s); }), "time features");
-  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(D, m->fd, m->w32 + m->lay.t_w1, Bp(m->lay.t_b1), m->tf, m->e1, 0, 1, s); }), "time mlp 1");
-  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(D, D, m->w32 + m->lay.t_w2, Bp(m->lay.t_b2), m->e1, m->e, 0, 0, s); }), "time mlp 2");
-  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(6 * D, D, m->w32 + m->lay.mod_w, Bp(m->lay.mod_b), m->e, m->m6, 1, 0, s); }), "modulation");
-  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(2 * D, D, m->w32 + m->lay.hmod_w, Bp(m->lay.hmod_b), m->e, m->hmod, 1, 0, s); }), "head modulation");
-  HIPCHK(timed(m, FLASHBON_SITE_TIME, s, [&] { return launch_block_mods(L, 6 * D, m->m6, m->w32 + m->lay.blk[0].mod, (int64_t)m->lay.block_stride, m->bmods, s); }),
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_TIME, s, [&] { return launch_time_features((double)a->t_cur, m->fd, B.tf, s); }), "time features");
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(D, m->fd, m->w32 + m->lay.t_w1, Bp(m->lay.t_b1), B.tf, B.e1, 0, 1, s); }), "time mlp 1");
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(D, D, m->w32 + m->lay.t_w2, Bp(m->lay.t_b2), B.e1, B.e, 0, 0, s); }), "time mlp 2");
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(6 * D, D, m->w32 + m->lay.mod_w, Bp(m->lay.mod_b), B.e, B.m6, 1, 0, s); }), "modulation");
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_TIME, s, [&] { return launch_gemv(2 * D, D, m->w32 + m->lay.hmod_w, Bp(m->lay.hmod_b), B.e, B.hmod, 1, 0, s); }), "head modulation");
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_TIME, s, [&] { return launch_block_mods(L, 6 * D, B.m6, m->w32 + m->lay.blk[0].mod, (int64_t)m->lay.block_stride, B.bmods, s); }),
          "block modulation");
 
-  // rotary table of this latent size (kept while the size does not change)
-  if (c.qk_norm_rope && (m->rope_h != a->latent_h || m->rope_w != a->latent_w)) {
-    HIPCHK(launch_rope_table(T, a->latent_w / p, m->dh, m->rope, s), "rotary table");
-    m->rope_h = a->latent_h;
-    m->rope_w = a->latent_w;
+  // rotary table of this latent size (kept in the model workspace while the size does not change; made
+  // on every call in scratch)
+  if (c.qk_norm_rope && (noalloc || m->rope_h != a->latent_h || m->rope_w != a->latent_w)) {
+    HIPCHK(launch_rope_table(T, a->latent_w / p, m->dh, B.rope, s), "rotary table");
+    if (!noalloc) {
+      m->rope_h = a->latent_h;
+      m->rope_w = a->latent_w;
+    }
   }
 
   const int64_t MD = M * D;
   // Where the residual stream currently lives.  A computed block of a draft step (output reading of
   // the proxy) writes its new rows only into its cache slot, which then serves as the stream until the
   // next block writes: the next computed block reads it there and its self-attention output
-  // projection writes the updated rows back into m->h; a proxy writes m->h; a skip leaves it.  This
+  // projection writes the updated rows back into B.h; a proxy writes B.h; a skip leaves it.  This
   // saves the second copy of every computed block's output.
-  const float *hcur = m->h;
+  const float *hcur = B.h;
   auto dump = [&](int idx) -> flashbon_status {
     if (!a->hidden_dump) return FLASHBON_OK;
     HIPCHK(hipMemcpyAsync(a->hidden_dump + (int64_t)idx * MD, hcur, MD * 4, hipMemcpyDeviceToDevice, s), "hidden dump");
@@ -400,10 +476,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   // dump then leaves those entries untouched (their values are never formed).
   bool formed = embed_live;
   if (embed_live) {
-    HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, R, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, m->tok, s); }), "patchify");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, R, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, B.tok, s); }), "patchify");
     EpiArgs e;
-    e.out = m->h; e.ldo = D; e.bias = Bp(m->lay.pe_b);
-    HIPCHK(timed(m, FLASHBON_SITE_EMBED, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, D, P, m->tok, Wp(m->lay.pe_w), e, s); }), "patch embed");
+    e.out = B.h; e.ldo = D; e.bias = Bp(m->lay.pe_b);
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_EMBED, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, D, P, B.tok, Wp(m->lay.pe_w), e, s); }), "patch embed");
     if ((st = dump(0)) != FLASHBON_OK) return st;
   }
 
@@ -411,7 +487,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
   for (int l = 0; l < L; ++l) {
     const flashbon_trace_entry &tr = trace[l];
     const BlockOff &b = m->lay.blk[l];
-    const float *mod = m->bmods + (int64_t)l * 6 * D;
+    const float *mod = B.bmods + (int64_t)l * 6 * D;
     if (tr.action == FLASHBON_SKIP) {
       if (formed && (st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
@@ -424,9 +500,9 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
       const flashbon_cache_meta &mb = a->meta[l];
       const int s1 = (mb.head + 2) % 3, s2 = (mb.head + 1) % 3, s3 = mb.head;
       auto slot_ptr = [&](int sl) { return a->cache + ((int64_t)l * 3 + sl) * MD; };
-      HIPCHK(timed(m, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], m->h, s, residual); }),
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_PROXY, s, [&] { return launch_proxy(MD, slot_ptr(s1), slot_ptr(s2), slot_ptr(s3), tr.order, ca[l], cb[l], B.h, s, residual); }),
              "activation proxy");
-      hcur = m->h;
+      hcur = B.h;
       formed = true;
       if ((st = dump(l + 1)) != FLASHBON_OK) return st;
       continue;
@@ -434,93 +510,93 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     // COMPUTE (Eq. 7); the residual reading first keeps the block input in its cache slot, which the
     // down-projection epilogue turns into the block's delta
     if (residual)
-      HIPCHK(hipMemcpyAsync(a->cache + ((int64_t)l * 3 + tr.slot) * MD, m->h, MD * 4, hipMemcpyDeviceToDevice, s),
+      HIPCHK(hipMemcpyAsync(a->cache + ((int64_t)l * 3 + tr.slot) * MD, B.h, MD * 4, hipMemcpyDeviceToDevice, s),
              "block input to cache");
-    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, mod + 0 * D, mod + 1 * D, m->a, s); }), "adaLN 1");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, mod + 0 * D, mod + 1 * D, B.a, s); }), "adaLN 1");
     {
-      EpiArgs e; e.out = m->qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
-      HIPCHK(timed(m, FLASHBON_SITE_QKV, s, [&] { return launch_linear(act, EPI_STORE, (int)M, 3 * D, D, m->a, Wp(b.wqkv), e, s); }), "qkv projection");
+      EpiArgs e; e.out = B.qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_QKV, s, [&] { return launch_linear(act, EPI_STORE, (int)M, 3 * D, D, B.a, Wp(b.wqkv), e, s); }), "qkv projection");
     }
     if (c.qk_norm_rope) {
-      void *kp = (char *)m->qkv + (size_t)D * asz;
-      HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, m->qkv, 3 * D, Bp(b.nq), c.ln_eps, m->rope, T, s); }), "q RMSNorm + rotary");
-      HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, kp, 3 * D, Bp(b.nk), c.ln_eps, m->rope, T, s); }), "k RMSNorm + rotary");
+      void *kp = (char *)B.qkv + (size_t)D * asz;
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, B.qkv, 3 * D, Bp(b.nq), c.ln_eps, B.rope, T, s); }), "q RMSNorm + rotary");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, kp, 3 * D, Bp(b.nk), c.ln_eps, B.rope, T, s); }), "k RMSNorm + rotary");
     }
     {
       AttnArgs at;
       at.batch = R; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = T;
-      at.q = m->qkv; at.q_bs = (int64_t)T * 3 * D; at.q_rs = 3 * D;
-      at.k = (const char *)m->qkv + (size_t)D * asz; at.v = (const char *)m->qkv + (size_t)2 * D * asz;
+      at.q = B.qkv; at.q_bs = (int64_t)T * 3 * D; at.q_rs = 3 * D;
+      at.k = (const char *)B.qkv + (size_t)D * asz; at.v = (const char *)B.qkv + (size_t)2 * D * asz;
       at.kv_bs = (int64_t)T * 3 * D; at.kv_rs = 3 * D; at.kv_index = nullptr; at.n_kv = R;
-      at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
-      HIPCHK(timed(m, FLASHBON_SITE_ATTN_SELF, s, [&] { return launch_attention(act, at, s); }), "self-attention");
+      at.out = B.o; at.o_bs = (int64_t)T * D; at.o_rs = D;
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_ATTN_SELF, s, [&] { return launch_attention(act, at, s); }), "self-attention");
     }
     {
-      EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.bo); e.gate = mod + 2 * D;
-      if (hcur != m->h) e.res_in = hcur;
-      HIPCHK(timed(m, FLASHBON_SITE_OUT, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.wo), e, s); }), "self-attn out projection");
-      hcur = m->h;
+      EpiArgs e; e.out = B.h; e.ldo = D; e.bias = Bp(b.bo); e.gate = mod + 2 * D;
+      if (hcur != B.h) e.res_in = hcur;
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_OUT, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, B.o, Wp(b.wo), e, s); }), "self-attn out projection");
+      hcur = B.h;
     }
-    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, nullptr, nullptr, m->a, s); }), "cross LN");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, B.h, nullptr, nullptr, B.a, s); }), "cross LN");
     {
-      EpiArgs e; e.out = m->qkv; e.ldo = D; e.bias = Bp(b.bqc);
-      HIPCHK(timed(m, FLASHBON_SITE_CROSS_Q, s, [&] { return launch_linear(act, EPI_STORE, (int)M, D, D, m->a, Wp(b.wqc), e, s); }), "cross q projection");
+      EpiArgs e; e.out = B.qkv; e.ldo = D; e.bias = Bp(b.bqc);
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_CROSS_Q, s, [&] { return launch_linear(act, EPI_STORE, (int)M, D, D, B.a, Wp(b.wqc), e, s); }), "cross q projection");
     }
     if (c.qk_norm_rope)
-      HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, m->qkv, D, Bp(b.nqc), c.ln_eps, nullptr, T, s); }), "cross q RMSNorm");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, B.qkv, D, Bp(b.nqc), c.ln_eps, nullptr, T, s); }), "cross q RMSNorm");
     {
       const char *kv = (const char *)a->text_kv + (size_t)l * kv_block * asz;
       AttnArgs at;
       at.batch = R; at.heads = H; at.head_dim = dh; at.tq = T; at.tk = Lt;
-      at.q = m->qkv; at.q_bs = (int64_t)T * D; at.q_rs = D;
+      at.q = B.qkv; at.q_bs = (int64_t)T * D; at.q_rs = D;
       at.k = kv; at.v = kv + (size_t)D * asz; at.kv_bs = (int64_t)Lt * 2 * D; at.kv_rs = 2 * D;
-      at.kv_index = m->d_cond; at.n_kv = NC;
-      at.out = m->o; at.o_bs = (int64_t)T * D; at.o_rs = D;
-      HIPCHK(timed(m, FLASHBON_SITE_ATTN_CROSS, s, [&] { return launch_attention(act, at, s); }), "cross-attention");
+      at.kv_index = B.d_cond; at.n_kv = NC;
+      at.out = B.o; at.o_bs = (int64_t)T * D; at.o_rs = D;
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_ATTN_CROSS, s, [&] { return launch_attention(act, at, s); }), "cross-attention");
     }
     {
-      EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.boc);
-      HIPCHK(timed(m, FLASHBON_SITE_OUT_CROSS, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, m->o, Wp(b.woc), e, s); }), "cross out projection");
+      EpiArgs e; e.out = B.h; e.ldo = D; e.bias = Bp(b.boc);
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_OUT_CROSS, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, B.o, Wp(b.woc), e, s); }), "cross out projection");
     }
-    HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, m->h, mod + 3 * D, mod + 4 * D, m->a, s); }), "adaLN 2");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, B.h, mod + 3 * D, mod + 4 * D, B.a, s); }), "adaLN 2");
     {
-      EpiArgs e; e.out = m->u; e.ldo = F; e.bias = Bp(b.b1);
-      HIPCHK(timed(m, FLASHBON_SITE_MLP_UP, s, [&] { return launch_linear(act, EPI_GELU, (int)M, F, D, m->a, Wp(b.w1), e, s); }), "mlp up");
+      EpiArgs e; e.out = B.u; e.ldo = F; e.bias = Bp(b.b1);
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_MLP_UP, s, [&] { return launch_linear(act, EPI_GELU, (int)M, F, D, B.a, Wp(b.w1), e, s); }), "mlp up");
     }
     {
-      EpiArgs e; e.out = m->h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
+      EpiArgs e; e.out = B.h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
       float *slot = draft ? a->cache + ((int64_t)l * 3 + tr.slot) * MD : nullptr;
       if (slot && !residual) {   // the new rows go to the cache slot only, which becomes the stream
         e.out = slot;
-        e.res_in = m->h;
+        e.res_in = B.h;
       } else {
         e.cache = slot;
         e.cache_delta = residual;
       }
-      HIPCHK(timed(m, FLASHBON_SITE_MLP_DOWN, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, F, m->u, Wp(b.w2), e, s); }), "mlp down");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_MLP_DOWN, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, F, B.u, Wp(b.w2), e, s); }), "mlp down");
       hcur = (const float *)e.out;
     }
     if ((st = dump(l + 1)) != FLASHBON_OK) return st;
   }
 
   // head + unpatchify + Euler update of the latents (or the stochastic update of Eq. 20)
-  HIPCHK(timed(m, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, m->hmod, m->hmod + D, m->a, s); }), "head adaLN");
+  HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, B.hmod, B.hmod + D, B.a, s); }), "head adaLN");
   if (stochastic || guided) {
     if (!stochastic) {                      // Euler update through the same kernel: no drift term, no noise
       sde = SdeArgs{};
       sde.dt = a->t_next - a->t_cur;
     }
     EpiArgs e;
-    e.out = m->vtok; e.ldo = P; e.bias = Bp(m->lay.head_b);
-    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head");
-    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_head_update(a->n, m->C, a->latent_h, a->latent_w, p, m->vtok, guided, a->cfg_scale, a->latents, sde, a->preview, a->t_cur, s); }),
+    e.out = B.vtok; e.ldo = P; e.bias = Bp(m->lay.head_b);
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, P, D, B.a, Wp(m->lay.head_w), e, s); }), "head");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return launch_head_update(a->n, m->C, a->latent_h, a->latent_w, p, B.vtok, guided, a->cfg_scale, a->latents, sde, a->preview, a->t_cur, s); }),
            "unpatchify + guidance + update");
   } else {
     EpiArgs e;
     e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;
     e.preview = a->preview; e.t_cur = a->t_cur;
     e.C = m->C; e.H = a->latent_h; e.W = a->latent_w; e.p = p; e.T = T;
-    HIPCHK(timed(m, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_EULER, (int)M, P, D, m->a, Wp(m->lay.head_w), e, s); }), "head + Euler");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_EULER, (int)M, P, D, B.a, Wp(m->lay.head_w), e, s); }), "head + Euler");
   }
 
   // ---------------------------------------------------------------- commit host state
@@ -541,6 +617,10 @@ flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args)
 
 flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args) {
   return run_step((Model *)model, args, false);
+}
+
+flashbon_status flashbon_refine_step_noalloc(void *model, const flashbon_step_args *args) {
+  return run_step((Model *)model, args, false, true);
 }
 
 flashbon_status flashbon_set_timing(void *model, uint32_t site_mask) {

@@ -70,7 +70,9 @@ EXPORTS = [
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
     "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_linear_residual", "flashbon_op_linear_plan", "flashbon_op_attention", "flashbon_op_ln_mod",
     "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde", "flashbon_select",
+    "flashbon_refine_step_noalloc",
 ]
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 JUDGE_FN = ctypes.CFUNCTYPE(ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                             ctypes.POINTER(ctypes.c_int32))
@@ -101,6 +103,8 @@ def load() -> ctypes.CDLL:
     L.flashbon_draft_step.restype = i32
     L.flashbon_refine_step.argtypes = [vp, ctypes.POINTER(StepArgs)]
     L.flashbon_refine_step.restype = i32
+    L.flashbon_refine_step_noalloc.argtypes = [vp, ctypes.POINTER(StepArgs)]
+    L.flashbon_refine_step_noalloc.restype = i32
     L.flashbon_free.argtypes = [vp]
     L.flashbon_free.restype = None
     L.flashbon_plan_step.argtypes = [i32, ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_uint8),
@@ -376,6 +380,15 @@ def flashbon_refine_step(model, latents, t_cur, t_next, text, cond_index, text_k
                          trace=None, hidden_dump=None, stream=None, sde=None, preview=None, cfg=None):
     _step(load().flashbon_refine_step, "flashbon_refine_step", model, latents, t_cur, t_next, text,
           cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde,
+          preview=preview, cfg=cfg, draft=False)
+
+
+def flashbon_refine_step_noalloc(model, latents, t_cur, t_next, text, cond_index, text_kv, text_kv_valid,
+                                 trace=None, hidden_dump=None, stream=None, sde=None, preview=None, cfg=None):
+    """flashbon_refine_step with its working buffers in the library's static per-GPU scratch array
+    (allocates nothing; overlapping calls on one GPU race)."""
+    _step(load().flashbon_refine_step_noalloc, "flashbon_refine_step_noalloc", model, latents, t_cur, t_next,
+          text, cond_index, text_kv, text_kv_valid, None, None, None, None, trace, hidden_dump, stream, sde=sde,
           preview=preview, cfg=cfg, draft=False)
 
 
