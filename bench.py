@@ -9,8 +9,13 @@ cross-attention K/V is prepared before the timed region (it is timed separately,
 refinement of the selected candidate).
 
 Prints one JSON line.  ``value`` = candidates drafted per second.  ``roofline`` reports the dominant
-kernel (the MLP up-projection GEMM, the largest single launch) timed live with HIP events on the
-library's stream inside the timed region; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+kernel by GPU time -- the residual-epilogue GEMM (``k_linear_dma8<EPI_RESIDUAL>``: the self- and
+cross-attention output projections and the MLP down-projection with gate, residual and cache store) --
+timed live with HIP events that the library records on its launch stream around every launch of those
+sites inside the timed region; ``roofline_secondary`` does the same for the MLP up-projection.
+``cpu_baseline`` times the CPU oracle on a bounded sample.  ``c2_full_step`` is one full-quality step
+of one candidate (the refinement's steps), and ``secondary_workloads`` drafts the 14B-shaped pool of 4
+and the 1.3B-shaped pool of 64 (each with a short timed region of its own).
 """
 import argparse
 import ctypes
@@ -77,12 +82,12 @@ def site_rooflines(wl, traces, breakdown):
     return out
 
 
-def recorded_traffic():
-    """HBM bytes per launch of the dominant kernel from the committed counter summary, or None if
-    the kernel source has changed since the counters were taken."""
+def recorded_traffic(profile="linear_residual_traffic.md"):
+    """HBM bytes per launch of a kernel from its committed counter summary under profiles/, or None if
+    the kernel source has changed since the counters were taken (or there is no summary)."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "linear_mlp_up_traffic.md")
+    path = os.path.join(ROOT, "profiles", profile)
     src = os.path.join(ROOT, "paper_2607_04461_amd", "csrc", "gemm.hip")
     try:
         txt = open(path).read()
@@ -94,35 +99,111 @@ def recorded_traffic():
     return val if rec == sha else None
 
 
-def cpu_baseline(wl, W, z0, text):
-    """The oracle, as it stands, on candidate 0: step 0 (computed blocks) and step 1 (proxies),
-    extrapolated to the draft's steps."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, W, z0, text, traces):
+    """The oracle, as it stands, on candidate 0 of the pool: its first two steps are timed, and the
+    draft's time per candidate is extrapolated from the pool's own dispatch traces -- each step costs
+    the timed computing step scaled by its number of computed blocks, or the timed proxy-only step.
+    The oracle's BLAS runs with the threads the process may use (``cores``)."""
     from oracle import dit as odit
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
+        host_cpus = len(os.sched_getaffinity(0))
+        limit = min(host_cpus, int(os.environ.get("OMP_NUM_THREADS", host_cpus)))
+        threadpool_limits(limit)
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
-        cores = os.cpu_count()
+        host_cpus = cores = os.cpu_count()
     sched = wl.schedule()
     t0 = time.time()
     kv = odit.prepare_text(W, wl.shape, text)
     cache = odit.PoolCache(wl.shape.num_blocks)
     t1 = time.time()
     z = z0.astype(np.float64)
-    times = []
+    times, ncomp = [], []
     for k in range(2):
         skip, proxy = wl.masks(k)
         ts = time.time()
-        z, _ = odit.draft_step(W, wl.shape, z, sched[k], sched[k + 1], kv, wl.cond_index(), skip, proxy,
-                               cache, candidates=[0])
+        z, tr = odit.draft_step(W, wl.shape, z, sched[k], sched[k + 1], kv, wl.cond_index(), skip, proxy,
+                                cache, candidates=[0])
         times.append(time.time() - ts)
-    n_compute_steps = sum(1 for k in range(wl.steps_draft) if k % 2 == 0)
-    per_cand = n_compute_steps * times[0] + (wl.steps_draft - n_compute_steps) * times[1]
+        ncomp.append(sum(1 for e in tr if e[0] == 0))
+    assert ncomp[0] > 0 and ncomp[1] == 0, "the sample expects a computing step followed by a proxy-only step"
+    per_block = times[0] / ncomp[0]
+    per_cand = 0.0
+    for tr in traces:
+        n = sum(1 for e in tr if e[0] == 0)
+        per_cand += n * per_block if n else times[1]
+    n_compute_steps = sum(1 for tr in traces if any(e[0] == 0 for e in tr))
     return {"value": 1.0 / per_cand, "unit": "candidates/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"candidate 0 of the pool: step 0 (all computed blocks) {times[0]:.1f} s and step 1 "
-                       f"(proxies) {times[1]:.2f} s, extrapolated to the {wl.steps_draft}-step draft "
-                       f"({n_compute_steps} computed + {wl.steps_draft - n_compute_steps} proxy steps); "
-                       f"text preparation {t1 - t0:.1f} s excluded; fp64 numpy")}
+            "host_cpus": int(host_cpus), "cpu_model": cpu_model(),
+            "sample": (f"candidate 0 of the pool: step 0 ({ncomp[0]} computed blocks) {times[0]:.1f} s and "
+                       f"step 1 (proxies only) {times[1]:.2f} s, extrapolated over the draft's traces "
+                       f"({n_compute_steps} computing + {len(traces) - n_compute_steps} proxy-only steps); "
+                       f"text preparation {t1 - t0:.1f} s excluded; fp64 numpy, BLAS on {cores} threads")}
+
+
+def describe_workload(wl, traces) -> str:
+    """The workload in words, from its shape and the dispatch traces the run produced."""
+    s = wl.shape
+    skips = [sum(1 for e in tr if e[0] == 1) for tr in traces]
+    comp = [sum(1 for e in tr if e[0] == 0) for tr in traces]
+    proxy_steps = [k for k, tr in enumerate(traces) if any(e[0] == 2 for e in tr)]
+    skip_txt = (f"{skips[0]} of {s.num_blocks} blocks skipped every step" if len(set(skips)) == 1
+                else f"{min(skips)}..{max(skips)} of {s.num_blocks} blocks skipped per step")
+    prompts = f"{wl.n_cond} prompts" if wl.n_cond > 1 else "1 prompt"
+    return (f"{wl.name}: DiT of {s.num_blocks} blocks, D={s.hidden}, {s.heads} heads x {s.head_dim}, "
+            f"MLP {s.mlp_hidden}; N={wl.n} candidates over {prompts}, {wl.tokens} image tokens "
+            f"({wl.latent_h}x{wl.latent_w} latent, patch {s.patch}), {wl.text_len} text tokens x "
+            f"{s.text_dim}; S'={wl.steps_draft} of {wl.steps_total} steps; {skip_txt}; proxies on steps "
+            f"{proxy_steps}; {sum(comp)} block evaluations per candidate")
+
+
+def secondary_draft(name, steps, warmup=1):
+    """Draft throughput of another workload (its own short timed region): candidates/s, ms per draft,
+    algorithmic TFLOP/s and the fraction of the bf16 peak."""
+    import torch
+    from paper_2607_04461_amd import synth
+    from paper_2607_04461_amd.pool import DraftPool
+    wl = synth.WORKLOADS[name]
+    flat, _ = synth.make_weights(wl.shape, wl.seed_w, threads=16)
+    pool = DraftPool(wl, dtype="bf16", weights=flat)
+    del flat
+    z0 = torch.from_numpy(synth.make_latents(wl.n, wl.shape.latent_channels, wl.latent_h, wl.latent_w)).cuda()
+
+    def one_draft():
+        pool.latents.copy_(z0)
+        ctypes.memset(pool.meta, 0, ctypes.sizeof(pool.meta))
+        return [pool.draft_step(k) for k in range(wl.steps_draft)]
+
+    traces = one_draft()
+    for _ in range(warmup - 1):
+        one_draft()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        one_draft()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    pool.close()
+    flops = draft_flops(wl, traces)
+    tf = flops / (ms / 1e3) / 1e12
+    return {"workload": describe_workload(wl, traces), "value": round(wl.n / (ms / 1e3), 3),
+            "unit": "candidates/s", "ms_per_draft": round(ms, 2), "drafts_timed": steps,
+            "algorithmic_tflop_per_draft": round(flops / 1e12, 2), "tflops": round(tf, 1),
+            "mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4)}
 
 
 def main():
@@ -135,6 +216,7 @@ def main():
     ap.add_argument("--no-breakdown", action="store_true")
     ap.add_argument("--no-refine", action="store_true", help="skip timing the refinement")
     ap.add_argument("--no-sde", action="store_true", help="skip timing the stochastic-update kernel")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the 14B pool and the pool of 64")
     ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB three times (counter calibration)")
     args = ap.parse_args()
@@ -180,8 +262,10 @@ def main():
     torch.cuda.synchronize()
     print(f"# warm-up done", file=sys.stderr, flush=True)
 
-    # timed region: K whole drafts; the dominant kernel is timed in place
-    fb.flashbon_set_timing(pool.model, ["mlp_up"])
+    # timed region: K whole drafts; the dominant kernel (the residual-epilogue GEMM at its three sites)
+    # and the MLP up-projection are timed in place, per launch, on the library's stream
+    res_sites = ["out", "out_cross", "mlp_down"]
+    fb.flashbon_set_timing(pool.model, res_sites + ["mlp_up"])
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
@@ -190,19 +274,28 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
-    up_ms, up_n = fb.flashbon_read_timing(pool.model, "mlp_up")
+    site_t = {site: fb.flashbon_read_timing(pool.model, site) for site in res_sites + ["mlp_up"]}
     fb.flashbon_set_timing(pool.model, [])
     ms_per_step = total_ms / args.steps
     value = wl.n / (ms_per_step / 1e3)
     flops = draft_flops(wl, traces)
     tflops = flops / (ms_per_step / 1e3) / 1e12
-    M = wl.n * wl.tokens
-    up_flops = 2.0 * M * wl.shape.mlp_hidden * wl.shape.hidden
+    M, D, F = wl.n * wl.tokens, wl.shape.hidden, wl.shape.mlp_hidden
+    site_flops = {"out": 2.0 * M * D * D, "out_cross": 2.0 * M * D * D, "mlp_down": 2.0 * M * D * F,
+                  "mlp_up": 2.0 * M * F * D}
+    res_ms = sum(site_t[x][0] for x in res_sites)
+    res_n = sum(site_t[x][1] for x in res_sites)
+    res_flops = sum(site_flops[x] * site_t[x][1] for x in res_sites)
+    res_avg_ms = res_ms / max(res_n, 1)
+    res_tflops = res_flops / (res_ms / 1e3) / 1e12
+    res_plans = {x: fb.flashbon_op_linear_plan(fb.BF16, M, D, K, fb.EPI_RESIDUAL)
+                 for x, K in (("out", D), ("mlp_down", F))}
+    up_ms, up_n = site_t["mlp_up"]
     up_avg_ms = up_ms / max(up_n, 1)
-    up_tflops = up_flops / (up_avg_ms / 1e3) / 1e12
-    up_plan = fb.flashbon_op_linear_plan(fb.BF16, M, wl.shape.mlp_hidden, wl.shape.hidden, fb.EPI_GELU)
-    print(f"# {args.steps} drafts in {total_ms:.1f} ms; mlp_up {up_n} calls avg {up_avg_ms:.3f} ms",
-          file=sys.stderr, flush=True)
+    up_tflops = site_flops["mlp_up"] / (up_avg_ms / 1e3) / 1e12
+    up_plan = fb.flashbon_op_linear_plan(fb.BF16, M, F, D, fb.EPI_GELU)
+    print(f"# {args.steps} drafts in {total_ms:.1f} ms; residual GEMM {res_n} calls avg {res_avg_ms:.3f} ms; "
+          f"mlp_up {up_n} calls avg {up_avg_ms:.3f} ms", file=sys.stderr, flush=True)
 
     breakdown = None
     if not args.no_breakdown:
@@ -227,11 +320,26 @@ def main():
         sel_ms = (time.time() - s0) * 1e3
         selection = {"winner": sel, "pairwise_calls": pool.last_selection[2],
                      "host_ms_incl_verifier": round(sel_ms, 3)}
+        pool.refine(sel)                           # warm-up of the N = 1 shapes
         torch.cuda.synchronize()
         r0 = time.time()
         pool.refine(sel)
         torch.cuda.synchronize()
         refine_ms = round((time.time() - r0) * 1e3, 2)
+
+    # C2: one full-quality step of one candidate at the pool's shape (every block computed), from the
+    # refinement's steps, host launch overhead included
+    c2 = None
+    if refine_ms is not None:
+        steps_r = wl.steps_total - wl.steps_draft
+        c2_ms = refine_ms / steps_r
+        c2_flops = block_flops(wl.shape, wl.tokens, wl.text_len) * wl.shape.num_blocks + \
+            4.0 * wl.tokens * wl.shape.patch_dim * wl.shape.hidden
+        c2_tf = c2_flops / (c2_ms / 1e3) / 1e12
+        c2 = {"workload": f"one candidate of {wl.name}, all {wl.shape.num_blocks} blocks computed (N=1, "
+                          f"{wl.tokens} tokens)", "ms_per_step": round(c2_ms, 3),
+              "algorithmic_tflop_per_step": round(c2_flops / 1e12, 3), "tflops": round(c2_tf, 1),
+              "mfma_frac": round(c2_tf / PEAK_BF16_TFLOPS, 4), "steps_timed": steps_r}
 
     # the stochastic update (App. A.1, Eq. 20) at the pool's latent shape: one fused unpatchify +
     # update launch; HBM-bound, algorithmic bytes = read z, read v, write z (12 bytes per element)
@@ -252,7 +360,7 @@ def main():
         torch.cuda.synchronize()
         sde_us = e0.elapsed_time(e1) / 200 * 1e3
         sde_bytes = 12.0 * z_sde.numel()
-        sde = {"kernel": "k_unpatch_sde (Philox4x32-10 + Box-Muller normals, unpatchify, Eq. 20 update)",
+        sde = {"kernel": "k_head_update (Philox4x32-10 + Box-Muller normals, unpatchify, Eq. 20 update)",
                "elements": z_sde.numel(), "avg_launch_us": round(sde_us, 2), "bound": "hbm",
                "achieved_GBs": round(sde_bytes / sde_us / 1e3, 1), "peak_GBs": PEAK_HBM_GBS,
                "frac": round(sde_bytes / sde_us / 1e3 / PEAK_HBM_GBS, 4)}
@@ -268,7 +376,8 @@ def main():
         del src, dst
 
     result = {
-        "metric": "draft candidates/sec (1.3B-shaped DiT, N=16) + % bf16 MFMA peak",
+        "metric": ("draft candidates/sec (1.3B-shaped DiT, N=16) + % bf16 MFMA peak" if wl.name == "wan1.3b_pool16"
+                   else f"draft candidates/sec ({wl.name}) + % bf16 MFMA peak"),
         "value": round(value, 3),
         "unit": "candidates/s",
         "n_gpus": 1,
@@ -281,21 +390,33 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) latents and text, N(0,0.02^2) random-init weights)",
         "config": {
-            "workload": (f"{wl.name}: 1.3B-shaped DiT ({wl.shape.num_blocks} blocks, D={wl.shape.hidden}, "
-                         f"{wl.shape.heads} heads x {wl.shape.head_dim}, MLP {wl.shape.mlp_hidden}), "
-                         f"N={wl.n} candidates, {wl.tokens} image tokens, {wl.text_len} text tokens, "
-                         f"S'={wl.steps_draft} of {wl.steps_total} steps, every 3rd block skipped, "
-                         f"proxies on odd steps"),
+            "workload": describe_workload(wl, traces),
             "global_batch": wl.n, "seq_len": wl.tokens, "parallelism": "none (1 GPU)",
         },
         "tflops_end_to_end": round(tflops, 2),
         "mfma_frac_end_to_end": round(tflops / PEAK_BF16_TFLOPS, 4),
         "algorithmic_tflop_per_step": round(flops / 1e12, 3),
         "roofline": {
+            "kernel": ("residual-epilogue GEMM k_linear_dma8<EPI_RESIDUAL> (gate, residual, cache store) at "
+                       "its three sites per computed block: self-attention and cross-attention output "
+                       "projections (M=%d N=%d K=%d: %s) and MLP down-projection (K=%d: %s); FLOPs and time "
+                       "summed over every launch of those sites, timed per call"
+                       % (M, D, D, res_plans["out"][1], F, res_plans["mlp_down"][1])),
+            "bound": "mfma", "achieved": round(res_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(res_tflops / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic("linear_residual_traffic.md"),
+            "traffic_unit": "bytes per launch, averaged over the three sites' launches (FETCH_SIZE + "
+                            "WRITE_SIZE, copy-calibrated)",
+            "avg_launch_ms": round(res_avg_ms, 4), "launches": res_n,
+            "algorithmic_gflop_per_launch": round(res_flops / max(res_n, 1) / 1e9, 2),
+            "sites": {x: {"launches": site_t[x][1], "avg_ms": round(site_t[x][0] / max(site_t[x][1], 1), 4),
+                          "tflops": round(site_flops[x] * site_t[x][1] / (site_t[x][0] / 1e3) / 1e12, 1)}
+                      for x in res_sites},
+        },
+        "roofline_secondary": {
             "kernel": ("MLP up-projection + GELU (M=%d N=%d K=%d): %s, EPI_GELU; timed per call"
-                       % (M, wl.shape.mlp_hidden, wl.shape.hidden, up_plan[1])),
+                       % (M, F, D, up_plan[1])),
             "bound": "mfma", "achieved": round(up_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
+            "frac": round(up_tflops / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic("linear_mlp_up_traffic.md"),
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_ms": round(up_avg_ms, 4), "launches": up_n, "kernels_per_launch": up_plan[0],
         },
@@ -304,13 +425,21 @@ def main():
         "sde_update": sde,
         "refine_ms": refine_ms,
         "refine_steps": wl.steps_total - wl.steps_draft,
+        "c2_full_step": c2,
         "site_breakdown_one_draft": breakdown,
         "site_rooflines_one_draft": site_rooflines(wl, traces, breakdown) if breakdown else None,
     }
     pool.close()
+    del pool
+    if not args.no_secondary:
+        result["secondary_workloads"] = {}
+        for name, k in (("wan1.3b_pool64", 3), ("wan14b_pool4", 3)):
+            print(f"# secondary workload {name}", file=sys.stderr, flush=True)
+            result["secondary_workloads"][name] = secondary_draft(name, k)
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle sample", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(wl, W, z0, text)
+        result["cpu_baseline"] = cpu_baseline(wl, W, z0, text, traces)
     print(json.dumps(result), flush=True)
 
 
