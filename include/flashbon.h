@@ -220,8 +220,9 @@ flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args
  * buffers (residual stream, activations, timestep path, text projection when *text_kv_valid is 0,
  * prompt indices, rotary table) come from a static device array of FLASHBON_NOALLOC_SCRATCH_BYTES that
  * the library holds on every GPU it runs on until the process ends; nothing in it has to start at
- * zero.  FLASHBON_ESHAPE, before any device work, if a call needs more (about 70 MB for one candidate
- * of the 1.3B-shaped model at 1560 tokens in bf16 mode, 118 MB in fp32 mode) or more than 128 token-row
+ * zero.  FLASHBON_ESHAPE, before any device work, if a call needs more (about 121 MB for one candidate
+ * of the 1.3B-shaped model at 1560 tokens in bf16 mode, 48 MiB of it the split-K partial sums of the
+ * linear layers; 118 MB in fp32 mode) or more than 128 token-row
  * blocks; FLASHBON_EINVAL if the current device is not the model's.  Every call on a GPU shares that
  * GPU's array: calls of this entry point that overlap on one GPU (other streams, other threads, other
  * models) race.  No timing sites are recorded. */

@@ -42,6 +42,19 @@ flashbon_status flashbon_op_linear_residual(int32_t dtype, int32_t M, int32_t N,
                                             const void *W, const float *bias, const float *gate,
                                             const float *residual_in, float *out, void *stream);
 
+/* flashbon_op_linear with a caller-owned workspace (device, workspace_bytes) for split-K partial sums,
+ * as the draft and refinement steps run their linear layers: a bf16 shape whose 224 x 256 tiles would
+ * fill less than half the CUs (one candidate's MLP down-projection, M = 1560, N = 1536, K = 8960) is cut
+ * into K ranges of at least 16 x 64 columns, each range's fp32 partial sums stored in the workspace
+ * (splits x M x N x 4 bytes, at most 48 MiB), then added in range order before the epilogue; other
+ * shapes, and a workspace too small for the plan, run exactly as flashbon_op_linear.  *splits (optional)
+ * receives the number of K ranges used (1 = none).  Arguments otherwise as flashbon_op_linear; the
+ * workspace must not overlap any other buffer. */
+flashbon_status flashbon_op_linear_ws(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
+                                      const void *W, const float *bias, int32_t epilogue, void *out,
+                                      const float *gate, float *cache_out, void *workspace,
+                                      size_t workspace_bytes, int32_t *splits, void *stream);
+
 /* The tile plan flashbon_op_linear (and every projection of the draft step) takes for this shape,
  * without launching anything or touching the GPU: *kernels = the number of kernel launches, desc =
  * a NUL-terminated one-line description of the kernels and tiles (truncated to desc_len - 1

@@ -671,7 +671,9 @@ __device__ __forceinline__ void dma_tile(int M, int N, int K, const bf16 *__rest
 // interleaving of fragment reads and loads with the MFMA groups as dma_tile.
 template <int EPI, typename TO, int WTA>
 __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__restrict__ A, const bf16 *__restrict__ Wt,
-                                          const EpiArgs &e, int m0, int n0, bf16 *smem) {
+                                          const EpiArgs &e, int m0, int n0, bf16 *smem, int ldk) {
+  // K: columns accumulated (K % 64 == 0, K >= 128); ldk: row stride of A and Wt in elements (ldk >= K;
+  // larger for one K range of a split-K launch, whose A and Wt point at the range's first column)
   using namespace mf;
   static_assert(WTA >= 5 && WTA <= 8, "tile height 160..256");
   constexpr int BM = 32 * WTA, BN = 256, WT = 4;
@@ -683,8 +685,8 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const bool loads_a = wave < 4;
-  const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * K, min(M - m0, BM), K);
-  const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * K, min(N - n0, BN), K);
+  const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * ldk, min(M - m0, BM), ldk);
+  const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * ldk, min(N - n0, BN), ldk);
   // load x of this wave: rows 8 WTA wave + 8 x .. + 7 of A (waves 0-3, x < WTA) or 64 (wave - 4) +
   // 8 x .. + 7 of W (waves 4-7); lane l -> row + (l >> 3), slot l & 7
   uint32_t voff[NL];
@@ -692,7 +694,7 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
 #pragma unroll
   for (int x = 0; x < NL; ++x) {
     const int r = row0 + 8 * x + (lane >> 3);
-    voff[x] = (uint32_t)((r * K + (((lane & 7) ^ swz(r)) << 3)) * 2);
+    voff[x] = (uint32_t)((r * ldk + (((lane & 7) ^ swz(r)) << 3)) * 2);
   }
   const uint32_t lds_row0 = (uint32_t)((loads_a ? 0 : BM * BK) + row0 * BK) * 2u;
   auto dma_one = [&](int kt, int st, int x) {
@@ -788,11 +790,55 @@ __global__ __launch_bounds__(512, 1) void k_linear_dma8(int M, int N, int K, con
   if (m0 >= M) return;   // a block past the last row (a forced plan with more blocks than M needs)
   if constexpr (WTA > 5) {
     if (upto == before) {
-      dma8_tile<EPI, TO, WTA - 1>(M, N, K, A, Wt, e, m0, n0, smem);
+      dma8_tile<EPI, TO, WTA - 1>(M, N, K, A, Wt, e, m0, n0, smem, K);
       return;
     }
   }
-  dma8_tile<EPI, TO, WTA>(M, N, K, A, Wt, e, m0, n0, smem);
+  dma8_tile<EPI, TO, WTA>(M, N, K, A, Wt, e, m0, n0, smem, K);
+}
+
+// Split-K: MT x NT tiles of 224 x 256 on the 8-wave tile, each tile's K range cut into `splits` ranges of
+// ks columns (the last one shorter); workgroup (tile, split) accumulates its range and stores the fp32
+// partial sums into part + split M N ([M][N] per split, no bias).  k_splitk_reduce then adds the splits
+// in order and applies the epilogue.  For launches whose tiles alone would leave most CUs idle (one
+// candidate's MLP down-projection: 42 tiles, K = 8960).
+__global__ __launch_bounds__(512, 1) void k_linear_dma8_splitk(int M, int N, int K, const bf16 *__restrict__ A,
+                                                        const bf16 *__restrict__ Wt, float *__restrict__ part,
+                                                        int MT, int NT, int ks, int group_m) {
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  const int tiles = MT * NT;
+  const int split = blockIdx.x / tiles;
+  int mt, nt;
+  mf::tile_of(blockIdx.x - split * tiles, MT, NT, mt, nt, group_m);
+  const int m0 = 224 * mt, n0 = nt * 256, k0 = split * ks;
+  if (m0 >= M || k0 >= K) return;
+  EpiArgs e;
+  e.out = part + (int64_t)split * M * N;
+  e.ldo = N;
+  dma8_tile<EPI_STORE_F32, float, 7>(M, N, min(ks, K - k0), A + k0, Wt + k0, e, m0, n0, smem, K);
+}
+
+// out = epilogue(sum over s of part[s] + bias), the splits added in order s = 0, 1, ..; one thread per 8
+// consecutive columns of a row (N % 8 == 0).
+template <int EPI>
+__global__ __launch_bounds__(256) void k_splitk_reduce(int M, int N, int splits, const float *__restrict__ part,
+                                                       EpiArgs e) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int n8 = N / 8;
+  if (i >= (int64_t)M * n8) return;
+  const int m = (int)(i / n8), n = (int)(i % n8) * 8;
+  const int64_t plane = (int64_t)M * N, at = (int64_t)m * N + n;
+  float v[8];
+  {
+    const float4 a = *reinterpret_cast<const float4 *>(part + at), b = *reinterpret_cast<const float4 *>(part + at + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+  for (int sp = 1; sp < splits; ++sp) {
+    const float *p = part + sp * plane + at;
+    const float4 a = *reinterpret_cast<const float4 *>(p), b = *reinterpret_cast<const float4 *>(p + 4);
+    v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w; v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+  }
+  epilogue8<EPI, bf16>(e, m, n, v);
 }
 
 // MT row blocks x NT column tiles of 256.  Row blocks come in two heights: `tall` of them 32 WTA rows
@@ -1164,6 +1210,58 @@ int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len)
     buf[n] = 0;
   }
   return kernels;
+}
+
+// Splits of the split-K plan for this shape (1 = none): only bf16 shapes the 8-wave kernel takes, whose
+// 224 x 256 tiles fill less than half the CUs, with at least 16 K tiles per split and the partial sums
+// within kSplitBytes.  A function of the shape alone, so every caller with a workspace gets the same
+// plan (and the same bits).
+int splitk_splits(int epi, int M, int N, int K) {
+  if (epi == EPI_EULER || K % mf::BK || N % 8 || K < 2 * mf::BK) return 1;
+  const int64_t tiles = (int64_t)((M + 223) / 224) * ((N + 255) / 256);
+  const int cus = cu_count();
+  if (2 * tiles > cus) return 1;
+  int sp = (int)std::min<int64_t>(cus / tiles, K / (16 * mf::BK));
+  sp = (int)std::min<int64_t>(sp, (int64_t)(kSplitBytes / ((size_t)M * N * 4)));
+  // the launch gives each split ceil(kt / sp) K tiles: take the largest count for which every split is
+  // non-empty and the last has at least the two K tiles the tile loop needs
+  const int kt = K / mf::BK;
+  for (; sp >= 2; --sp) {
+    const int ks = (kt + sp - 1) / sp;
+    if ((kt + ks - 1) / ks == sp && kt - (sp - 1) * ks >= 2) return sp;
+  }
+  return 1;
+}
+
+hipError_t launch_linear_ws(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
+                            hipStream_t s, void *ws, size_t ws_bytes) {
+  const int sp = t == ACT_BF16 && ws ? splitk_splits(epi, M, N, K) : 1;
+  if (sp < 2 || (size_t)sp * M * N * 4 > ws_bytes) return launch_linear(t, epi, M, N, K, A, Wt, e, s);
+  const int ks = (K / mf::BK + sp - 1) / sp * mf::BK;
+  const size_t lds = (size_t)2 * (224 + 256) * mf::BK * sizeof(bf16);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void *)k_linear_dma8_splitk, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int MT = (M + 223) / 224, NT = (N + 255) / 256;
+  float *part = (float *)ws;
+  hipLaunchKernelGGL(k_linear_dma8_splitk, dim3(MT * NT * sp), dim3(512), lds, s, M, N, K, (const bf16 *)A,
+                     (const bf16 *)Wt, part, MT, NT, ks, group_rows(MT, NT, K));
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int64_t threads = (int64_t)M * (N / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL(k_splitk_reduce<EPI_STORE>, grid, dim3(256), 0, s, M, N, sp, part, e); break;
+    case EPI_GELU: hipLaunchKernelGGL(k_splitk_reduce<EPI_GELU>, grid, dim3(256), 0, s, M, N, sp, part, e); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL(k_splitk_reduce<EPI_STORE_F32>, grid, dim3(256), 0, s, M, N, sp, part, e); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL(k_splitk_reduce<EPI_RESIDUAL>, grid, dim3(256), 0, s, M, N, sp, part, e); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_linear(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt,

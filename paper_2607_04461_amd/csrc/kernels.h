@@ -37,6 +37,13 @@ struct EpiArgs {
 // C[m][n] = sum_k A[m][k] * Wt[n][k] (+ epilogue).  K % 8 == 0.
 hipError_t launch_linear(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt,
                          const EpiArgs &e, hipStream_t s);
+// As launch_linear, given a workspace of ws_bytes for split-K partial sums: shapes whose tiles would
+// leave most CUs idle (splitk_splits > 1) then run as a split-K launch plus an in-order reduction that
+// applies the epilogue (needs splits x M x N x 4 bytes, at most kSplitBytes); else as launch_linear.
+constexpr size_t kSplitBytes = (size_t)48 << 20;
+int splitk_splits(int epi, int M, int N, int K);
+hipError_t launch_linear_ws(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
+                            hipStream_t s, void *ws, size_t ws_bytes);
 // The kernels launch_linear would use for this shape, without launching: returns the number of
 // launches and writes a NUL-terminated description (truncated to len - 1 characters) into buf.
 int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len);

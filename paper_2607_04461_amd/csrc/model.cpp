@@ -115,12 +115,15 @@ size_t scratch_layout(const Model *m, int rows, int tokens, int text_rows, char 
        *txt = carve(m->act == ACT_BF16 ? (size_t)text_rows * m->Dt * a : 0), *ctx = carve((size_t)text_rows * D * a),
        *tf = carve(m->fd * 4), *e1 = carve(D * 4), *e = carve(D * 4), *m6 = carve(6 * D * 4),
        *bm = carve((size_t)m->L * 6 * D * 4), *hm = carve(2 * D * 4), *cond = carve((size_t)rows * 4),
-       *rope = carve(m->c.qk_norm_rope ? (size_t)tokens * (m->dh / 2) * 8 : 0);
+       *rope = carve(m->c.qk_norm_rope ? (size_t)tokens * (m->dh / 2) * 8 : 0),
+       *part = carve(m->act == ACT_BF16 ? kSplitBytes : 0);
   if (B) {
     B->h = (float *)h; B->a = act; B->qkv = qkv; B->o = o; B->u = u; B->tok = tok; B->vtok = (float *)vtok;
     B->txt = txt; B->ctx = ctx; B->tf = (float *)tf; B->e1 = (float *)e1; B->e = (float *)e; B->m6 = (float *)m6;
     B->bmods = (float *)bm; B->hmod = (float *)hm; B->d_cond = (int32_t *)cond;
     B->rope = m->c.qk_norm_rope ? (float2 *)rope : nullptr;
+    B->part = m->act == ACT_BF16 ? part : nullptr;
+    B->part_bytes = m->act == ACT_BF16 ? kSplitBytes : 0;
   }
   return off;
 }
@@ -205,7 +208,8 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
          o_tf = carve(m->fd * 4), o_e1 = carve(D * 4), o_e = carve(D * 4), o_m6 = carve(6 * D * 4),
          o_bm = carve((size_t)m->L * 6 * D * 4), o_hm = carve(2 * D * 4), o_cond = carve(cfg->max_n * 4),
          o_v = carve(M * P * 4),
-         o_rope = carve(cfg->qk_norm_rope ? (size_t)cfg->max_tokens * (D / cfg->heads / 2) * 8 : 0);
+         o_rope = carve(cfg->qk_norm_rope ? (size_t)cfg->max_tokens * (D / cfg->heads / 2) * 8 : 0),
+         o_part = carve(m->act == ACT_BF16 ? kSplitBytes : 0);
   if (hipMalloc(&m->ws, off) != hipSuccess) return cleanup(FLASHBON_ENOMEM, "workspace of " + std::to_string(off) + " bytes");
   m->ws_bytes = off;
   char *w = (char *)m->ws;
@@ -216,6 +220,7 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
   B.m6 = (float *)(w + o_m6); B.bmods = (float *)(w + o_bm); B.hmod = (float *)(w + o_hm);
   B.d_cond = (int32_t *)(w + o_cond); B.vtok = (float *)(w + o_v);
   if (cfg->qk_norm_rope) B.rope = (float2 *)(w + o_rope);
+  if (m->act == ACT_BF16) { B.part = w + o_part; B.part_bytes = kSplitBytes; }
   // the allocation-free step's scratch array of this device: its address, once per device
   {
     char *base = nullptr;
@@ -392,6 +397,10 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     scratch_layout(m, R, T, *a->text_kv_valid ? 0 : a->n_cond * a->text_len, base, &B);
   }
 
+  // linear layers: split-K (with its partial sums in this step's buffers) where the plan asks for it
+  auto lin = [&](ActType t_, int epi_, int M_, int N_, int K_, const void *A_, const void *W_, const EpiArgs &e_,
+                 hipStream_t s_) { return launch_linear_ws(t_, epi_, M_, N_, K_, A_, W_, e_, s_, B.part, B.part_bytes); };
+
   // ---------------------------------------------------------------- enqueue
   hipStream_t s = (hipStream_t)a->stream;
   const ActType act = m->act;
@@ -423,11 +432,11 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     EpiArgs e;
     e.out = B.ctx; e.ldo = D; e.bias = Bp(m->lay.txt_b);
-    HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s); }), "text projection");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return lin(act, EPI_STORE, NC * Lt, D, m->Dt, txt, Wp(m->lay.txt_w), e, s); }), "text projection");
     for (int l = 0; l < L; ++l) {
       EpiArgs k;
       k.out = (char *)a->text_kv + (size_t)l * kv_block * asz; k.ldo = 2 * D; k.bias = Bp(m->lay.blk[l].bkvc);
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_linear(act, EPI_STORE, NC * Lt, 2 * D, D, B.ctx, Wp(m->lay.blk[l].wkvc), k, s); }), "text K/V");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return lin(act, EPI_STORE, NC * Lt, 2 * D, D, B.ctx, Wp(m->lay.blk[l].wkvc), k, s); }), "text K/V");
       if (c.qk_norm_rope)
         HIPCHK(timed(m, tmask, FLASHBON_SITE_TEXT, s, [&] { return launch_qk_norm(act, NC * Lt, D, m->dh, k.out, 2 * D, Bp(m->lay.blk[l].nkc), c.ln_eps, nullptr, 1, s); }),
                "text key RMSNorm");
@@ -479,7 +488,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     HIPCHK(timed(m, tmask, FLASHBON_SITE_EMBED, s, [&] { return launch_patchify(act, R, a->n, m->C, a->latent_h, a->latent_w, p, a->latents, B.tok, s); }), "patchify");
     EpiArgs e;
     e.out = B.h; e.ldo = D; e.bias = Bp(m->lay.pe_b);
-    HIPCHK(timed(m, tmask, FLASHBON_SITE_EMBED, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, D, P, B.tok, Wp(m->lay.pe_w), e, s); }), "patch embed");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_EMBED, s, [&] { return lin(act, EPI_STORE_F32, (int)M, D, P, B.tok, Wp(m->lay.pe_w), e, s); }), "patch embed");
     if ((st = dump(0)) != FLASHBON_OK) return st;
   }
 
@@ -515,7 +524,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, hcur, mod + 0 * D, mod + 1 * D, B.a, s); }), "adaLN 1");
     {
       EpiArgs e; e.out = B.qkv; e.ldo = 3 * D; e.bias = Bp(b.bqkv);
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_QKV, s, [&] { return launch_linear(act, EPI_STORE, (int)M, 3 * D, D, B.a, Wp(b.wqkv), e, s); }), "qkv projection");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_QKV, s, [&] { return lin(act, EPI_STORE, (int)M, 3 * D, D, B.a, Wp(b.wqkv), e, s); }), "qkv projection");
     }
     if (c.qk_norm_rope) {
       void *kp = (char *)B.qkv + (size_t)D * asz;
@@ -534,13 +543,13 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     {
       EpiArgs e; e.out = B.h; e.ldo = D; e.bias = Bp(b.bo); e.gate = mod + 2 * D;
       if (hcur != B.h) e.res_in = hcur;
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_OUT, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, B.o, Wp(b.wo), e, s); }), "self-attn out projection");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_OUT, s, [&] { return lin(act, EPI_RESIDUAL, (int)M, D, D, B.o, Wp(b.wo), e, s); }), "self-attn out projection");
       hcur = B.h;
     }
     HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, B.h, nullptr, nullptr, B.a, s); }), "cross LN");
     {
       EpiArgs e; e.out = B.qkv; e.ldo = D; e.bias = Bp(b.bqc);
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_CROSS_Q, s, [&] { return launch_linear(act, EPI_STORE, (int)M, D, D, B.a, Wp(b.wqc), e, s); }), "cross q projection");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_CROSS_Q, s, [&] { return lin(act, EPI_STORE, (int)M, D, D, B.a, Wp(b.wqc), e, s); }), "cross q projection");
     }
     if (c.qk_norm_rope)
       HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_qk_norm(act, (int)M, D, dh, B.qkv, D, Bp(b.nqc), c.ln_eps, nullptr, T, s); }), "cross q RMSNorm");
@@ -556,12 +565,12 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     {
       EpiArgs e; e.out = B.h; e.ldo = D; e.bias = Bp(b.boc);
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_OUT_CROSS, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, D, B.o, Wp(b.woc), e, s); }), "cross out projection");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_OUT_CROSS, s, [&] { return lin(act, EPI_RESIDUAL, (int)M, D, D, B.o, Wp(b.woc), e, s); }), "cross out projection");
     }
     HIPCHK(timed(m, tmask, FLASHBON_SITE_NORM, s, [&] { return launch_ln_mod(act, (int)M, D, c.ln_eps, B.h, mod + 3 * D, mod + 4 * D, B.a, s); }), "adaLN 2");
     {
       EpiArgs e; e.out = B.u; e.ldo = F; e.bias = Bp(b.b1);
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_MLP_UP, s, [&] { return launch_linear(act, EPI_GELU, (int)M, F, D, B.a, Wp(b.w1), e, s); }), "mlp up");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_MLP_UP, s, [&] { return lin(act, EPI_GELU, (int)M, F, D, B.a, Wp(b.w1), e, s); }), "mlp up");
     }
     {
       EpiArgs e; e.out = B.h; e.ldo = D; e.bias = Bp(b.b2); e.gate = mod + 5 * D;
@@ -573,7 +582,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
         e.cache = slot;
         e.cache_delta = residual;
       }
-      HIPCHK(timed(m, tmask, FLASHBON_SITE_MLP_DOWN, s, [&] { return launch_linear(act, EPI_RESIDUAL, (int)M, D, F, B.u, Wp(b.w2), e, s); }), "mlp down");
+      HIPCHK(timed(m, tmask, FLASHBON_SITE_MLP_DOWN, s, [&] { return lin(act, EPI_RESIDUAL, (int)M, D, F, B.u, Wp(b.w2), e, s); }), "mlp down");
       hcur = (const float *)e.out;
     }
     if ((st = dump(l + 1)) != FLASHBON_OK) return st;
@@ -588,7 +597,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     }
     EpiArgs e;
     e.out = B.vtok; e.ldo = P; e.bias = Bp(m->lay.head_b);
-    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_STORE_F32, (int)M, P, D, B.a, Wp(m->lay.head_w), e, s); }), "head");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return lin(act, EPI_STORE_F32, (int)M, P, D, B.a, Wp(m->lay.head_w), e, s); }), "head");
     HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return launch_head_update(a->n, m->C, a->latent_h, a->latent_w, p, B.vtok, guided, a->cfg_scale, a->latents, sde, a->preview, a->t_cur, s); }),
            "unpatchify + guidance + update");
   } else {
@@ -596,7 +605,7 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
     e.bias = Bp(m->lay.head_b); e.z = a->latents; e.dt = a->t_next - a->t_cur;
     e.preview = a->preview; e.t_cur = a->t_cur;
     e.C = m->C; e.H = a->latent_h; e.W = a->latent_w; e.p = p; e.T = T;
-    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return launch_linear(act, EPI_EULER, (int)M, P, D, B.a, Wp(m->lay.head_w), e, s); }), "head + Euler");
+    HIPCHK(timed(m, tmask, FLASHBON_SITE_HEAD, s, [&] { return lin(act, EPI_EULER, (int)M, P, D, B.a, Wp(m->lay.head_w), e, s); }), "head + Euler");
   }
 
   // ---------------------------------------------------------------- commit host state

@@ -33,6 +33,8 @@ struct StepBufs {
   float2 *rope = nullptr;      // (cos, sin) per token and pair [T][head_dim/2] (qk_norm_rope)
   float *tf = nullptr, *e1 = nullptr, *e = nullptr, *m6 = nullptr, *bmods = nullptr, *hmod = nullptr;
   int32_t *d_cond = nullptr;   // prompt of each token-row block
+  void *part = nullptr;        // split-K partial sums of the linear layers (bf16 mode), kSplitBytes
+  size_t part_bytes = 0;
 };
 
 struct Model {

@@ -34,6 +34,26 @@ flashbon_status flashbon_op_linear(int32_t dtype, int32_t M, int32_t N, int32_t 
   return launched(launch_linear(t, epilogue, M, N, K, A, W, e, (hipStream_t)stream), "linear");
 }
 
+flashbon_status flashbon_op_linear_ws(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
+                                      const void *W, const float *bias, int32_t epilogue, void *out,
+                                      const float *gate, float *cache_out, void *workspace,
+                                      size_t workspace_bytes, int32_t *splits, void *stream) {
+  if (dtype != FLASHBON_FP32 && dtype != FLASHBON_BF16) return fail(FLASHBON_EINVAL, "bad dtype");
+  if (M < 1 || N < 1 || K < 1 || K % 8 || N % 4 || K > 65536)
+    return fail(FLASHBON_ESHAPE, "need M,N,K >= 1, K <= 65536, K % 8 == 0, N % 4 == 0");
+  if (!A || !W || !out) return fail(FLASHBON_EINVAL, "A, W and out are required");
+  if (epilogue < FLASHBON_EPI_STORE || epilogue > FLASHBON_EPI_RESIDUAL) return fail(FLASHBON_EINVAL, "bad epilogue");
+  EpiArgs e;
+  e.out = out; e.ldo = N; e.bias = bias;
+  if (epilogue == FLASHBON_EPI_RESIDUAL) { e.gate = gate; e.cache = cache_out; }
+  ActType t = dtype == FLASHBON_BF16 ? ACT_BF16 : ACT_F32;
+  int sp = t == ACT_BF16 && workspace ? splitk_splits(epilogue, M, N, K) : 1;
+  if (sp > 1 && (size_t)sp * M * N * 4 > workspace_bytes) sp = 1;
+  if (splits) *splits = sp;
+  return launched(launch_linear_ws(t, epilogue, M, N, K, A, W, e, (hipStream_t)stream, workspace, workspace_bytes),
+                  "linear");
+}
+
 flashbon_status flashbon_op_linear_residual(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
                                             const void *W, const float *bias, const float *gate,
                                             const float *residual_in, float *out, void *stream) {

@@ -70,7 +70,7 @@ EXPORTS = [
     "flashbon_draft_step", "flashbon_refine_step", "flashbon_free", "flashbon_plan_step",
     "flashbon_last_error", "flashbon_set_timing", "flashbon_read_timing", "flashbon_op_linear", "flashbon_op_linear_residual", "flashbon_op_linear_plan", "flashbon_op_attention", "flashbon_op_ln_mod",
     "flashbon_op_proxy", "flashbon_op_normals", "flashbon_op_unpatch_sde", "flashbon_select",
-    "flashbon_refine_step_noalloc",
+    "flashbon_refine_step_noalloc", "flashbon_op_linear_ws",
 ]
 NOALLOC_SCRATCH_BYTES = 128 << 20
 
@@ -118,6 +118,9 @@ def load() -> ctypes.CDLL:
     L.flashbon_last_error.restype = ctypes.c_char_p
     L.flashbon_op_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
     L.flashbon_op_linear.restype = i32
+    L.flashbon_op_linear_ws.argtypes = [i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz,
+                                        ctypes.POINTER(ctypes.c_int32), vp]
+    L.flashbon_op_linear_ws.restype = i32
     L.flashbon_op_linear_residual.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     L.flashbon_op_linear_residual.restype = i32
     L.flashbon_op_linear_plan.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_char_p, i32]
@@ -452,6 +455,17 @@ def flashbon_read_timing(model: int, site: str):
 def flashbon_op_linear(dtype, M, N, K, A, W, bias, epilogue, out, gate=None, cache_out=None, stream=None):
     _check(load().flashbon_op_linear(dtype, M, N, K, _ptr(A), _ptr(W), _ptr(bias), epilogue, _ptr(out),
                                      _ptr(gate), _ptr(cache_out), _stream(stream)), "flashbon_op_linear")
+
+
+def flashbon_op_linear_ws(dtype, M, N, K, A, W, bias, epilogue, out, workspace, gate=None, cache_out=None,
+                          stream=None) -> int:
+    """flashbon_op_linear with a split-K workspace (a device tensor); returns the number of K ranges."""
+    sp = ctypes.c_int32()
+    nbytes = 0 if workspace is None else int(workspace.numel()) * int(workspace.element_size())
+    _check(load().flashbon_op_linear_ws(dtype, M, N, K, _ptr(A), _ptr(W), _ptr(bias), epilogue, _ptr(out),
+                                        _ptr(gate), _ptr(cache_out), _ptr(workspace), nbytes, ctypes.byref(sp),
+                                        _stream(stream)), "flashbon_op_linear_ws")
+    return sp.value
 
 
 def flashbon_op_linear_residual(dtype, M, N, K, A, W, bias, gate, residual_in, out, stream=None):

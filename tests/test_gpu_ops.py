@@ -409,3 +409,49 @@ def test_linear_tail_rows_split(M, N, K, epi, split):
         assert torch.equal(cache, out)
         expect = h0[idx].cpu().numpy().astype(np.float64) + gate * ref
         assert rel_l2(out[idx].cpu().numpy(), expect) <= 2e-6
+
+
+@pytest.mark.parametrize("M,N,K,epi", [
+    (200, 136, 2048, "store"), (200, 136, 2048, "gelu"), (200, 136, 2048, "store_f32"), (200, 136, 2048, "residual"),
+    (1560, 1536, 8960, "residual"),      # one candidate's MLP down-projection (refinement)
+    (512, 1536, 4096, "store"),          # the text projection of one 512-token prompt
+])
+def test_linear_splitk_with_workspace(M, N, K, epi):
+    """The split-K plan of the linear layers (K ranges of partial sums in a workspace, added in order
+    before the epilogue) against the fp64 reference, at a ragged small shape and at the refinement's
+    shapes; the plan must actually split there, and a workspace too small falls back to one range."""
+    F = fb()
+    A = _operand((M, K), 11, "bf16")
+    W = _operand((N, K), 12, "bf16", 0.02)
+    bias = synth.random_matrix((N,), 13, 0.02)
+    gate = synth.random_matrix((N,), 14)
+    h0 = synth.random_matrix((M, N), 15)
+    dA, dW, db, dg = _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"), _dev(gate, "fp32")
+    ws = torch.empty(48 << 18, device="cuda", dtype=torch.float32)          # 48 MiB
+    code = {"store": F.EPI_STORE, "gelu": F.EPI_GELU, "store_f32": F.EPI_STORE_F32, "residual": F.EPI_RESIDUAL}[epi]
+    rows = np.arange(M) if M <= 256 else np.random.default_rng(16).choice(M, 48, replace=False)
+    ref = odit.linear(A[rows].astype(np.float64), W, bias)
+    if epi == "gelu":
+        ref = odit.gelu_tanh(ref)
+    outs = []
+    for w in (ws, ws[:1024]):
+        if epi in ("store", "gelu"):
+            out = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+            sp = F.flashbon_op_linear_ws(F.BF16, M, N, K, dA, dW, db, code, out, w)
+            tol, expect = 6e-3, ref
+        elif epi == "store_f32":
+            out = torch.empty((M, N), device="cuda", dtype=torch.float32)
+            sp = F.flashbon_op_linear_ws(F.BF16, M, N, K, dA, dW, db, code, out, w)
+            tol, expect = 2e-6, ref
+        else:
+            out = _dev(h0, "fp32")
+            sp = F.flashbon_op_linear_ws(F.BF16, M, N, K, dA, dW, db, code, out, w, gate=dg)
+            tol, expect = 2e-6, h0[rows] + gate * ref
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy()[rows].astype(np.float64)
+        err = rel_l2(got, expect)
+        print(f"linear_ws {M}x{N}x{K} {epi}: {sp} K ranges, rel-L2 {err:.2e}", flush=True)
+        assert err <= tol
+        outs.append((sp, got))
+    assert outs[0][0] > 1, "the plan should split this shape"
+    assert outs[1][0] == 1, "a workspace too small for the plan runs one range"
