@@ -38,6 +38,9 @@
 extern "C" {
 #endif
 
+/* Opaque handle of a model (weights + workspace), created by flashbon_init_model. */
+typedef struct flashbon_model flashbon_model;
+
 typedef enum {
   FLASHBON_OK = 0,
   FLASHBON_EINVAL = -1, /* NULL where a pointer is required, bad enum, non-finite or unordered t */
@@ -196,22 +199,22 @@ size_t flashbon_weight_count(const flashbon_model_config *cfg);
  * (shift1, scale1, gate1, shift2, scale2, gate2); the head uses head_mod_w SiLU(e) + head_mod_b split
  * as (shift, scale).  On success *out owns the model; free it with flashbon_free. */
 flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const float *host_weights,
-                                    size_t n_weights, void **out);
+                                    size_t n_weights, flashbon_model **out);
 
 /* Bytes of the caller-owned cross-attention K/V scratch for n_cond prompts of text_len tokens. */
-size_t flashbon_text_kv_bytes(const void *model, int32_t n_cond, int32_t text_len);
+size_t flashbon_text_kv_bytes(const flashbon_model *model, int32_t n_cond, int32_t text_len);
 
 /* Bytes of the caller-owned activation cache for n candidates of `tokens` tokens. */
-size_t flashbon_cache_bytes(const void *model, int32_t n, int32_t tokens);
+size_t flashbon_cache_bytes(const flashbon_model *model, int32_t n, int32_t tokens);
 
 /* One draft step (Sec. 4.2 Stage 1, Eq. 8) over the pool with the step's skip/proxy masks: plans
  * every block on the host (trace, meta), then enqueues the step.  Skipped blocks and dead proxies
  * launch nothing. */
-flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args);
+flashbon_status flashbon_draft_step(flashbon_model *model, const flashbon_step_args *args);
 
 /* One full-quality step (Sec. 4.2 Stage 3, Eq. 13): as flashbon_draft_step with every mask zero;
  * skip, proxy, cache and meta are ignored (may be NULL).  trace, if given, reports all COMPUTE. */
-flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args);
+flashbon_status flashbon_refine_step(flashbon_model *model, const flashbon_step_args *args);
 
 /* Refinement step that allocates nothing and touches no model workspace -- for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
@@ -227,10 +230,10 @@ flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args
  * GPU's array: calls of this entry point that overlap on one GPU (other streams, other threads, other
  * models) race.  No timing sites are recorded. */
 #define FLASHBON_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
-flashbon_status flashbon_refine_step_noalloc(void *model, const flashbon_step_args *args);
+flashbon_status flashbon_refine_step_noalloc(flashbon_model *model, const flashbon_step_args *args);
 
 /* Release the model.  NULL is a no-op.  Synchronises the device before freeing. */
-void flashbon_free(void *model);
+void flashbon_free(flashbon_model *model);
 
 enum { FLASHBON_PROXY_OUTPUT = 0, FLASHBON_PROXY_RESIDUAL = 1 };
 
@@ -286,11 +289,11 @@ enum {
  * records a HIP event pair on the step's stream around every launch at those sites (a few
  * microseconds of host time per launch; 0 disables).  Accumulated results are read, and reset, by
  * flashbon_read_timing. */
-flashbon_status flashbon_set_timing(void *model, uint32_t site_mask);
+flashbon_status flashbon_set_timing(flashbon_model *model, uint32_t site_mask);
 
 /* Synchronise on the recorded events and return, for one site, the summed device time (ms) and the
  * number of launches timed since the last read; resets that site's record. */
-flashbon_status flashbon_read_timing(void *model, int32_t site, double *total_ms, int64_t *launches);
+flashbon_status flashbon_read_timing(flashbon_model *model, int32_t site, double *total_ms, int64_t *launches);
 
 /* Description of the calling thread's last failure ("" if none).  Valid until the next call. */
 const char *flashbon_last_error(void);

@@ -163,7 +163,7 @@ flashbon_status flashbon_plan_step(int32_t num_blocks, const uint8_t *skip, cons
 }
 
 flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const float *host_weights,
-                                    size_t n_weights, void **out) {
+                                    size_t n_weights, flashbon_model **out) {
   std::string why;
   if (!out) return fail(FLASHBON_EINVAL, "out is NULL");
   *out = nullptr;
@@ -186,7 +186,7 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
   if (hipGetDevice(&m->device) != hipSuccess) { delete m; return fail(FLASHBON_EHIP, "hipGetDevice"); }
 
   auto cleanup = [&](flashbon_status st, const std::string &msg) {
-    flashbon_free(m);
+    flashbon_free(reinterpret_cast<flashbon_model *>(m));
     // a failed allocation is also recorded as the thread's last HIP error, which the next launch check
     // (hipGetLastError after a launch) would report as that launch's failure: clear it
     if (st == FLASHBON_ENOMEM) (void)hipGetLastError();
@@ -235,14 +235,14 @@ flashbon_status flashbon_init_model(const flashbon_model_config *cfg, const floa
       return cleanup(FLASHBON_EHIP, "weight conversion");
   }
   if (hipDeviceSynchronize() != hipSuccess) return cleanup(FLASHBON_EHIP, "init synchronise");
-  *out = m;
+  *out = reinterpret_cast<flashbon_model *>(m);
   g_err.clear();
   return FLASHBON_OK;
 }
 
-void flashbon_free(void *model) {
+void flashbon_free(flashbon_model *model) {
   if (!model) return;
-  Model *m = (Model *)model;
+  Model *m = reinterpret_cast<Model *>(model);
   (void)hipDeviceSynchronize();
   for (auto &site : m->sites)
     for (auto &pr : site.pending) { (void)hipEventDestroy(pr.first); (void)hipEventDestroy(pr.second); }
@@ -253,15 +253,15 @@ void flashbon_free(void *model) {
   delete m;
 }
 
-size_t flashbon_text_kv_bytes(const void *model, int32_t n_cond, int32_t text_len) {
+size_t flashbon_text_kv_bytes(const flashbon_model *model, int32_t n_cond, int32_t text_len) {
   if (!model || n_cond < 1 || text_len < 1) return 0;
-  const Model *m = (const Model *)model;
+  const Model *m = reinterpret_cast<const Model *>(model);
   return (size_t)m->L * n_cond * text_len * 2 * m->D * m->asz;
 }
 
-size_t flashbon_cache_bytes(const void *model, int32_t n, int32_t tokens) {
+size_t flashbon_cache_bytes(const flashbon_model *model, int32_t n, int32_t tokens) {
   if (!model || n < 1 || tokens < 1) return 0;
-  const Model *m = (const Model *)model;
+  const Model *m = reinterpret_cast<const Model *>(model);
   return (size_t)m->L * 3 * n * tokens * m->D * 4;
 }
 
@@ -620,30 +620,30 @@ static flashbon_status run_step(Model *m, const flashbon_step_args *a, bool draf
 
 extern "C" {
 
-flashbon_status flashbon_draft_step(void *model, const flashbon_step_args *args) {
-  return run_step((Model *)model, args, true);
+flashbon_status flashbon_draft_step(flashbon_model *model, const flashbon_step_args *args) {
+  return run_step(reinterpret_cast<Model *>(model), args, true);
 }
 
-flashbon_status flashbon_refine_step(void *model, const flashbon_step_args *args) {
-  return run_step((Model *)model, args, false);
+flashbon_status flashbon_refine_step(flashbon_model *model, const flashbon_step_args *args) {
+  return run_step(reinterpret_cast<Model *>(model), args, false);
 }
 
-flashbon_status flashbon_refine_step_noalloc(void *model, const flashbon_step_args *args) {
-  return run_step((Model *)model, args, false, true);
+flashbon_status flashbon_refine_step_noalloc(flashbon_model *model, const flashbon_step_args *args) {
+  return run_step(reinterpret_cast<Model *>(model), args, false, true);
 }
 
-flashbon_status flashbon_set_timing(void *model, uint32_t site_mask) {
+flashbon_status flashbon_set_timing(flashbon_model *model, uint32_t site_mask) {
   if (!model) return fail(FLASHBON_EINVAL, "model is NULL");
   if (site_mask >> FLASHBON_NUM_SITES) return fail(FLASHBON_EINVAL, "unknown site in mask");
-  ((Model *)model)->timing_mask = site_mask;
+  reinterpret_cast<Model *>(model)->timing_mask = site_mask;
   g_err.clear();
   return FLASHBON_OK;
 }
 
-flashbon_status flashbon_read_timing(void *model, int32_t site, double *total_ms, int64_t *launches) {
+flashbon_status flashbon_read_timing(flashbon_model *model, int32_t site, double *total_ms, int64_t *launches) {
   if (!model || !total_ms || !launches) return fail(FLASHBON_EINVAL, "model, total_ms and launches are required");
   if (site < 0 || site >= FLASHBON_NUM_SITES) return fail(FLASHBON_EINVAL, "unknown site");
-  Model *m = (Model *)model;
+  Model *m = reinterpret_cast<Model *>(model);
   HIPCHK(harvest(m, site), "timing events");
   *total_ms = m->sites[site].total_ms;
   *launches = m->sites[site].launches;

@@ -32,6 +32,29 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(fb.EXPORTS)
 
 
+def test_headers_are_plain_c_and_the_handle_is_typed(tmp_path):
+    """The two headers compile as C99 on their own, and the model handle is the opaque flashbon_model type
+    (a wrong handle type is a compile error, not a silent void* conversion)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use.c"
+    src.write_text('#include "flashbon_ops.h"\n'
+                   "flashbon_status step(flashbon_model *m, const flashbon_step_args *a) {\n"
+                   "  return flashbon_draft_step(m, a);\n}\n")
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), "-c", str(src),
+                        "-o", str(tmp_path / "use.o")], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    bad = tmp_path / "bad.c"
+    bad.write_text('#include "flashbon.h"\nflashbon_status f(const flashbon_model_config *c, const flashbon_step_args *a) {\n'
+                   "  return flashbon_draft_step(c, a);\n}\n")
+    r = subprocess.run([cc, "-std=c99", "-Werror", "-I", os.path.join(ROOT, "include"), "-c", str(bad),
+                        "-o", str(tmp_path / "bad.o")], capture_output=True, text=True)
+    assert r.returncode != 0
+
+
 @pytest.mark.parametrize("name", ["tiny", "mid", "wan1.3b_pool16", "wan14b_pool4", "wan1.3b_pool64"])
 def test_plan_step_matches_oracle_on_workloads(name):
     wl = synth.WORKLOADS[name]
