@@ -46,13 +46,15 @@ def _snapshot(pool, a, meta, trace, valid):
             pool.latents.clone())
 
 
-@pytest.mark.parametrize("kind", ["draft", "refine"])
-@pytest.mark.parametrize("name,status,draft_only", CASES, ids=[c[0] for c in CASES])
-def test_rejected_before_any_side_effect(pool, kind, name, status, draft_only):
+# every case through both entry points, except the draft-only ones (refinement ignores meta and cache)
+PARAMS = [(kind, name, status) for kind in ("draft", "refine") for name, status, draft_only in CASES
+          if kind == "draft" or not draft_only]
+
+
+@pytest.mark.parametrize("kind,name,status", PARAMS, ids=[f"{k}-{n}" for k, n, _ in PARAMS])
+def test_rejected_before_any_side_effect(pool, kind, name, status):
     import torch
     from paper_2607_04461_amd import flashbon as fb
-    if draft_only and kind == "refine":
-        pytest.skip("refinement ignores meta and cache")
     wl, L = pool.wl, pool.L
     meta = fb.new_meta(L)
     for l in range(L):                       # a valid ring: one computed entry at t = 1
