@@ -269,3 +269,25 @@ def test_linear_plan_follows_override_and_rejects_bad_arguments(monkeypatch):
     assert lib.flashbon_op_linear_plan(fb.BF16, 64, 64, 64, 0, None, buf, len(buf)) != 0
     assert lib.flashbon_op_linear_plan(fb.BF16, 64, 64, 64, 0, ctypes.byref(n), buf, len(buf)) == 0
     assert len(buf.value) == 7    # truncated to desc_len - 1 characters
+
+
+@pytest.mark.parametrize("args,status", [
+    ((7, 64, 64, 64), fb.EINVAL),          # bad dtype
+    ((fb.BF16, 0, 64, 64), fb.ESHAPE),     # M < 1
+    ((fb.BF16, 64, 6, 64), fb.ESHAPE),     # N % 4 != 0
+    ((fb.BF16, 64, 64, 12), fb.ESHAPE),    # K % 8 != 0
+])
+def test_linear_ws_rejects_bad_arguments_before_device_work(args, status):
+    """flashbon_op_linear_ws validates on the host and returns before any launch (no device needed)."""
+    sp = ctypes.c_int32(-7)
+    st = fb.load().flashbon_op_linear_ws(*args, None, None, None, fb.EPI_STORE, None, None, None, None, 0,
+                                         ctypes.byref(sp), None)
+    assert st == status
+    assert sp.value == -7                  # nothing reported for a rejected call
+
+
+def test_linear_ws_requires_operands():
+    sp = ctypes.c_int32(-7)
+    st = fb.load().flashbon_op_linear_ws(fb.BF16, 64, 64, 64, None, None, None, fb.EPI_STORE, None, None, None,
+                                         None, 0, ctypes.byref(sp), None)
+    assert st == fb.EINVAL and sp.value == -7
