@@ -270,14 +270,13 @@ def test_cross_attention_kv_index(dtype):
     assert rel_l2(got, ref) <= (1e-2 if dtype == "bf16" else 2e-6)
 
 
-@pytest.mark.parametrize("kernel", ["fa", "mfma"])
-@pytest.mark.parametrize("tq,tk", [(1, 1), (130, 64), (129, 128), (200, 65), (67, 192), (160, 321)])
-def test_attention_mfma_kernels_tile_edges(kernel, tq, tk, monkeypatch):
-    """Both head_dim-128 bf16 kernels (FLASHBON_ATTN: "fa" the pipelined one, the default; "mfma" the
-    unpipelined one) over key counts that give one key, exactly one or two full 64-key tiles, a
-    one-key ragged tail, and odd and even tile counts, with query blocks that end mid-wave; one of
-    the batches reads its keys through the kv index."""
-    monkeypatch.setenv("FLASHBON_ATTN", kernel)
+@pytest.mark.parametrize("tq,tk", [(1, 1), (130, 64), (129, 128), (200, 65), (67, 192), (100, 256),
+                                   (33, 255), (64, 257), (160, 321), (128, 384)])
+def test_attention_mfma_kernel_tile_edges(tq, tk):
+    """The head_dim-128 bf16 kernel over key counts that give one key, 1 to 6 64-key tiles (odd and even
+    counts: the step loop runs in pairs and peels the last one or two), full tiles only, a one-key
+    ragged tail and a one-key-short one, with query blocks that end mid-wave or leave whole waves idle;
+    one of the batches reads its keys through the kv index."""
     F = fb()
     B, NC, heads, dh = 3, 2, 2, 128
     D = heads * dh
