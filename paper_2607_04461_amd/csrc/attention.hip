@@ -10,7 +10,7 @@
 //     accumulated transposed as well, O^T += V^T P^T: the probabilities feed the second MFMA straight
 //     from the first one's accumulator registers (the key order inside each 16-key chunk is permuted
 //     identically on both operands), and every lane rescales only its own query.  K and V tiles are
-//     staged in LDS row-major with 16-byte stores and XOR swizzles; V^T fragments come from gfx950's
+//     staged in LDS row-major, 16-byte chunks XOR-swizzled per row; V^T fragments come from gfx950's
 //     LDS transpose read (ds_read_b64_tr_b16): in each group of 16 lanes, lane j addresses 4
 //     consecutive head dims of one key and lane 4a + b receives element b of the pieces addressed by
 //     lanes a, a + 4, a + 8, a + 12 -- i.e. one head dim across four keys.  Keys are taken in tiles of
