@@ -4,7 +4,9 @@
 //     (k_linear_dma8: 8 waves, two per SIMD, LDS filled by buffer loads that write LDS themselves,
 //     K % 64 == 0 -- the default; k_linear_dma: the same tiles on 4 waves, one per SIMD, for forced
 //     plans; k_linear_mfma<8,4,2,4>: 8 waves of 128x64 with register-staged loads for other K) or
-//     128x128 (4 waves of 64x64, two workgroups per CU), chosen per shape by a round-count model; K
+//     128x128 (4 waves of 64x64, two workgroups per CU), chosen per shape by a round-count model;
+//     k_linear_deep: the 8-wave tile at 128 or 160 rows x 128 or 256 columns with a three-stage LDS
+//     ring, for launches that fit one round of workgroups one per CU (one or two candidates); K
 //     tiles of 64 in double-buffered, XOR-swizzled LDS; XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) and the weight rows
 //     permuted so that every lane owns 8 consecutive output columns of one row.  Every kernel
 //     accumulates K in the same order, so an output element does not depend on the tiling.
@@ -669,28 +671,47 @@ __device__ __forceinline__ void dma_tile(int M, int N, int K, const bf16 *__rest
 // alternating waves keep them busy.  Same LDS layout, LDS-writing loads (waves 0-3 fill the A rows,
 // WTA instructions each per K tile, waves 4-7 the W rows, 8 each), two stages of K = 64 and the same
 // interleaving of fragment reads and loads with the MFMA groups as dma_tile.
-template <int EPI, typename TO, int WTA>
+// s_waitcnt until at most n (wave-uniform, 0..4) K tiles of PER loads each are in flight
+template <int PER>
+__device__ __forceinline__ void wait_tiles(int n) {
+  static_assert(4 * PER < 64, "vmcnt holds 6 bits");
+  switch (n) {
+    case 0: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(vmcnt_imm(PER)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * PER)); break;
+    case 3: __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * PER)); break;
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * PER)); break;
+  }
+}
+
+// One (32 WTA) x (64 WT) tile on 8 waves in a 2 (m) x 4 (n) grid of (16 WTA) x (16 WT) wave tiles, K tiles
+// of 64 through an LDS ring of NST stages, each K tile's loads issued NST - 1 tiles ahead.
+template <int EPI, typename TO, int WTA, int WT = 4, int NST = 2>
 __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__restrict__ A, const bf16 *__restrict__ Wt,
                                           const EpiArgs &e, int m0, int n0, bf16 *smem, int ldk) {
   // K: columns accumulated (K % 64 == 0, K >= 128); ldk: row stride of A and Wt in elements (ldk >= K;
   // larger for one K range of a split-K launch, whose A and Wt point at the range's first column)
   using namespace mf;
-  static_assert(WTA >= 5 && WTA <= 8, "tile height 160..256");
-  constexpr int BM = 32 * WTA, BN = 256, WT = 4;
+  static_assert(WTA >= 4 && WTA <= 8, "tile height 128..256");
+  static_assert(WT == 2 || WT == 4, "tile width 128 or 256");
+  static_assert(NST >= 2 && NST * (32 * WTA + 64 * WT) * BK * 2 <= 160 * 1024, "LDS ring within 160 KB");
+  constexpr int BM = 32 * WTA, BN = 64 * WT;
   constexpr int STAGE = (BM + BN) * BK;
-  constexpr int NL = 8;            // load slots per wave per K tile (A waves use the first WTA)
+  // load slots per K tile: WTA for an A wave (8 WTA rows), 2 WT for a W wave (16 WT rows)
+  constexpr int NL = WTA > 2 * WT ? WTA : 2 * WT;
   constexpr int NR = WT + WTA;     // fragment reads per wave per substep (W, then A)
-  constexpr int NS = WTA;          // MFMA groups of 4 per substep
+  constexpr int NS = WTA;          // MFMA groups of WT per substep
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const bool loads_a = wave < 4;
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A + (int64_t)m0 * ldk, min(M - m0, BM), ldk);
   const __amdgpu_buffer_rsrc_t rsW = tile_rsrc(Wt + (int64_t)n0 * ldk, min(N - n0, BN), ldk);
-  // load x of this wave: rows 8 WTA wave + 8 x .. + 7 of A (waves 0-3, x < WTA) or 64 (wave - 4) +
-  // 8 x .. + 7 of W (waves 4-7); lane l -> row + (l >> 3), slot l & 7
-  uint32_t voff[NL];
-  const int row0 = loads_a ? 8 * WTA * wave : 64 * (wave - 4);
+  // load x of this wave: rows 8 WTA wave + 8 x .. + 7 of A (waves 0-3, x < WTA) or 16 WT (wave - 4) +
+  // 8 x .. + 7 of W (waves 4-7, x < 2 WT); lane l -> row + (l >> 3), slot l & 7
+  static_assert(NL <= 8, "load slots");
+  uint32_t voff[8];   // (a size that depends on the template arguments fails the host pass of hipcc)
+  const int row0 = loads_a ? 8 * WTA * wave : 16 * WT * (wave - 4);
 #pragma unroll
   for (int x = 0; x < NL; ++x) {
     const int r = row0 + 8 * x + (lane >> 3);
@@ -698,7 +719,7 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   }
   const uint32_t lds_row0 = (uint32_t)((loads_a ? 0 : BM * BK) + row0 * BK) * 2u;
   auto dma_one = [&](int kt, int st, int x) {
-    if (loads_a && x >= WTA) return;
+    if (loads_a ? x >= WTA : x >= 2 * WT) return;
     char *dst = reinterpret_cast<char *>(smem) + st * (STAGE * 2) + lds_row0 + x * (8 * BK * 2);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(loads_a ? rsA : rsW, (__attribute__((address_space(3))) void *)dst, 16,
                                              voff[x], kt * BK * 2, 0, 0);
@@ -709,14 +730,14 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   };
   f32x4 acc[WT][WTA];
   const int fr = lane & 15, fq = lane >> 4;
-  // Fragment x of substep ks: x < WT -> W fragment i = x, rows 64 wn + 32 (i/2) + 8 (fr/4) + 4 (i%2) +
+  // Fragment x of substep ks: x < WT -> W fragment i = x, rows 16 WT wn + 32 (i/2) + 8 (fr/4) + 4 (i%2) +
   // fr%4; x >= WT -> A fragment j = x - WT, rows 16 WTA wm + 16 j + fr.  Rows 32 apart share the swizzle.
   uint32_t offW[2][2], offA[2][2];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      offW[ks][q] = 2 * (BM * BK + lds_off(64 * wn + 8 * (fr >> 2) + 4 * q + (fr & 3), fq + 4 * ks));
+      offW[ks][q] = 2 * (BM * BK + lds_off(16 * WT * wn + 8 * (fr >> 2) + 4 * q + (fr & 3), fq + 4 * ks));
       offA[ks][q] = 2 * lds_off(16 * WTA * wm + 16 * q + fr, fq + 4 * ks);
     }
   const char *lds = reinterpret_cast<const char *>(smem);
@@ -747,11 +768,20 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   using T_ = std::true_type;
   using F_ = std::false_type;
   const int KT = K / BK;   // >= 2
-  dma_all(0, 0);
-  dma_all(1, 1);
-  // tile 0 has landed once only this wave's loads of tile 1 may be in flight
-  if (loads_a) __builtin_amdgcn_s_waitcnt(vmcnt_imm(WTA));
-  else __builtin_amdgcn_s_waitcnt(vmcnt_imm(NL));
+  if constexpr (NST == 2) {
+    dma_all(0, 0);
+    dma_all(1, 1);
+    // tile 0 has landed once only this wave's loads of tile 1 may be in flight
+    if (loads_a) __builtin_amdgcn_s_waitcnt(vmcnt_imm(WTA));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * WT));
+  } else {
+    // tiles 0 .. min(NST, KT) - 1 into stages 0 ..; tile 0 has landed once the others alone may be in flight
+#pragma unroll
+    for (int t = 0; t < NST; ++t)
+      if (t < KT) dma_all(t, t);
+    if (loads_a) wait_tiles<WTA>(min(NST, KT) - 1);
+    else wait_tiles<2 * WT>(min(NST, KT) - 1);
+  }
   __syncthreads();
 #pragma unroll
   for (int x = 0; x < NR; ++x) rd(0, 0, fw0, fa0, x);
@@ -759,21 +789,46 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   for (int i = 0; i < WT; ++i)
 #pragma unroll
     for (int j = 0; j < WTA; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
-  int kt = 0;
-  for (; kt + 2 < KT; ++kt) {
+  int kt = 0, last;   // last: the stage of the last K tile
+  if constexpr (NST == 2) {
+    for (; kt + 2 < KT; ++kt) {
+      substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // tile kt+1 has landed
+      __syncthreads();                            // nobody reads stage kt & 1 any more
+      substep(T_{}, T_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, kt + 2, kt & 1);
+    }
     substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // tile kt+1 has landed
-    __syncthreads();                            // nobody reads stage kt & 1 any more
-    substep(T_{}, T_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, kt + 2, kt & 1);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the last K tile has landed
+    __syncthreads();
+    substep(T_{}, F_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, 0, 0);
+    last = (kt + 1) & 1;
+  } else {
+    // stage of tile t: t % NST.  Iteration kt loads tile kt + NST into the stage of tile kt, which every
+    // wave has finished reading by the barrier.
+    int st = 0;
+    for (; kt + NST < KT; ++kt) {
+      const int nx = st + 1 == NST ? 0 : st + 1;
+      substep(T_{}, F_{}, fw0, fa0, st, 1, fw1, fa1, 0, 0);
+      if (loads_a) wait_tiles<WTA>(NST - 2);   // tile kt+1 has landed
+      else wait_tiles<2 * WT>(NST - 2);
+      __syncthreads();
+      substep(T_{}, T_{}, fw1, fa1, nx, 0, fw0, fa0, kt + NST, st);
+      st = nx;
+    }
+    for (; kt + 1 < KT; ++kt) {   // no loads left to issue; tiles kt+2 .. KT-1 may still be in flight
+      const int nx = st + 1 == NST ? 0 : st + 1;
+      substep(T_{}, F_{}, fw0, fa0, st, 1, fw1, fa1, 0, 0);
+      if (loads_a) wait_tiles<WTA>(KT - 2 - kt);
+      else wait_tiles<2 * WT>(KT - 2 - kt);
+      __syncthreads();
+      substep(T_{}, F_{}, fw1, fa1, nx, 0, fw0, fa0, 0, 0);
+      st = nx;
+    }
+    last = st;
   }
-  substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the last K tile has landed
-  __syncthreads();
-  substep(T_{}, F_{}, fw1, fa1, (kt + 1) & 1, 0, fw0, fa0, 0, 0);
-  ++kt;
-  substep(T_{}, F_{}, fw0, fa0, kt & 1, 1, fw1, fa1, 0, 0);
+  substep(T_{}, F_{}, fw0, fa0, last, 1, fw1, fa1, 0, 0);
   substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
-  tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 64 * wn, fr, fq);
+  tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
 }
 
 // MT row blocks x NT column tiles of 256 on the 8-wave tile; row blocks of two heights as in
@@ -795,6 +850,21 @@ __global__ __launch_bounds__(512, 1) void k_linear_dma8(int M, int N, int K, con
     }
   }
   dma8_tile<EPI, TO, WTA>(M, N, K, A, Wt, e, m0, n0, smem, K);
+}
+
+// MT x NT tiles of (32 WTA) x (64 WT) on the 8-wave tile with an LDS ring of NST stages: for launches with
+// no more tiles than CUs, where each workgroup's K loop waits on load latency rather than on the matrix
+// cores (one candidate's projections, M = 1560).
+template <int EPI, typename TO, int WTA, int WT, int NST>
+__global__ __launch_bounds__(512, 1) void k_linear_deep(int M, int N, int K, const bf16 *__restrict__ A,
+                                                 const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT,
+                                                 int group_m) {
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  int mt, nt;
+  mf::tile_of(blockIdx.x, MT, NT, mt, nt, group_m);
+  const int m0 = 32 * WTA * mt, n0 = 64 * WT * nt;
+  if (m0 >= M) return;
+  dma8_tile<EPI, TO, WTA, WT, NST>(M, N, K, A, Wt, e, m0, n0, smem, K);
 }
 
 // Split-K: MT x NT tiles of 224 x 256 on the 8-wave tile, each tile's K range cut into `splits` ranges of
@@ -917,7 +987,7 @@ __global__ __launch_bounds__(256) void k_linear_valu(int M, int N, int K, const 
 // == 0, K >= 128, N % 8 == 0) the 256-column tiles run on the 8-wave kernel, which measured 6-7%
 // faster than the 4-wave kernel on the same tiles at every projection of the draft; the 4-wave
 // kernel is kept for forced plans.
-enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT, PLAN_MIX };
+enum TilePlan { PLAN_BIG, PLAN_SMALL, PLAN_SPLIT, PLAN_MIX, PLAN_DEEP };
 struct TileChoice {
   TilePlan plan;
   int wta;    // PLAN_MIX: the taller height, 32 wta rows
@@ -925,8 +995,13 @@ struct TileChoice {
   int mb;     // PLAN_MIX: row blocks
   int tall;   // PLAN_MIX: row blocks of the taller height (the others are 32 (wta - 1) rows)
   int waves = 4;   // PLAN_MIX: the 4-wave (k_linear_dma) or the 8-wave (k_linear_dma8) kernel
+  int wt = 4, nst = 2;   // PLAN_DEEP: (32 wta) x (64 wt) tiles, nst LDS stages
 };
 static int cu_count();
+// The deep-ring instantiations: 128 or 160 rows x 128 or 256 columns, 2 or 3 LDS stages.
+static bool deep_ok(int wta, int wt, int nst) {
+  return (wta == 4 || wta == 5) && (wt == 2 || wt == 4) && (nst == 2 || nst == 3);
+}
 
 // Round-count model, in units of one K step of a 256x256 round: a launch takes ceil(tiles / slots)
 // rounds; a round of 4-wave tiles 32 w rows high costs kF[w] K + kG (the constant: per-tile prologue
@@ -951,9 +1026,20 @@ static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
   // `tall` of them 32 w rows high and the rest 32 (w - 1), w in 6..8, covering M), or
   // "split:<rows>" (rows a multiple of 256 with 0 < rows < M: the first rows on 256x256 tiles, the
   // rest on 128x128 tiles); "w8" (the 8-wave kernel, 256x256 tiles), "w8:bm:<rows>" and
-  // "w8:mix:<w>:<blocks>:<tall>" (the 8-wave kernel with those row blocks)
+  // "w8:mix:<w>:<blocks>:<tall>" (the 8-wave kernel with those row blocks); "deep:<rows>:<cols>:<stages>"
+  // (k_linear_deep: rows 128 or 160, cols 128 or 256, 2 or 3 LDS stages)
   const char *force = getenv("FLASHBON_LINEAR_TILE");
   if (force) {
+    if (dma_ok && !strncmp(force, "deep:", 5)) {
+      int rows = 0, cols = 0, nst = 0;
+      if (sscanf(force + 5, "%d:%d:%d", &rows, &cols, &nst) == 3 && deep_ok(rows / 32, cols / 64, nst) &&
+          rows % 32 == 0 && cols % 64 == 0) {
+        TileChoice c = {PLAN_DEEP, rows / 32, 0, 0, 0, 8};
+        c.wt = cols / 64;
+        c.nst = nst;
+        return c;
+      }
+    }
     if (!strncmp(force, "split:", 6)) {
       const int rows = atoi(force + 6);
       if (rows > 0 && rows % 256 == 0 && rows < M && K % mf::BK == 0) return {PLAN_SPLIT, 8, rows, 0, 0};
@@ -1027,6 +1113,27 @@ static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
         if (t < (1.0 - gain) * t_pure && t < t_best) { t_best = t; best = {PLAN_MIX, w, 0, mb, tall, 8}; }
       }
     }
+    // Where a launch fits in one round of workgroups one per CU (one or two candidates' projections,
+    // M = 1560 or 3120), every workgroup's K loop waits on load latency: there the 8-wave tile with a
+    // third LDS stage (loads two K tiles ahead) runs instead, on whichever of 128 x 128, 160 x 128,
+    // 128 x 256 and 160 x 256 gives the most tiles within one round.  Measured at M = 1560, K = 1536:
+    // QKV (128 x 256, 234 tiles) 28.3 -> 26.6 us, the N = 1536 projections (128 x 128, 156 tiles)
+    // 21.0 -> 14.0 us (store) and 24.6 -> 18.2 us (residual); at M = 3120 (160 x 128, 240 tiles) the
+    // N = 1536 residual projection 37.2 -> 22.4 us and MLP down 104.3 -> 83.5 us.  Four or five stages
+    // measured no faster than three.
+    static constexpr int kDeepTiles[4][2] = {{4, 2}, {5, 2}, {4, 4}, {5, 4}};   // (wta, wt)
+    TileChoice deep = {PLAN_DEEP, 0, 0, 0, 0, 8};
+    deep.nst = 3;
+    int64_t most = 0;
+    for (const auto &d : kDeepTiles) {
+      const int64_t t = (int64_t)((M + 32 * d[0] - 1) / (32 * d[0])) * ((N + 64 * d[1] - 1) / (64 * d[1]));
+      if (t <= cus && t > most) {
+        most = t;
+        deep.wta = d[0];
+        deep.wt = d[1];
+      }
+    }
+    if (most > 0) return deep;
   }
   return best;
 }
@@ -1104,6 +1211,23 @@ static hipError_t launch_dma8(int M, int N, int K, const void *A, const void *Wt
   return hipGetLastError();
 }
 
+// The deep-ring 8-wave kernel: (32 WTA) x (64 WT) tiles, NST LDS stages.
+template <int EPI, int WTA, int WT, int NST>
+static hipError_t launch_deep(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s) {
+  const size_t lds = (size_t)NST * (32 * WTA + 64 * WT) * mf::BK * sizeof(bf16);
+  auto kern = k_linear_deep<EPI, bf16, WTA, WT, NST>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int MT = (M + 32 * WTA - 1) / (32 * WTA), NT = (N + 64 * WT - 1) / (64 * WT);
+  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(512), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e, MT, NT,
+                     group_rows(MT, NT, K));
+  return hipGetLastError();
+}
+
 static int cu_count() {
   static int n = 0;
   if (!n) {
@@ -1152,6 +1276,20 @@ static hipError_t launch_epi(ActType t, int M, int N, int K, const void *A, cons
     if (c.plan == PLAN_SMALL) return launch_mfma<4, 4, 2, 2, EPI, 2>(M, N, K, A, Wt, e, s);
     if (c.plan == PLAN_BIG) return launch_big<EPI>(M, N, K, A, Wt, e, s);
     if constexpr (EPI != EPI_EULER) {
+      if (c.plan == PLAN_DEEP) {
+        const int key = 100 * c.wta + 10 * c.wt + c.nst;
+        switch (key) {
+          case 422: return launch_deep<EPI, 4, 2, 2>(M, N, K, A, Wt, e, s);
+          case 423: return launch_deep<EPI, 4, 2, 3>(M, N, K, A, Wt, e, s);
+          case 522: return launch_deep<EPI, 5, 2, 2>(M, N, K, A, Wt, e, s);
+          case 523: return launch_deep<EPI, 5, 2, 3>(M, N, K, A, Wt, e, s);
+          case 442: return launch_deep<EPI, 4, 4, 2>(M, N, K, A, Wt, e, s);
+          case 443: return launch_deep<EPI, 4, 4, 3>(M, N, K, A, Wt, e, s);
+          case 542: return launch_deep<EPI, 5, 4, 2>(M, N, K, A, Wt, e, s);
+          case 543: return launch_deep<EPI, 5, 4, 3>(M, N, K, A, Wt, e, s);
+          default: return hipErrorInvalidValue;
+        }
+      }
       if (c.plan == PLAN_MIX && c.waves == 8) {
         if (c.wta == 8) return launch_dma8<EPI, 8>(M, N, K, A, Wt, e, s, c.mb, c.tall);
         if (c.wta == 7) return launch_dma8<EPI, 7>(M, N, K, A, Wt, e, s, c.mb, c.tall);
@@ -1185,7 +1323,10 @@ int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len)
     TileChoice c = pick_tiles(M, N, K, dma_ok);
     if (c.plan == PLAN_SPLIT && epi == EPI_EULER) c = {PLAN_BIG, 8, 0, 0, 0};
     const std::string nt = std::to_string((N + 255) / 256);
-    if (c.plan == PLAN_SMALL) {
+    if (c.plan == PLAN_DEEP) {
+      d = "k_linear_deep (8 waves): " + rows_of(c.wta) + "x" + std::to_string(64 * c.wt) + " tiles, " +
+          std::to_string(c.nst) + " LDS stages";
+    } else if (c.plan == PLAN_SMALL) {
       d = "k_linear_mfma: 128x128 tiles, 4 waves, two workgroups per CU";
     } else if (c.plan == PLAN_BIG) {
       d = dma_ok ? "k_linear_dma8 (8 waves): 256x256 tiles, " + std::to_string((M + 255) / 256) + " row blocks x " + nt

@@ -84,7 +84,9 @@ def test_linear_small(dtype, M, N, K, epi):
 
 
 @pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256", "bm:224", "bm:192", "bm:160", "mix:7:3:1",
-                                  "mix:8:3:1", "mix:6:4:2", "w8", "w8:bm:160", "w8:mix:7:3:1", "w8:mix:8:3:1"])
+                                  "mix:8:3:1", "mix:6:4:2", "w8", "w8:bm:160", "w8:mix:7:3:1", "w8:mix:8:3:1",
+                                  "deep:128:128:2", "deep:128:128:3", "deep:160:128:3", "deep:128:256:3",
+                                  "deep:160:256:3"])
 @pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
                                    (520, 776, 1024)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
@@ -94,7 +96,8 @@ def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
     on 128x128 tiles, when M > 256 and K % 64 == 0; "bm:<rows>" the 4-wave kernel with tiles of one
     height; "mix:w:blocks:tall" the 4-wave kernel with row blocks of two heights, 32 w and 32 (w - 1)
     rows, spread over the blocks; "w8", "w8:bm:<rows>", "w8:mix:..." the 8-wave kernel with LDS-writing
-    loads on the same row blocks; plans the
+    loads on the same row blocks; "deep:<rows>:<cols>:<stages>" the 8-wave tile with a deeper LDS ring,
+    whose K loop is shorter than its ring for the smaller K; plans the
     shape cannot take fall back to 256x256) on ragged M, N
     and K tails, against the oracle.
     The residual case also writes the cache copy."""
@@ -136,7 +139,9 @@ def test_linear_tile_plans_bit_identical(epi, monkeypatch):
     h0 = _dev(synth.random_matrix((M, N), 85), "fp32")
     outs = []
     for tile in ["256x256", "128x128", "split:512", "bm:224", "bm:192", "bm:160", "mix:7:6:1", "mix:8:5:1",
-                 "mix:6:7:3", "w8", "w8:bm:224", "w8:bm:192", "w8:bm:160", "w8:mix:7:6:1", "w8:mix:6:7:3"]:
+                 "mix:6:7:3", "w8", "w8:bm:224", "w8:bm:192", "w8:bm:160", "w8:mix:7:6:1", "w8:mix:6:7:3",
+                 "deep:128:128:2", "deep:128:128:3", "deep:160:128:2", "deep:160:128:3", "deep:128:256:2",
+                 "deep:128:256:3", "deep:160:256:2", "deep:160:256:3"]:
         monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
         if epi == "store":
             out = torch.empty((M, N), device="cuda", dtype=torch.float32)

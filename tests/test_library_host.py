@@ -225,13 +225,20 @@ def test_select_rejects_bad_arguments():
     ((24960, 1536, 8960, 3), 1, "k_linear_dma8 (8 waves): 128 row blocks x 6, 12 of 224 rows and 116 of 192"),
     ((16384, 15360, 5120, 0), 1, "k_linear_dma8 (8 waves): 256x256 tiles, 64 row blocks x 60"),
     ((200, 136, 72, 0), 1, "k_linear_mfma: 256x256 tiles, 8 waves"),
+    ((1560, 4608, 1536, 0), 1, "k_linear_deep (8 waves): 128x256 tiles, 3 LDS stages"),
+    ((1560, 8960, 1536, 1), 1, "k_linear_dma8 (8 waves): 224x256 tiles, 7 row blocks x 35"),
+    ((1560, 1536, 1536, 3), 1, "k_linear_deep (8 waves): 128x128 tiles, 3 LDS stages"),
+    ((1560, 1536, 8960, 3), 1, "k_linear_deep (8 waves): 128x128 tiles, 3 LDS stages"),
+    ((3120, 1536, 1536, 3), 1, "k_linear_deep (8 waves): 160x128 tiles, 3 LDS stages"),
 ])
 def test_linear_plan_of_model_shapes(shape, kernels, desc, monkeypatch):
     """The tile plan is a host decision (no device needed; 256 CUs assumed without one).  At the
     1.3B-shaped pool's M = 16 x 1560 rows: QKV and MLP up on row blocks of 256 and 224 rows of the
     8-wave kernel that fill 7 and 14 rounds, the N = 1536 projections on 128 row blocks of 224 and 192
     rows that fill three rounds exactly;
-    K % 64 != 0 takes the generic 8-wave kernel with register-staged loads."""
+    K % 64 != 0 takes the generic 8-wave kernel with register-staged loads.  One candidate's projections
+    (M = 1560) and two candidates' N = 1536 projections fit one round of the deep-ring tile, on the tile
+    that gives the most workgroups within it; MLP up at M = 1560 does not (7 x 35 tiles of 224 rows)."""
     monkeypatch.delenv("FLASHBON_LINEAR_TILE", raising=False)
     assert fb.flashbon_op_linear_plan(fb.BF16, *shape) == (kernels, desc)
     # the row blocks named cover M with no block starting past it
