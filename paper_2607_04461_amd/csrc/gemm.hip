@@ -867,25 +867,26 @@ __global__ __launch_bounds__(512, 1) void k_linear_deep(int M, int N, int K, con
   dma8_tile<EPI, TO, WTA, WT, NST>(M, N, K, A, Wt, e, m0, n0, smem, K);
 }
 
-// Split-K: MT x NT tiles of 224 x 256 on the 8-wave tile, each tile's K range cut into `splits` ranges of
-// ks columns (the last one shorter); workgroup (tile, split) accumulates its range and stores the fp32
-// partial sums into part + split M N ([M][N] per split, no bias).  k_splitk_reduce then adds the splits
-// in order and applies the epilogue.  For launches whose tiles alone would leave most CUs idle (one
-// candidate's MLP down-projection: 42 tiles, K = 8960).
-__global__ __launch_bounds__(512, 1) void k_linear_dma8_splitk(int M, int N, int K, const bf16 *__restrict__ A,
-                                                        const bf16 *__restrict__ Wt, float *__restrict__ part,
-                                                        int MT, int NT, int ks, int group_m) {
+// Split-K: MT x NT tiles of (32 WTA) x (64 WT) on the 8-wave tile with an LDS ring of NST stages, each
+// tile's K range cut into `splits` ranges of ks columns (the last one shorter); workgroup (tile, split)
+// accumulates its range and stores the fp32 partial sums into part + split M N ([M][N] per split, no
+// bias).  k_splitk_reduce then adds the splits in order and applies the epilogue.  For launches whose
+// tiles alone would leave most CUs idle (one candidate's MLP down-projection, K = 8960).
+template <int WTA, int WT, int NST>
+__global__ __launch_bounds__(512, 1) void k_linear_splitk(int M, int N, int K, const bf16 *__restrict__ A,
+                                                   const bf16 *__restrict__ Wt, float *__restrict__ part,
+                                                   int MT, int NT, int ks, int group_m) {
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   const int tiles = MT * NT;
   const int split = blockIdx.x / tiles;
   int mt, nt;
   mf::tile_of(blockIdx.x - split * tiles, MT, NT, mt, nt, group_m);
-  const int m0 = 224 * mt, n0 = nt * 256, k0 = split * ks;
+  const int m0 = 32 * WTA * mt, n0 = 64 * WT * nt, k0 = split * ks;
   if (m0 >= M || k0 >= K) return;
   EpiArgs e;
   e.out = part + (int64_t)split * M * N;
   e.ldo = N;
-  dma8_tile<EPI_STORE_F32, float, 7>(M, N, min(ks, K - k0), A + k0, Wt + k0, e, m0, n0, smem, K);
+  dma8_tile<EPI_STORE_F32, float, WTA, WT, NST>(M, N, min(ks, K - k0), A + k0, Wt + k0, e, m0, n0, smem, K);
 }
 
 // out = epilogue(sum over s of part[s] + bias), the splits added in order s = 0, 1, ..; one thread per 8
@@ -998,6 +999,8 @@ struct TileChoice {
   int wt = 4, nst = 2;   // PLAN_DEEP: (32 wta) x (64 wt) tiles, nst LDS stages
 };
 static int cu_count();
+// The deep-ring tiles (wta, wt) in the order the plans try them: 128 x 128, 160 x 128, 128 x 256, 160 x 256.
+static constexpr int kDeepTiles[4][2] = {{4, 2}, {5, 2}, {4, 4}, {5, 4}};
 // The deep-ring instantiations: 128 or 160 rows x 128 or 256 columns, 2 or 3 LDS stages.
 static bool deep_ok(int wta, int wt, int nst) {
   return (wta == 4 || wta == 5) && (wt == 2 || wt == 4) && (nst == 2 || nst == 3);
@@ -1121,7 +1124,6 @@ static TileChoice pick_tiles(int M, int N, int K, bool dma_ok) {
     // 21.0 -> 14.0 us (store) and 24.6 -> 18.2 us (residual); at M = 3120 (160 x 128, 240 tiles) the
     // N = 1536 residual projection 37.2 -> 22.4 us and MLP down 104.3 -> 83.5 us.  Four or five stages
     // measured no faster than three.
-    static constexpr int kDeepTiles[4][2] = {{4, 2}, {5, 2}, {4, 4}, {5, 4}};   // (wta, wt)
     TileChoice deep = {PLAN_DEEP, 0, 0, 0, 0, 8};
     deep.nst = 3;
     int64_t most = 0;
@@ -1353,45 +1355,93 @@ int describe_linear(ActType t, int epi, int M, int N, int K, char *buf, int len)
   return kernels;
 }
 
-// Splits of the split-K plan for this shape (1 = none): only bf16 shapes the 8-wave kernel takes, whose
-// 224 x 256 tiles fill less than half the CUs, with at least 16 K tiles per split and the partial sums
-// within kSplitBytes.  A function of the shape alone, so every caller with a workspace gets the same
-// plan (and the same bits).
-int splitk_splits(int epi, int M, int N, int K) {
-  if (epi == EPI_EULER || K % mf::BK || N % 8 || K < 2 * mf::BK) return 1;
+// The split-K plan of a shape: the tile (32 wta) x (64 wt) with nst LDS stages, cut into `splits` K
+// ranges (1 = none).  Only bf16 shapes the 8-wave kernel takes, whose 224 x 256 tiles fill less than half
+// the CUs, with at least 16 K tiles per split and the partial sums within kSplitBytes.  Among the
+// deep-ring tiles (three LDS stages) and split counts, the plan with the most workgroups within one
+// round of the CUs (on a tie, the first tile in kDeepTiles order and the fewest splits).  Measured for one
+// candidate's MLP down-projection (M = 1560, N = 1536, K = 8960, residual epilogue; reduction included):
+// 160 x 128 x 2 ranges (240 workgroups) 53 us, against 62 us for 224 x 256 x 5 ranges on two stages,
+// 56 us for 128 x 256 x 3, 60 us for 160 x 256 x 4 and 63 us unsplit (128 x 128, 156 workgroups).  A
+// function of the shape alone, so every caller with a workspace gets the same plan (and the same bits).
+// FLASHBON_SPLITK (tuning): "<rows>:<cols>:<stages>:<splits>" forces a plan on the shapes that split.
+struct SplitPlan {
+  int splits, wta, wt, nst;
+};
+static SplitPlan splitk_plan(int epi, int M, int N, int K) {
+  SplitPlan none = {1, 7, 4, 2};
+  if (epi == EPI_EULER || K % mf::BK || N % 8 || K < 2 * mf::BK) return none;
   const int64_t tiles = (int64_t)((M + 223) / 224) * ((N + 255) / 256);
   const int cus = cu_count();
-  if (2 * tiles > cus) return 1;
-  int sp = (int)std::min<int64_t>(cus / tiles, K / (16 * mf::BK));
-  sp = (int)std::min<int64_t>(sp, (int64_t)(kSplitBytes / ((size_t)M * N * 4)));
-  // the launch gives each split ceil(kt / sp) K tiles: take the largest count for which every split is
-  // non-empty and the last has at least the two K tiles the tile loop needs
+  if (2 * tiles > cus) return none;
   const int kt = K / mf::BK;
-  for (; sp >= 2; --sp) {
+  // the launch gives each split ceil(kt / sp) K tiles: a count is usable when every split is non-empty
+  // and the last has at least the two K tiles the tile loop needs
+  auto usable = [&](int sp) {
     const int ks = (kt + sp - 1) / sp;
-    if ((kt + ks - 1) / ks == sp && kt - (sp - 1) * ks >= 2) return sp;
+    return sp >= 2 && (kt + ks - 1) / ks == sp && kt - (sp - 1) * ks >= 2 &&
+           (size_t)sp * M * N * 4 <= kSplitBytes;
+  };
+  const char *force = getenv("FLASHBON_SPLITK");
+  if (force) {
+    int rows = 0, cols = 0, nst = 0, sp = 0;
+    if (sscanf(force, "%d:%d:%d:%d", &rows, &cols, &nst, &sp) == 4 && usable(sp) &&
+        ((rows == 224 && cols == 256 && nst == 2) || (deep_ok(rows / 32, cols / 64, nst) && rows % 32 == 0 &&
+                                                       cols % 64 == 0)))
+      return {sp, rows / 32, cols / 64, nst};
   }
-  return 1;
+  SplitPlan best = none;
+  int64_t most = 0;
+  for (const auto &d : kDeepTiles) {
+    const int64_t t = (int64_t)((M + 32 * d[0] - 1) / (32 * d[0])) * ((N + 64 * d[1] - 1) / (64 * d[1]));
+    for (int sp = 2; sp <= K / (16 * mf::BK) && t * sp <= cus; ++sp)
+      if (usable(sp) && t * sp > most) {
+        most = t * sp;
+        best = {sp, d[0], d[1], 3};
+      }
+  }
+  return best;
+}
+
+int splitk_splits(int epi, int M, int N, int K) { return splitk_plan(epi, M, N, K).splits; }
+
+template <int WTA, int WT, int NST>
+static hipError_t launch_splitk(int M, int N, int K, const void *A, const void *Wt, float *part, int sp,
+                                hipStream_t s) {
+  const int ks = (K / mf::BK + sp - 1) / sp * mf::BK;
+  const size_t lds = (size_t)NST * (32 * WTA + 64 * WT) * mf::BK * sizeof(bf16);
+  auto kern = k_linear_splitk<WTA, WT, NST>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int MT = (M + 32 * WTA - 1) / (32 * WTA), NT = (N + 64 * WT - 1) / (64 * WT);
+  hipLaunchKernelGGL(kern, dim3(MT * NT * sp), dim3(512), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, part,
+                     MT, NT, ks, group_rows(MT, NT, K));
+  return hipGetLastError();
 }
 
 hipError_t launch_linear_ws(ActType t, int epi, int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e,
                             hipStream_t s, void *ws, size_t ws_bytes) {
-  const int sp = t == ACT_BF16 && ws ? splitk_splits(epi, M, N, K) : 1;
+  const SplitPlan pl = t == ACT_BF16 && ws ? splitk_plan(epi, M, N, K) : SplitPlan{1, 7, 4, 2};
+  const int sp = pl.splits;
   if (sp < 2 || (size_t)sp * M * N * 4 > ws_bytes) return launch_linear(t, epi, M, N, K, A, Wt, e, s);
-  const int ks = (K / mf::BK + sp - 1) / sp * mf::BK;
-  const size_t lds = (size_t)2 * (224 + 256) * mf::BK * sizeof(bf16);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute((const void *)k_linear_dma8_splitk, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)lds);
-    if (err != hipSuccess) return err;
-    attr_set = true;
-  }
-  const int MT = (M + 223) / 224, NT = (N + 255) / 256;
   float *part = (float *)ws;
-  hipLaunchKernelGGL(k_linear_dma8_splitk, dim3(MT * NT * sp), dim3(512), lds, s, M, N, K, (const bf16 *)A,
-                     (const bf16 *)Wt, part, MT, NT, ks, group_rows(MT, NT, K));
-  hipError_t err = hipGetLastError();
+  hipError_t err;
+  switch (100 * pl.wta + 10 * pl.wt + pl.nst) {
+    case 742: err = launch_splitk<7, 4, 2>(M, N, K, A, Wt, part, sp, s); break;
+    case 422: err = launch_splitk<4, 2, 2>(M, N, K, A, Wt, part, sp, s); break;
+    case 423: err = launch_splitk<4, 2, 3>(M, N, K, A, Wt, part, sp, s); break;
+    case 522: err = launch_splitk<5, 2, 2>(M, N, K, A, Wt, part, sp, s); break;
+    case 523: err = launch_splitk<5, 2, 3>(M, N, K, A, Wt, part, sp, s); break;
+    case 442: err = launch_splitk<4, 4, 2>(M, N, K, A, Wt, part, sp, s); break;
+    case 443: err = launch_splitk<4, 4, 3>(M, N, K, A, Wt, part, sp, s); break;
+    case 542: err = launch_splitk<5, 4, 2>(M, N, K, A, Wt, part, sp, s); break;
+    case 543: err = launch_splitk<5, 4, 3>(M, N, K, A, Wt, part, sp, s); break;
+    default: return hipErrorInvalidValue;
+  }
   if (err != hipSuccess) return err;
   const int64_t threads = (int64_t)M * (N / 8);
   const dim3 grid((unsigned)((threads + 255) / 256));
