@@ -459,3 +459,35 @@ def test_linear_splitk_with_workspace(M, N, K, epi):
         outs.append((sp, got))
     assert outs[0][0] > 1, "the plan should split this shape"
     assert outs[1][0] == 1, "a workspace too small for the plan runs one range"
+
+
+@pytest.mark.parametrize("plan", ["224:256:2:2", "128:128:3:2", "128:128:2:3", "160:128:3:3", "128:256:3:2",
+                                  "160:256:3:2", "160:256:2:3"])
+@pytest.mark.parametrize("epi", ["gelu", "residual"])
+def test_linear_splitk_forced_plans(plan, epi, monkeypatch):
+    """Every split-K tile (FLASHBON_SPLITK = rows:cols:stages:ranges) on ragged M and N, against the fp64
+    reference: the K ranges of each tile's partial sums, written to the workspace and added in range
+    order, must cover K exactly once for every tile shape and ring depth."""
+    monkeypatch.setenv("FLASHBON_SPLITK", plan)
+    F = fb()
+    M, N, K = 300, 520, 3072
+    A = _operand((M, K), 21, "bf16")
+    W = _operand((N, K), 22, "bf16", 0.02)
+    bias = synth.random_matrix((N,), 23, 0.02)
+    gate = synth.random_matrix((N,), 24)
+    h0 = synth.random_matrix((M, N), 25)
+    ws = torch.empty(48 << 18, device="cuda", dtype=torch.float32)
+    ref = odit.linear(A.astype(np.float64), W, bias)
+    if epi == "gelu":
+        out = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        sp = F.flashbon_op_linear_ws(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"),
+                                     F.EPI_GELU, out, ws)
+        expect, tol = odit.gelu_tanh(ref), 6e-3
+    else:
+        out = _dev(h0, "fp32")
+        sp = F.flashbon_op_linear_ws(F.BF16, M, N, K, _dev(A, "bf16"), _dev(W, "bf16"), _dev(bias, "fp32"),
+                                     F.EPI_RESIDUAL, out, ws, gate=_dev(gate, "fp32"))
+        expect, tol = h0 + gate * ref, 2e-6
+    torch.cuda.synchronize()
+    assert sp == int(plan.split(":")[3])
+    assert rel_l2(out.float().cpu().numpy(), expect) <= tol
