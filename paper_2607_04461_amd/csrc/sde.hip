@@ -69,12 +69,21 @@ __global__ __launch_bounds__(256) void k_head_update(int C, int H, int W, int p,
   float *zb = z + (int64_t)b * chw;
   const float *vb = v + (int64_t)b * T * P;
   const float *vu = guided ? v + (int64_t)(n + b) * T * P : nullptr;
+  // (c, y, x) of the quad's first element by one 32-bit division each (a candidate's latent holds
+  // fewer than 2^31 elements), then carried element by element
+  const int e0 = (int)(4 * q);
+  int c = e0 / hw, y = (e0 - c * hw) / W, x = e0 - c * hw - y * W;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int64_t e = 4 * q + i;
     if (e >= chw) break;
-    const int c = (int)(e / hw), yx = (int)(e - (int64_t)c * hw);
-    const int y = yx / W, x = yx - y * W;
+    if (i > 0 && ++x == W) {
+      x = 0;
+      if (++y == H) {
+        y = 0;
+        ++c;
+      }
+    }
     const int ti = y / p, di = y - ti * p, tj = x / p, dj = x - tj * p;
     const int64_t vi = (int64_t)(ti * wp + tj) * P + c * pp + di * p + dj;
     float vv = vb[vi];
