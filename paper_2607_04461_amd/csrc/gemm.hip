@@ -173,9 +173,20 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_
 __device__ __forceinline__ f32x4 ld4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
+// POL: the cache-policy bits of the store (0, or kStoreNT below)
+template <int POL = 0>
 __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, POL);
 }
+// Non-temporal (the nt bit): the 8-wave kernel's bf16 output stores (store and GELU epilogues) when the
+// launch's output is at least kNTBytes, so that a round's burst of output lines does not push the next
+// tiles' operands out of L2.  Measured on the 1.3B-shaped pool of 16 (same box, alternating, latents
+// bit-identical): draft 240.7 -> 238.4 ms; with the residual epilogues' fp32 stores non-temporal too 238.9
+// (the residual projection alone 168 -> 146 us, but the next LayerNorm then reads its rows from further
+// out); with non-temporal stores at every size, one candidate's refinement step (outputs of 10-28 MB, read
+// back from the caches by the next kernel) measured 7.53 -> 7.78 ms, hence the size threshold.
+constexpr int kStoreNT = 2;
+constexpr size_t kNTBytes = (size_t)128 << 20;
 }  // namespace epi
 
 // A wave's output, whatever the MFMA shape, is walked as NCG column groups x NRB row blocks: in row
@@ -186,7 +197,7 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
 // (CM 1: copy of the new row, CM 2: new row minus what the cache held).  Batches of JB row blocks of one column group; a column group's
 // bias and gate come with its first batch.  PIPE 2: the loads of batch x + 1 are issued before the
 // stores of batch x.
-template <int NCG, int NRB, int RS, int CM, int PIPE, int JB, typename Col, typename Val>
+template <int NCG, int NRB, int RS, int CM, int PIPE, int JB, int POL = 0, typename Col, typename Val>
 __device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, int mbase, int nbase, int r0,
                                               Col col, Val val) {
   using namespace epi;
@@ -250,9 +261,9 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, in
 #pragma unroll
         for (int q = 0; q < 4; ++q) o[q] += g[cg][hf][q] * (val(cg, j0 + jj, 4 * hf + q) + b[cg][hf][q]);
         const uint32_t off = ro + (uint32_t)(j0 + jj) * rstep + (hf ? c1[cg] : c0[cg]);
-        st4(rsO, off, o);
-        if constexpr (CM == 1) st4(rsC, off, o);
-        if constexpr (CM == 2) st4(rsC, off, o - c[buf][jj][hf]);
+        st4<POL>(rsO, off, o);
+        if constexpr (CM == 1) st4<POL>(rsC, off, o);
+        if constexpr (CM == 2) st4<POL>(rsC, off, o - c[buf][jj][hf]);
       }
     }
   }
@@ -260,7 +271,7 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, in
 
 // Store (bf16 or fp32), GELU-and-store, or fp32 store; bias loaded first, no load between the
 // stores.  WHOLE8: N % 8 == 0, one 16-byte store per 8 bf16 values; else two 8-byte stores.
-template <int EPI, typename TO, int NCG, int NRB, int RS, bool WHOLE8, typename Col, typename Val>
+template <int EPI, typename TO, int NCG, int NRB, int RS, bool WHOLE8, int POL = 0, typename Col, typename Val>
 __device__ __forceinline__ void store_tile(const EpiArgs &e, int M, int N, int mbase, int nbase, int r0, Col col,
                                            Val val) {
   using namespace epi;
@@ -295,17 +306,17 @@ __device__ __forceinline__ void store_tile(const EpiArgs &e, int M, int N, int m
       const uint32_t o0 = c0[cg] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c0[cg]) * ES;
       const uint32_t o1 = c1[cg] == OUT_OF_RANGE ? OUT_OF_RANGE : (ro + c1[cg]) * ES;
       if constexpr (F32) {
-        st4(rsO, o0, f32x4{v[0], v[1], v[2], v[3]});
-        st4(rsO, o1, f32x4{v[4], v[5], v[6], v[7]});
+        st4<POL>(rsO, o0, f32x4{v[0], v[1], v[2], v[3]});
+        st4<POL>(rsO, o1, f32x4{v[4], v[5], v[6], v[7]});
       } else {
         const bf16x4 w0 = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
         const bf16x4 w1 = {(bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
         if constexpr (WHOLE8) {
           const bf16x8 w = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w), rsO, o0, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w), rsO, o0, 0, POL);
         } else {
-          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w0), rsO, o0, 0, 0);
-          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w1), rsO, o1, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w0), rsO, o0, 0, POL);
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w1), rsO, o1, 0, POL);
         }
       }
     }
@@ -314,14 +325,14 @@ __device__ __forceinline__ void store_tile(const EpiArgs &e, int M, int N, int m
 
 // The epilogue of a wave's output for every epilogue kind, on the group/block walk above.  PIPE:
 // residual rows fetched one batch ahead (2) or per batch (1), by the kernel's register budget.
-template <int EPI, typename TO, int NCG, int NRB, int RS, int PIPE, bool WHOLE8, typename Col, typename Val>
+template <int EPI, typename TO, int NCG, int NRB, int RS, int PIPE, bool WHOLE8, int POL = 0, typename Col, typename Val>
 __device__ __forceinline__ void wave_epilogue(const EpiArgs &e, int M, int N, int mbase, int nbase, int r0, Col col,
                                               Val val) {
   if constexpr (EPI == EPI_RESIDUAL) {
     constexpr int JB = PIPE == 2 ? (NRB % 2 == 0 ? 2 : 1) : (NRB % 4 == 0 ? 4 : (NRB % 2 == 0 ? 2 : 1));
-    if (!e.cache) residual_tile<NCG, NRB, RS, 0, PIPE, JB>(e, M, N, mbase, nbase, r0, col, val);
-    else if (!e.cache_delta) residual_tile<NCG, NRB, RS, 1, PIPE, JB>(e, M, N, mbase, nbase, r0, col, val);
-    else residual_tile<NCG, NRB, RS, 2, 1, JB>(e, M, N, mbase, nbase, r0, col, val);
+    if (!e.cache) residual_tile<NCG, NRB, RS, 0, PIPE, JB, POL>(e, M, N, mbase, nbase, r0, col, val);
+    else if (!e.cache_delta) residual_tile<NCG, NRB, RS, 1, PIPE, JB, POL>(e, M, N, mbase, nbase, r0, col, val);
+    else residual_tile<NCG, NRB, RS, 2, 1, JB, POL>(e, M, N, mbase, nbase, r0, col, val);
   } else if constexpr (EPI == EPI_EULER) {
 #pragma unroll
     for (int cg = 0; cg < NCG; ++cg) {
@@ -339,17 +350,17 @@ __device__ __forceinline__ void wave_epilogue(const EpiArgs &e, int M, int N, in
       }
     }
   } else {
-    store_tile<EPI, TO, NCG, NRB, RS, WHOLE8>(e, M, N, mbase, nbase, r0, col, val);
+    store_tile<EPI, TO, NCG, NRB, RS, WHOLE8, POL>(e, M, N, mbase, nbase, r0, col, val);
   }
 }
 
 // 16x16 MFMA tiles: acc[i][j] (i over 16-column W fragments, permuted so that fragments 2a and 2a+1
 // give a lane 8 consecutive columns; j over 16-row A fragments) holds rows mbase + 16 j + fr and
 // columns nbase + 32 a + 8 fq .. + 7 (fr = lane & 15, fq = lane >> 4).
-template <int EPI, typename TO, int WTN, int WTM, int PIPE, bool WHOLE8>
+template <int EPI, typename TO, int WTN, int WTM, int PIPE, bool WHOLE8, int POL = 0>
 __device__ __forceinline__ void tile_epilogue(const EpiArgs &e, const f32x4 (&acc)[WTN][WTM], int M, int N,
                                               int mbase, int nbase, int fr, int fq) {
-  wave_epilogue<EPI, TO, WTN / 2, WTM, 16, PIPE, WHOLE8>(
+  wave_epilogue<EPI, TO, WTN / 2, WTM, 16, PIPE, WHOLE8, POL>(
       e, M, N, mbase, nbase, fr, [&](int cg) { return 32 * cg + 8 * fq; },
       [&](int cg, int rb, int q) { return acc[2 * cg + (q >> 2)][rb][q & 3]; });
 }
@@ -686,7 +697,7 @@ __device__ __forceinline__ void wait_tiles(int n) {
 
 // One (32 WTA) x (64 WT) tile on 8 waves in a 2 (m) x 4 (n) grid of (16 WTA) x (16 WT) wave tiles, K tiles
 // of 64 through an LDS ring of NST stages, each K tile's loads issued NST - 1 tiles ahead.
-template <int EPI, typename TO, int WTA, int WT = 4, int NST = 2>
+template <int EPI, typename TO, int WTA, int WT = 4, int NST = 2, int POL = 0>
 __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__restrict__ A, const bf16 *__restrict__ Wt,
                                           const EpiArgs &e, int m0, int n0, bf16 *smem, int ldk) {
   // K: columns accumulated (K % 64 == 0, K >= 128); ldk: row stride of A and Wt in elements (ldk >= K;
@@ -828,12 +839,12 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   }
   substep(T_{}, F_{}, fw0, fa0, last, 1, fw1, fa1, 0, 0);
   substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
-  tile_epilogue<EPI, TO, WT, WTA, 2, true>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
+  tile_epilogue<EPI, TO, WT, WTA, 2, true, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
 }
 
 // MT row blocks x NT column tiles of 256 on the 8-wave tile; row blocks of two heights as in
 // k_linear_dma.
-template <int EPI, typename TO, int WTA>
+template <int EPI, typename TO, int WTA, int POL = 0>
 __global__ __launch_bounds__(512, 1) void k_linear_dma8(int M, int N, int K, const bf16 *__restrict__ A,
                                                  const bf16 *__restrict__ Wt, EpiArgs e, int MT, int NT, int tall,
                                                  int group_m) {
@@ -845,11 +856,11 @@ __global__ __launch_bounds__(512, 1) void k_linear_dma8(int M, int N, int K, con
   if (m0 >= M) return;   // a block past the last row (a forced plan with more blocks than M needs)
   if constexpr (WTA > 5) {
     if (upto == before) {
-      dma8_tile<EPI, TO, WTA - 1>(M, N, K, A, Wt, e, m0, n0, smem, K);
+      dma8_tile<EPI, TO, WTA - 1, 4, 2, POL>(M, N, K, A, Wt, e, m0, n0, smem, K);
       return;
     }
   }
-  dma8_tile<EPI, TO, WTA>(M, N, K, A, Wt, e, m0, n0, smem, K);
+  dma8_tile<EPI, TO, WTA, 4, 2, POL>(M, N, K, A, Wt, e, m0, n0, smem, K);
 }
 
 // MT x NT tiles of (32 WTA) x (64 WT) on the 8-wave tile with an LDS ring of NST stages: for launches with
@@ -1200,12 +1211,19 @@ template <int EPI, int WTA>
 static hipError_t launch_dma8(int M, int N, int K, const void *A, const void *Wt, const EpiArgs &e, hipStream_t s,
                               int mb, int tall) {
   const size_t lds = (size_t)2 * (32 * WTA + 256) * mf::BK * sizeof(bf16);
-  auto kern = k_linear_dma8<EPI, bf16, WTA>;
-  static bool attr_set = false;
-  if (!attr_set) {
+  // the store policy of a bf16 output by its size (epi::kNTBytes); the fp32 outputs (residual stream and
+  // cache, read back by the next LayerNorm or proxy) keep the default
+  bool nt = false;
+  auto kern = k_linear_dma8<EPI, bf16, WTA, 0>;
+  if constexpr (EPI == EPI_STORE || EPI == EPI_GELU) {
+    nt = (size_t)M * (size_t)e.ldo * sizeof(bf16) >= epi::kNTBytes;
+    if (nt) kern = k_linear_dma8<EPI, bf16, WTA, epi::kStoreNT>;
+  }
+  static bool attr_set[2] = {false, false};
+  if (!attr_set[nt]) {
     hipError_t err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (err != hipSuccess) return err;
-    attr_set = true;
+    attr_set[nt] = true;
   }
   const int NT = (N + 255) / 256;
   hipLaunchKernelGGL(kern, dim3(mb * NT), dim3(512), lds, s, M, N, K, (const bf16 *)A, (const bf16 *)Wt, e, mb, NT,
