@@ -179,14 +179,16 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, POL);
 }
 // Non-temporal (the nt bit): the 8-wave kernel's bf16 output stores (store and GELU epilogues) when the
-// launch's output is at least kNTBytes, so that a round's burst of output lines does not push the next
+// launch's output is at least kNTBytes (64 MiB), so that a round's burst of output lines does not push the next
 // tiles' operands out of L2.  Measured on the 1.3B-shaped pool of 16 (same box, alternating, latents
-// bit-identical): draft 240.7 -> 238.4 ms; with the residual epilogues' fp32 stores non-temporal too 238.9
+// bit-identical): draft 240.7 -> 238.4 ms at a 128 MiB threshold (QKV and MLP up), 247.1 -> 245.7 ms on
+// another box when the threshold also takes cross q's 77 MB; with the residual epilogues' fp32 stores
+// non-temporal too 238.9
 // (the residual projection alone 168 -> 146 us, but the next LayerNorm then reads its rows from further
 // out); with non-temporal stores at every size, one candidate's refinement step (outputs of 10-28 MB, read
 // back from the caches by the next kernel) measured 7.53 -> 7.78 ms, hence the size threshold.
 constexpr int kStoreNT = 2;
-constexpr size_t kNTBytes = (size_t)128 << 20;
+constexpr size_t kNTBytes = (size_t)64 << 20;
 }  // namespace epi
 
 // A wave's output, whatever the MFMA shape, is walked as NCG column groups x NRB row blocks: in row
