@@ -183,10 +183,10 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
 // tiles' operands out of L2.  Measured on the 1.3B-shaped pool of 16 (same box, alternating, latents
 // bit-identical): draft 240.7 -> 238.4 ms at a 128 MiB threshold (QKV and MLP up), 247.1 -> 245.7 ms on
 // another box when the threshold also takes cross q's 77 MB; with the residual epilogues' fp32 stores
-// non-temporal too 238.9
-// (the residual projection alone 168 -> 146 us, but the next LayerNorm then reads its rows from further
-// out); with non-temporal stores at every size, one candidate's refinement step (outputs of 10-28 MB, read
-// back from the caches by the next kernel) measured 7.53 -> 7.78 ms, hence the size threshold.
+// non-temporal too 238.9 (the residual projection alone 168 -> 146 us, but the next LayerNorm then reads
+// its rows from further out); with non-temporal stores at every size, one candidate's refinement step
+// (outputs of 10-28 MB, read back from the caches by the next kernel) measured 7.53 -> 7.78 ms, hence the
+// size threshold.
 constexpr int kStoreNT = 2;
 constexpr size_t kNTBytes = (size_t)64 << 20;
 }  // namespace epi
