@@ -179,8 +179,8 @@ __device__ __forceinline__ void st4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, POL);
 }
 // Non-temporal (the nt bit): the 8-wave kernel's bf16 output stores (store and GELU epilogues) when the
-// launch's output is at least kNTBytes (64 MiB), so that a round's burst of output lines does not push the next
-// tiles' operands out of L2.  Measured on the 1.3B-shaped pool of 16 (same box, alternating, latents
+// launch's output is at least kNTBytes (64 MiB), so that a round's burst of output lines does not push the
+// next tiles' operands out of L2.  Measured on the 1.3B-shaped pool of 16 (same box, alternating, latents
 // bit-identical): draft 240.7 -> 238.4 ms at a 128 MiB threshold (QKV and MLP up), 247.1 -> 245.7 ms on
 // another box when the threshold also takes cross q's 77 MB; with the residual epilogues' fp32 stores
 // non-temporal too 238.9 (the residual projection alone 168 -> 146 us, but the next LayerNorm then reads
@@ -723,7 +723,7 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   // load x of this wave: rows 8 WTA wave + 8 x .. + 7 of A (waves 0-3, x < WTA) or 16 WT (wave - 4) +
   // 8 x .. + 7 of W (waves 4-7, x < 2 WT); lane l -> row + (l >> 3), slot l & 7
   static_assert(NL <= 8, "load slots");
-  uint32_t voff[8];   // (a size that depends on the template arguments fails the host pass of hipcc)
+  uint32_t voff[8];   // a fixed size: hipcc's host pass rejects one that depends on the template arguments
   const int row0 = loads_a ? 8 * WTA * wave : 16 * WT * (wave - 4);
 #pragma unroll
   for (int x = 0; x < NL; ++x) {
