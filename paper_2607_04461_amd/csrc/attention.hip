@@ -126,6 +126,11 @@ constexpr int K_OFF = 0, V_OFF = 2 * TILE_B;
 // zero (the buffer range ends at the last key) and are masked on the ragged last tile.  1-D grid,
 // XCD-aware: workgroups go to the 8 XCDs round-robin by id, so id -> (unit u = head * batch + candidate,
 // query block) keeps every query block of a unit on XCD u % 8, where its K and V stay in that XCD's L2.
+// The normalised output leaves through LDS (the rings are free after a last barrier): a lane holds
+// 16-byte pieces of one query row, so direct stores would write every 128-byte line of the output in
+// several partial pieces; staged, each store instruction writes 4 whole rows.  Measured (same box,
+// outputs bit-identical): cross-attention 110 -> 100 us, self-attention 308-320 -> 299-309 us, the
+// 1.3B-shaped pool's draft 238.9 -> 236.8 ms.
 __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
   using namespace fa2;
   constexpr int RW = KT / WAVES;     // K (V) tile rows each wave loads
@@ -353,6 +358,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
       if (j + 1 < nt) load_v(j + 1, (j + 1) & 1);
       if (j + 2 < nt) load_k(j + 2, j & 1);
     }
+    __syncthreads();   // the output pass's barrier below
     return;
   }
   f32x16 sa[2], sb[2];
@@ -383,16 +389,27 @@ __global__ __launch_bounds__(256, 2) void k_attn_fa(AttnP p) {
   }
   const float ltot = lsum + __shfl_xor(lsum, 32, 64);
   const float inv = 1.0f / ltot;
-  if (q0 + li >= p.tq) return;
-  bf16 *O = (bf16 *)p.out + (int64_t)b * p.o_bs + (int64_t)(q0 + li) * p.o_rs + h * DH;
+  __syncthreads();   // every wave has read its last K and V fragments: the rings are free
+  // the wave's 32 x 128 output block goes through LDS (16-byte chunk c of row r at c ^ (r & 15)), so that
+  // each global store writes 4 whole rows
+  char *ob = lds + w * (QW * DH * 2);
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int jq = 0; jq < 4; ++jq) {
       bf16x4 w4 = {(bf16)(o[dt][4 * jq] * inv), (bf16)(o[dt][4 * jq + 1] * inv),
                    (bf16)(o[dt][4 * jq + 2] * inv), (bf16)(o[dt][4 * jq + 3] * inv)};
-      *reinterpret_cast<bf16x4 *>(O + 32 * dt + 8 * jq + 4 * g) = w4;
+      const int c = 4 * dt + jq;
+      *reinterpret_cast<bf16x4 *>(ob + li * (DH * 2) + ((c ^ (li & 15)) << 4) + 8 * g) = w4;
     }
+  const int cc = lane & 15;
+  bf16 *Ob = (bf16 *)p.out + (int64_t)b * p.o_bs + h * DH + 8 * cc;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = (lane >> 4) + 4 * i;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(ob + r * (DH * 2) + ((cc ^ (r & 15)) << 4));
+    if (q0 + r < p.tq) *reinterpret_cast<u32x4 *>(Ob + (int64_t)(q0 + r) * p.o_rs) = v;
+  }
 }
 
 template <typename T>
