@@ -271,6 +271,78 @@ __device__ __forceinline__ void residual_tile(const EpiArgs &e, int M, int N, in
   }
 }
 
+// Residual update of the 8-wave tile (NCG column groups of 32 per wave, 16 WTA rows) through LDS: for each
+// column group the wave writes its (16 WTA) x 32 fp32 block to a region of its own (16-byte chunk k of
+// row r at k ^ (r & 7)) and reads it back row by row, so that every load of the residual rows, store of
+// the updated rows and cache write covers 8 whole rows x 128 bytes per instruction instead of 16-byte
+// pieces of 16 rows.  Arithmetic as residual_tile (out = in + gate (acc + bias), the same expression per
+// element).  lds: the K-loop's ring, free once every wave is past its last fragment reads (the barrier);
+// a wave reuses its region for the next column group without one, its LDS accesses completing in order.
+// Batches of B read-back rows, the residual loads of batch b + 1 issued before the stores of batch b.
+template <int NCG, int WTA, int CM, int POL>
+__device__ __forceinline__ void residual_staged(const EpiArgs &e, const f32x4 (&acc)[2 * NCG][WTA], int M, int N,
+                                                int mbase, int nbase, int fr, int fq, int lane, int wave,
+                                                char *lds) {
+  using namespace epi;
+  constexpr int R = 16 * WTA;              // rows of the wave's block
+  constexpr int NT = R / 8;                // read-back instructions per column group
+  constexpr int B = NT % 4 == 0 ? 4 : 2;   // rows-sets per batch
+  constexpr int NB = NT / B;
+  char *wl = lds + wave * (R * 32 * 4);
+  const int rows = max(0, min(M - mbase, R));
+  const uint32_t bytes = (uint32_t)rows * (uint32_t)e.ldo * 4u;
+  const __amdgpu_buffer_rsrc_t rsO = rsrc((float *)e.out + (int64_t)mbase * e.ldo, bytes);
+  const __amdgpu_buffer_rsrc_t rsI = rsrc((e.res_in ? e.res_in : (const float *)e.out) + (int64_t)mbase * e.ldo, bytes);
+  const __amdgpu_buffer_rsrc_t rsC = rsrc(CM ? e.cache + (int64_t)mbase * e.ldo : nullptr, CM ? bytes : 0u);
+  const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
+  const __amdgpu_buffer_rsrc_t rsG = rsrc(e.gate, e.gate ? (uint32_t)N * 4u : 0u);
+  const bool has_gate = e.gate != nullptr;
+  const int k = lane & 7, rr = lane >> 3;   // read-back: columns 4 k .. + 3 of row 8 t + rr
+  const uint32_t rstep = 8u * (uint32_t)e.ldo * 4u, r0 = (uint32_t)rr * (uint32_t)e.ldo * 4u;
+  __syncthreads();   // every wave is past its last fragment reads: the ring is free
+#pragma unroll
+  for (int cg = 0; cg < NCG; ++cg) {
+#pragma unroll
+    for (int rb = 0; rb < WTA; ++rb)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const int r = 16 * rb + fr, kk = 2 * fq + hf;   // the lane's columns 8 fq + 4 hf .. + 3 of row r
+        *reinterpret_cast<f32x4 *>(wl + r * 128 + ((kk ^ (r & 7)) << 4)) = acc[2 * cg + hf][rb];
+      }
+    const int n = nbase + 32 * cg + 4 * k;
+    const uint32_t cn = n < N ? (uint32_t)n * 4u : OUT_OF_RANGE;
+    const f32x4 bb = ld4(rsB, cn);
+    const f32x4 gg = has_gate ? ld4(rsG, cn) : f32x4{1.f, 1.f, 1.f, 1.f};
+    f32x4 h[2][B], c[CM == 2 ? 2 : 1][B];
+    auto fetch = [&](int bt, int buf) {
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        const uint32_t off = r0 + (uint32_t)(B * bt + i) * rstep + cn;
+        h[buf][i] = ld4(rsI, off);
+        if constexpr (CM == 2) c[buf][i] = ld4(rsC, off);
+      }
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int bt = 0; bt < NB; ++bt) {
+      const int buf = bt & 1;
+      if (bt + 1 < NB) fetch(bt + 1, buf ^ 1);
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        const int t = B * bt + i, r = 8 * t + rr;
+        const f32x4 a = *reinterpret_cast<const f32x4 *>(wl + r * 128 + ((k ^ (r & 7)) << 4));
+        f32x4 o = h[buf][i];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] += gg[q] * (a[q] + bb[q]);
+        const uint32_t off = r0 + (uint32_t)t * rstep + cn;
+        st4<POL>(rsO, off, o);
+        if constexpr (CM == 1) st4<POL>(rsC, off, o);
+        if constexpr (CM == 2) st4<POL>(rsC, off, o - c[buf][i]);
+      }
+    }
+  }
+}
+
 // Store (bf16 or fp32), GELU-and-store, or fp32 store; bias loaded first, no load between the
 // stores.  WHOLE8: N % 8 == 0, one 16-byte store per 8 bf16 values; else two 8-byte stores.
 template <int EPI, typename TO, int NCG, int NRB, int RS, bool WHOLE8, int POL = 0, typename Col, typename Val>
@@ -841,7 +913,17 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
   }
   substep(T_{}, F_{}, fw0, fa0, last, 1, fw1, fa1, 0, 0);
   substep(F_{}, F_{}, fw1, fa1, 0, 0, fw0, fa0, 0, 0);
-  tile_epilogue<EPI, TO, WT, WTA, 2, true, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
+  if constexpr (EPI == EPI_RESIDUAL && 8 * 16 * WTA * 32 * 4 <= NST * STAGE * 2) {
+    // the ring (NST stages of (32 WTA + 64 WT) x 64 bf16) holds the 8 waves' (16 WTA) x 32 fp32 blocks
+    // (all tiles but 160 x 128 with 2 stages)
+    char *lw = reinterpret_cast<char *>(smem);
+    const int mb = m0 + 16 * WTA * wm, nb = n0 + 16 * WT * wn;
+    if (!e.cache) residual_staged<WT / 2, WTA, 0, POL>(e, acc, M, N, mb, nb, fr, fq, lane, wave, lw);
+    else if (!e.cache_delta) residual_staged<WT / 2, WTA, 1, POL>(e, acc, M, N, mb, nb, fr, fq, lane, wave, lw);
+    else residual_staged<WT / 2, WTA, 2, POL>(e, acc, M, N, mb, nb, fr, fq, lane, wave, lw);
+  } else {
+    tile_epilogue<EPI, TO, WT, WTA, 2, true, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
+  }
 }
 
 // MT row blocks x NT column tiles of 256 on the 8-wave tile; row blocks of two heights as in

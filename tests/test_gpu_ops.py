@@ -85,8 +85,8 @@ def test_linear_small(dtype, M, N, K, epi):
 
 @pytest.mark.parametrize("tile", ["256x256", "128x128", "split:256", "bm:224", "bm:192", "bm:160", "mix:7:3:1",
                                   "mix:8:3:1", "mix:6:4:2", "w8", "w8:bm:160", "w8:mix:7:3:1", "w8:mix:8:3:1",
-                                  "deep:128:128:2", "deep:128:128:3", "deep:160:128:3", "deep:128:256:3",
-                                  "deep:160:256:3"])
+                                  "deep:128:128:2", "deep:128:128:3", "deep:160:128:3", "deep:128:256:2",
+                                  "deep:128:256:3", "deep:160:256:2", "deep:160:256:3"])
 @pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
                                    (520, 776, 1024), (300, 520, 128)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])

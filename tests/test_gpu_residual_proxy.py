@@ -19,9 +19,14 @@ def _gpu():
     flashbon.load()
 
 
-@pytest.mark.parametrize("dtype,tol", [("fp32", 1e-5), ("bf16", 2e-2)])
+@pytest.mark.parametrize("dtype,tol,tile", [("fp32", 1e-5, None), ("bf16", 2e-2, None), ("bf16", 2e-2, "256x256"),
+                                            ("bf16", 2e-2, "w8:bm:224"), ("bf16", 2e-2, "deep:160:256:2")])
 @pytest.mark.parametrize("name", ["tiny", "mid"])
-def test_residual_proxy_trajectory_matches_oracle(name, dtype, tol):
+def test_residual_proxy_trajectory_matches_oracle(name, dtype, tol, tile, monkeypatch):
+    """tile: a forced linear-layer tiling (the 8-wave kernels of 256, 224 and 160 rows), so that the
+    block-delta cache write of the down-projection's residual epilogue runs on each of them."""
+    if tile is not None:
+        monkeypatch.setenv("FLASHBON_LINEAR_TILE", tile)
     from paper_2607_04461_amd.pool import DraftPool
     wl = synth.WORKLOADS[name]
     flat, W = synth.make_weights(wl.shape, wl.seed_w)
