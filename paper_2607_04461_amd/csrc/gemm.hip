@@ -397,6 +397,57 @@ __device__ __forceinline__ void store_tile(const EpiArgs &e, int M, int N, int m
   }
 }
 
+// bf16 store or GELU-and-store of the 8-wave tile with 256-column tiles (2 column groups of 32 per wave)
+// through LDS: the wave writes its (16 WTA) x 64 bf16 block to a region of its own (16-byte chunk k of
+// row r at k ^ (r & 7), rows of 128 bytes) and reads it back so that each store instruction writes 8
+// whole rows x 128 bytes instead of 16 rows x 64 bytes.  Values as store_tile (bias added, GELU, rounded
+// to bf16 before staging).  lds: the K-loop's ring, free once every wave is past its last fragment reads.
+template <int EPI, int WTA, int POL>
+__device__ __forceinline__ void store_staged(const EpiArgs &e, const f32x4 (&acc)[4][WTA], int M, int N, int mbase,
+                                             int nbase, int fr, int fq, int lane, int wave, char *lds) {
+  using namespace epi;
+  constexpr int R = 16 * WTA;
+  char *wl = lds + wave * (R * 128);
+  const int rows = max(0, min(M - mbase, R));
+  const __amdgpu_buffer_rsrc_t rsO = rsrc((bf16 *)e.out + (int64_t)mbase * e.ldo, (uint32_t)rows * (uint32_t)e.ldo * 2u);
+  const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
+  f32x4 b[2][2];
+#pragma unroll
+  for (int cg = 0; cg < 2; ++cg) {
+    const int n = nbase + 32 * cg + 8 * fq;
+    b[cg][0] = ld4(rsB, n < N ? (uint32_t)n * 4u : OUT_OF_RANGE);
+    b[cg][1] = ld4(rsB, n + 4 < N ? (uint32_t)(n + 4) * 4u : OUT_OF_RANGE);
+  }
+  __syncthreads();   // every wave is past its last fragment reads: the ring is free
+#pragma unroll
+  for (int cg = 0; cg < 2; ++cg)
+#pragma unroll
+    for (int rb = 0; rb < WTA; ++rb) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = acc[2 * cg + (q >> 2)][rb][q & 3] + b[cg][q >> 2][q & 3];
+      if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = gelu_tanh(v[q]);
+      }
+      const bf16x8 w = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3], (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+      const int r = 16 * rb + fr, kk = 4 * cg + fq;   // columns 8 kk .. + 7 of row r
+      *reinterpret_cast<bf16x8 *>(wl + r * 128 + ((kk ^ (r & 7)) << 4)) = w;
+      // GELU on 256-row tiles: without a fence the scheduler overlaps enough chunks to spill
+    }
+  const int k = lane & 7, rr = lane >> 3;   // read-back: columns 8 k .. + 7 of row 8 t + rr
+  const int n = nbase + 8 * k;
+  const uint32_t cn = n < N ? (uint32_t)n * 2u : OUT_OF_RANGE;   // N % 8 == 0: a chunk is in or out whole
+  const uint32_t rstep = 8u * (uint32_t)e.ldo * 2u, r0 = (uint32_t)rr * (uint32_t)e.ldo * 2u;
+#pragma unroll
+  for (int t = 0; t < R / 8; ++t) {
+    const int r = 8 * t + rr;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(wl + r * 128 + ((k ^ (r & 7)) << 4));
+    __builtin_amdgcn_raw_buffer_store_b128(v, rsO, cn == OUT_OF_RANGE ? OUT_OF_RANGE : r0 + (uint32_t)t * rstep + cn, 0,
+                                           POL);
+  }
+}
+
 // The epilogue of a wave's output for every epilogue kind, on the group/block walk above.  PIPE:
 // residual rows fetched one batch ahead (2) or per batch (1), by the kernel's register budget.
 template <int EPI, typename TO, int NCG, int NRB, int RS, int PIPE, bool WHOLE8, int POL = 0, typename Col, typename Val>
@@ -921,6 +972,10 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
     if (!e.cache) residual_staged<WT / 2, WTA, 0, POL>(e, acc, M, N, mb, nb, fr, fq, lane, wave, lw);
     else if (!e.cache_delta) residual_staged<WT / 2, WTA, 1, POL>(e, acc, M, N, mb, nb, fr, fq, lane, wave, lw);
     else residual_staged<WT / 2, WTA, 2, POL>(e, acc, M, N, mb, nb, fr, fq, lane, wave, lw);
+  } else if constexpr ((EPI == EPI_STORE || EPI == EPI_GELU) && sizeof(TO) == 2 && WT == 4 &&
+                       8 * 16 * WTA * 128 <= NST * STAGE * 2) {
+    store_staged<EPI, WTA, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq, lane, wave,
+                                reinterpret_cast<char *>(smem));
   } else {
     tile_epilogue<EPI, TO, WT, WTA, 2, true, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
   }

@@ -125,11 +125,13 @@ def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
     assert rel_l2(out.float().cpu().numpy(), ref) <= tol
 
 
-@pytest.mark.parametrize("epi", ["store", "residual"])
+@pytest.mark.parametrize("epi", ["store", "store_bf16", "gelu", "residual"])
 def test_linear_tile_plans_bit_identical(epi, monkeypatch):
     """Every tiling accumulates K in the same order, so an output element does not depend on the tile
     that computed it: all plans give bit-identical results (this is what keeps a candidate's draft
-    independent of its position in the pool)."""
+    independent of its position in the pool).  The bf16 store and GELU epilogues of the 256-column
+    8-wave tiles and every residual epilogue of the 8-wave tiles pass through LDS; the 4-wave kernels'
+    do not, so the comparison also pins the staged epilogues to the direct ones."""
     F = fb()
     M, N, K = 1100, 776, 512
     A = _dev(_operand((M, K), 81, "bf16"), "bf16")
@@ -146,6 +148,9 @@ def test_linear_tile_plans_bit_identical(epi, monkeypatch):
         if epi == "store":
             out = torch.empty((M, N), device="cuda", dtype=torch.float32)
             F.flashbon_op_linear(F.BF16, M, N, K, A, W, bias, F.EPI_STORE_F32, out)
+        elif epi in ("store_bf16", "gelu"):
+            out = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+            F.flashbon_op_linear(F.BF16, M, N, K, A, W, bias, F.EPI_STORE if epi == "store_bf16" else F.EPI_GELU, out)
         else:
             out = h0.clone()
             F.flashbon_op_linear(F.BF16, M, N, K, A, W, bias, F.EPI_RESIDUAL, out, gate)
