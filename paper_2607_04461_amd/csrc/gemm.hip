@@ -448,6 +448,46 @@ __device__ __forceinline__ void store_staged(const EpiArgs &e, const f32x4 (&acc
   }
 }
 
+// fp32 store of the 8-wave tile (the K ranges' partial sums of a split-K launch) through LDS, as
+// residual_staged without the residual: per column group the wave's (16 WTA) x 32 block goes to its LDS
+// region and back so that each store instruction writes 8 whole rows x 128 bytes.  out = acc + bias.
+template <int NCG, int WTA, int POL>
+__device__ __forceinline__ void store_staged_f32(const EpiArgs &e, const f32x4 (&acc)[2 * NCG][WTA], int M, int N,
+                                                 int mbase, int nbase, int fr, int fq, int lane, int wave,
+                                                 char *lds) {
+  using namespace epi;
+  constexpr int R = 16 * WTA;
+  char *wl = lds + wave * (R * 32 * 4);
+  const int rows = max(0, min(M - mbase, R));
+  const __amdgpu_buffer_rsrc_t rsO = rsrc((float *)e.out + (int64_t)mbase * e.ldo, (uint32_t)rows * (uint32_t)e.ldo * 4u);
+  const __amdgpu_buffer_rsrc_t rsB = rsrc(e.bias, e.bias ? (uint32_t)N * 4u : 0u);
+  const int k = lane & 7, rr = lane >> 3;   // read-back: columns 4 k .. + 3 of row 8 t + rr
+  const uint32_t rstep = 8u * (uint32_t)e.ldo * 4u, r0 = (uint32_t)rr * (uint32_t)e.ldo * 4u;
+  __syncthreads();   // every wave is past its last fragment reads: the ring is free
+#pragma unroll
+  for (int cg = 0; cg < NCG; ++cg) {
+#pragma unroll
+    for (int rb = 0; rb < WTA; ++rb)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const int r = 16 * rb + fr, kk = 2 * fq + hf;
+        *reinterpret_cast<f32x4 *>(wl + r * 128 + ((kk ^ (r & 7)) << 4)) = acc[2 * cg + hf][rb];
+      }
+    const int n = nbase + 32 * cg + 4 * k;
+    const uint32_t cn = n < N ? (uint32_t)n * 4u : OUT_OF_RANGE;
+    const f32x4 bb = ld4(rsB, cn);
+#pragma unroll
+    for (int t = 0; t < R / 8; ++t) {
+      const int r = 8 * t + rr;
+      const f32x4 a = *reinterpret_cast<const f32x4 *>(wl + r * 128 + ((k ^ (r & 7)) << 4));
+      f32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = a[q] + bb[q];
+      st4<POL>(rsO, cn == OUT_OF_RANGE ? OUT_OF_RANGE : r0 + (uint32_t)t * rstep + cn, o);
+    }
+  }
+}
+
 // The epilogue of a wave's output for every epilogue kind, on the group/block walk above.  PIPE:
 // residual rows fetched one batch ahead (2) or per batch (1), by the kernel's register budget.
 template <int EPI, typename TO, int NCG, int NRB, int RS, int PIPE, bool WHOLE8, int POL = 0, typename Col, typename Val>
@@ -976,6 +1016,9 @@ __device__ __forceinline__ void dma8_tile(int M, int N, int K, const bf16 *__res
                        8 * 16 * WTA * 128 <= NST * STAGE * 2) {
     store_staged<EPI, WTA, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq, lane, wave,
                                 reinterpret_cast<char *>(smem));
+  } else if constexpr (EPI == EPI_STORE_F32 && 8 * 16 * WTA * 32 * 4 <= NST * STAGE * 2) {
+    store_staged_f32<WT / 2, WTA, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq, lane, wave,
+                                       reinterpret_cast<char *>(smem));
   } else {
     tile_epilogue<EPI, TO, WT, WTA, 2, true, POL>(e, acc, M, N, m0 + 16 * WTA * wm, n0 + 16 * WT * wn, fr, fq);
   }
