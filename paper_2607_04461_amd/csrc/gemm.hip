@@ -9,7 +9,10 @@
 //     ring, for launches that fit one round of workgroups one per CU (one or two candidates); K
 //     tiles of 64 in double-buffered, XOR-swizzled LDS; XCD-aware grouped tile order.  Operands are swapped (the weight tile feeds the MFMA "A" side) and the weight rows
 //     permuted so that every lane owns 8 consecutive output columns of one row.  Every kernel
-//     accumulates K in the same order, so an output element does not depend on the tiling.
+//     accumulates K in the same order, so an output element does not depend on the tiling.  The
+//     8-wave tiles' epilogues (bf16 store and GELU of 256-column tiles, residual updates, split-K
+//     partial sums) pass each wave's block through the freed LDS ring so that every global access
+//     covers whole 128-byte rows.
 //   * k_linear_valu: fp32 (or bf16) operands on the vector ALUs, 64x64 tiles; used by the fp32 mode
 //     and for shapes the MFMA tiling does not take.
 #include <cmath>
