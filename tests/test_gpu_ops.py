@@ -349,7 +349,7 @@ def test_attention_full_shapes_bf16_sampled_queries(B, heads, T, tk):
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 @pytest.mark.parametrize("M,D,mod", [(37, 64, True), (24960, 1536, True), (300, 5120, False), (5, 256, False),
                                      (23, 1000, True), (9, 68, True), (1, 4096, True), (2, 8, False),
-                                     (4097, 1536, False)])
+                                     (4097, 1536, False), (4099, 1536, True)])
 def test_ln_mod(dtype, M, D, mod):
     F = fb()
     dt = F.BF16 if dtype == "bf16" else F.FP32
@@ -364,6 +364,23 @@ def test_ln_mod(dtype, M, D, mod):
     if mod:
         ref = ref * (1 + sc) + sh
     assert rel_l2(out.float().cpu().numpy(), ref) <= (6e-3 if dtype == "bf16" else 2e-6)
+
+
+@pytest.mark.parametrize("M", [5000, 24960])
+def test_ln_mod_row_loop_matches_per_row_kernel(M):
+    """The modulated bf16 LayerNorm of many rows (D = 1536, M >= 4096: each wave loops over rows with the
+    modulation in registers) gives the same bits as the one-row-per-wave kernel that a launch of fewer
+    rows takes, on the same rows."""
+    F = fb()
+    D, m = 1536, 1000
+    x = _dev(synth.random_matrix((M, D), 54) * 3 + 1, "fp32")
+    sh, sc = _dev(synth.random_matrix((D,), 55), "fp32"), _dev(synth.random_matrix((D,), 56), "fp32")
+    many = torch.empty((M, D), device="cuda", dtype=torch.bfloat16)
+    few = torch.empty((m, D), device="cuda", dtype=torch.bfloat16)
+    F.flashbon_op_ln_mod(F.BF16, M, D, 1e-6, x, sh, sc, many)
+    F.flashbon_op_ln_mod(F.BF16, m, D, 1e-6, x[M - m:].contiguous(), sh, sc, few)
+    torch.cuda.synchronize()
+    assert torch.equal(many[M - m:], few)
 
 
 @pytest.mark.parametrize("count", [38_338_560, 1001])
