@@ -74,85 +74,6 @@ __global__ __launch_bounds__(256) void k_ln_mod(int M, int D, float eps, const f
 
 constexpr size_t kNTLoadBytes = (size_t)128 << 20;
 
-// The same LayerNorm with modulation for the pool's launches: each wave keeps (1 + scale) and shift in
-// registers and takes rows w, w + waves, w + 2 waves, .. (waves: the resident waves of the launch), two
-// rows' loads in flight at a time, so the modulation is read once per wave instead of once per row.  Per
-// element the same operations as k_ln_mod, so the output is bit-identical.  At 24960 x 1536 (fp32 rows
-// in, bf16 out, same box, alternating): 42.1-42.5 us per launch with k_ln_mod, 40.5-40.6 with one row in
-// flight, 39.4-39.9 with two.
-template <typename T, int NV, bool NT>
-__global__ __launch_bounds__(256) void k_ln_mod_rows(int M, int D, float eps, const float *__restrict__ x,
-                                                     const float *__restrict__ shift,
-                                                     const float *__restrict__ scale, T *__restrict__ out,
-                                                     int waves) {
-  const int lane = threadIdx.x & 63;
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int nv = D >> 2;
-  float4 sh[NV], sc[NV];
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      sh[i] = reinterpret_cast<const float4 *>(shift)[c];
-      const float4 t = reinterpret_cast<const float4 *>(scale)[c];
-      sc[i] = make_float4(1.0f + t.x, 1.0f + t.y, 1.0f + t.z, 1.0f + t.w);
-    }
-  }
-  auto load_row = [&](int64_t row, float4 (&v)[NV]) {
-    const float4 *xr = reinterpret_cast<const float4 *>(x + row * D);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int c = lane + i * 64;
-      if (c >= nv || row >= M) {
-        v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-      } else if constexpr (NT) {
-        const f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(xr) + c);
-        v[i] = make_float4(t[0], t[1], t[2], t[3]);
-      } else {
-        v[i] = xr[c];
-      }
-    }
-  };
-  auto finish = [&](int64_t row, const float4 (&v)[NV]) {
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
-    const float mean = wave_sum(s) / (float)D;
-    float q = 0.f;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int c = lane + i * 64;
-      if (c < nv) {
-        const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
-        q += (a * a + b * b) + (cc * cc + d * d);
-      }
-    }
-    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
-    T *orow = out + row * D;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int c = lane + i * 64;
-      if (c < nv) {
-        const float r0 = (v[i].x - mean) * rstd * sc[i].x + sh[i].x, r1 = (v[i].y - mean) * rstd * sc[i].y + sh[i].y;
-        const float r2 = (v[i].z - mean) * rstd * sc[i].z + sh[i].z, r3 = (v[i].w - mean) * rstd * sc[i].w + sh[i].w;
-        if constexpr (sizeof(T) == 4) {
-          reinterpret_cast<float4 *>(orow)[c] = make_float4(r0, r1, r2, r3);
-        } else {
-          const bf16x4 o4 = {(bf16)r0, (bf16)r1, (bf16)r2, (bf16)r3};
-          reinterpret_cast<bf16x4 *>(orow)[c] = o4;
-        }
-      }
-    }
-  };
-  for (int64_t row = w; row < M; row += 2 * (int64_t)waves) {
-    float4 va[NV], vb[NV];
-    load_row(row, va);
-    load_row(row + waves, vb);
-    finish(row, va);
-    if (row + waves < M) finish(row + waves, vb);
-  }
-}
-
 template <typename T, bool NT>
 static hipError_t launch_ln_t(int M, int D, float eps, const float *x, const float *shift,
                               const float *scale, void *out, hipStream_t s) {
@@ -175,30 +96,8 @@ static hipError_t launch_ln_t(int M, int D, float eps, const float *x, const flo
   return hipGetLastError();
 }
 
-// k_ln_mod_rows for the modulated bf16 LayerNorm of D = 1536 (six float4 per lane) over many rows: as
-// many workgroups as are resident at once, rows taken in a stride over the launch's waves.
-static hipError_t launch_ln_rows(int M, int D, float eps, const float *x, const float *shift, const float *scale,
-                                 void *out, bool nt, hipStream_t s) {
-  auto kern = nt ? k_ln_mod_rows<bf16, 6, true> : k_ln_mod_rows<bf16, 6, false>;
-  static int per_cu[2] = {0, 0}, cus = 0;
-  if (!per_cu[nt]) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[nt], (const void *)kern, 256, 0);
-    if (e != hipSuccess) return e;
-    if (per_cu[nt] < 1) per_cu[nt] = 1;
-  }
-  const int64_t want = (int64_t)cus * per_cu[nt], need = ((int64_t)M + 3) / 4;
-  const int grid = (int)std::min(want, need);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, M, D, eps, x, shift, scale, (bf16 *)out, grid * 4);
-  return hipGetLastError();
-}
-
 hipError_t launch_ln_mod(ActType t, int M, int D, float eps, const float *x, const float *shift,
                          const float *scale, void *out, hipStream_t s) {
-  if (t == ACT_BF16 && shift && D == 1536 && M >= 4096)
-    return launch_ln_rows(M, D, eps, x, shift, scale, out, (size_t)M * (size_t)D * sizeof(float) >= kNTLoadBytes, s);
   if (t == ACT_BF16) {
     if ((size_t)M * (size_t)D * sizeof(float) >= kNTLoadBytes)
       return launch_ln_t<bf16, true>(M, D, eps, x, shift, scale, out, s);

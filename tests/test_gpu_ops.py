@@ -366,23 +366,6 @@ def test_ln_mod(dtype, M, D, mod):
     assert rel_l2(out.float().cpu().numpy(), ref) <= (6e-3 if dtype == "bf16" else 2e-6)
 
 
-@pytest.mark.parametrize("M", [5000, 24960])
-def test_ln_mod_row_loop_matches_per_row_kernel(M):
-    """The modulated bf16 LayerNorm of many rows (D = 1536, M >= 4096: each wave loops over rows with the
-    modulation in registers) gives the same bits as the one-row-per-wave kernel that a launch of fewer
-    rows takes, on the same rows."""
-    F = fb()
-    D, m = 1536, 1000
-    x = _dev(synth.random_matrix((M, D), 54) * 3 + 1, "fp32")
-    sh, sc = _dev(synth.random_matrix((D,), 55), "fp32"), _dev(synth.random_matrix((D,), 56), "fp32")
-    many = torch.empty((M, D), device="cuda", dtype=torch.bfloat16)
-    few = torch.empty((m, D), device="cuda", dtype=torch.bfloat16)
-    F.flashbon_op_ln_mod(F.BF16, M, D, 1e-6, x, sh, sc, many)
-    F.flashbon_op_ln_mod(F.BF16, m, D, 1e-6, x[M - m:].contiguous(), sh, sc, few)
-    torch.cuda.synchronize()
-    assert torch.equal(many[M - m:], few)
-
-
 @pytest.mark.parametrize("count", [38_338_560, 1001])
 @pytest.mark.parametrize("order", [0, 1, 2])
 def test_proxy_kernel(count, order):
