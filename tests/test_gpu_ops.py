@@ -88,7 +88,7 @@ def test_linear_small(dtype, M, N, K, epi):
                                   "deep:128:128:2", "deep:128:128:3", "deep:160:128:3", "deep:128:256:2",
                                   "deep:128:256:3", "deep:160:256:2", "deep:160:256:3"])
 @pytest.mark.parametrize("M,N,K", [(200, 136, 72), (517, 300, 640), (256, 256, 64), (1, 4, 8), (300, 520, 192),
-                                   (520, 776, 1024), (300, 520, 128)])
+                                   (520, 776, 1024), (300, 520, 128), (1, 8, 128), (33, 264, 128)])
 @pytest.mark.parametrize("epi", ["gelu", "residual"])
 def test_linear_each_tile_kernel(tile, M, N, K, epi, monkeypatch):
     """Every MFMA tiling (forced: "256x256" is the 8-wave kernel with LDS-writing loads when K % 64 == 0
